@@ -1,0 +1,426 @@
+"""fp64 NumPy oracle of the split LM head, its payload encoding and verification.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): the HIP library never
+imports, links or runs anything from here.
+
+Notation follows the paper (Section 5.4): the hidden state h' is the
+concatenation of h_end (the first D_end dimensions, kept on the endpoint) and
+h_cloud (the remaining D_cloud dimensions); the LM-head weight is split the
+same way, W_lm = [W_end; W_cloud] (eq. 10).  Weights are stored vocab-major
+here, i.e. row v of an array is column v of the paper's D x V matrix.  S is
+the language-restricted vocabulary subset V_l, a strictly ascending id list.
+
+Readings where the paper is silent (each is listed with its justification in
+the design notes of the repository):
+
+* clipping is a symmetric clamp of the cloud partial logits to [-c, c];
+* the b-bit quantiser Q_b of eq. 18 is per-row symmetric int8 with a dynamic
+  scale s = amax/127, codes in [-127, 127], round-half-to-even, computed with
+  correctly rounded fp32 division;
+* dequantisation and fusion are one fp32 rounding of q*s + z_end;
+* greedy ties go to the lowest vocabulary id;
+* sampling uses top-p nucleus selection on top of eq. 15, with the draw made
+  by inverse CDF in ascending id order from a Philox4x32-10 uniform;
+* draft r of a session is judged by verification row r (prefix match).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# exact input decodings
+# ---------------------------------------------------------------------------
+
+
+def decode_bf16(bits) -> np.ndarray:
+    """bf16 bit patterns -> exact fp64 values (a bf16 is the top half of an fp32).
+
+    Pinned by: torch.bfloat16 -> float32 conversion of every bit pattern.
+    """
+    u = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u.view(np.float32).astype(np.float64)
+
+
+def decode_e4m3(codes) -> np.ndarray:
+    """OCP 8-bit floating point, E4M3 variant -> exact fp64 values.
+
+    Layout: 1 sign bit, 4 exponent bits (bias 7), 3 mantissa bits; exponent
+    field 0 encodes subnormals m/8 * 2^-6; S.1111.111 is NaN; there is no
+    infinity, so the largest finite magnitude is 1.75 * 2^8 = 448.
+    Pinned by: torch.float8_e4m3fn -> float32 on all 256 codes.
+    """
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = (c & 0x7).astype(np.float64)
+    normal = (1.0 + m / 8.0) * np.exp2(e.astype(np.float64) - 7.0)
+    sub = (m / 8.0) * 2.0 ** -6
+    val = sign * np.where(e == 0, sub, normal)
+    return np.where((e == 15) & ((c & 0x7) == 7), np.nan, val)
+
+
+def _cloud_rows_f64(ids, w_cloud_bits=None, w_cloud_codes=None, w_cloud_scale=None):
+    """Decoded cloud weight rows W_cloud[ids] in fp64 (vocab-major)."""
+    if w_cloud_bits is not None:
+        return decode_bf16(w_cloud_bits[ids])
+    w = decode_e4m3(w_cloud_codes[ids])
+    return w * np.asarray(w_cloud_scale, dtype=np.float32)[ids].astype(np.float64)[:, None]
+
+
+def _to_f32(x64: np.ndarray) -> np.ndarray:
+    return np.asarray(x64, dtype=np.float64).astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# eq. 9: the unsplit head (used only to pin the split)
+# ---------------------------------------------------------------------------
+
+
+def full_head_logits(h_bits, w_full_f64, bias=None) -> np.ndarray:
+    """z = h' W_lm + b over the whole vocabulary, fp64 (eq. 9).
+
+    ``w_full_f64`` is the complete weight [V, D] in fp64 (vocab-major).
+    Brute force, small shapes only.
+    """
+    H = decode_bf16(h_bits)
+    z = H @ np.asarray(w_full_f64, dtype=np.float64).T
+    if bias is not None:
+        z = z + np.asarray(bias, dtype=np.float32).astype(np.float64)[None, :]
+    return z
+
+
+# ---------------------------------------------------------------------------
+# eq. 12 restricted to S: the cloud partial
+# ---------------------------------------------------------------------------
+
+
+def cloud_partial_logits(h_bits, d_end, subset, w_cloud_bits=None, w_cloud_codes=None,
+                         w_cloud_scale=None, bias=None, rows=None, with_abs=False,
+                         chunk=4096):
+    """z_cloud[m, j] = fp32( sum_i h_cloud[m, i] * W_cloud[S_j, i] (+ b[S_j]) ).
+
+    Eq. 12 evaluated only on the subset ids (Section 5.4: the cloud returns
+    z_cloud[V_l]).  The bias is added here, on the cloud side, and nowhere
+    else, so it is applied exactly once.  For fp8 weights each vocabulary
+    row is decode(code) * row_scale.  The dot products are accumulated in
+    fp64 (a BLAS matmul) and rounded once to fp32.
+
+    Returns (z fp32 [M, n], absdot fp64 [M, n] or None) where absdot is
+    sum_i |h_i * w_i| (+ |b|), the scale of the fp32 tolerance.
+    Pinned by: the split identity against the unsplit head (eq. 9-13), the
+    d_end = 0 case against torch.nn.functional.linear, the worked example.
+    """
+    h_bits = np.asarray(h_bits)
+    if rows is not None:
+        h_bits = h_bits[np.asarray(rows)]
+    H = decode_bf16(h_bits[:, d_end:])
+    subset = np.asarray(subset, dtype=np.int64)
+    n = subset.size
+    z = np.empty((H.shape[0], n), dtype=np.float32)
+    absdot = np.empty((H.shape[0], n), dtype=np.float64) if with_abs else None
+    for j0 in range(0, n, chunk):
+        ids = subset[j0:j0 + chunk]
+        W = _cloud_rows_f64(ids, w_cloud_bits, w_cloud_codes, w_cloud_scale)
+        acc = H @ W.T
+        if bias is not None:
+            acc = acc + np.asarray(bias, dtype=np.float32)[ids].astype(np.float64)[None, :]
+        z[:, j0:j0 + len(ids)] = _to_f32(acc)
+        if with_abs:
+            a = np.abs(H) @ np.abs(W).T
+            if bias is not None:
+                a = a + np.abs(np.asarray(bias, dtype=np.float32)[ids].astype(np.float64))[None, :]
+            absdot[:, j0:j0 + len(ids)] = a
+    return z, absdot
+
+
+def clip_quantize(z, clip_c):
+    """Clip the cloud partial logits and quantise each row to int8.
+
+    Section 5.4 returns z_cloud[V_l] "after clipping, quantization and
+    encryption"; eq. 18 writes the quantiser as q = Q_b(r) with b = 8 for
+    logits (Section 7.3).  Reading (the paper fixes neither the clip nor
+    Q_b):
+        y = clamp(z, -c, c)                  (fp32)
+        a = max_j |y_j|                      (exact)
+        s = fp32(a / 127), s = 0 if a = 0    (correctly rounded)
+        t = fp32(y / s)                      (correctly rounded)
+        q = clamp(rint_half_even(t), -127, 127), q = 0 if s = 0
+    Returns dict(y, amax, scale, t, q).
+    Pinned by: |q*s - y| <= s/2, the code at argmax|y| is +-127, a clipped
+    row has s = fp32(30/127), a zero row has s = q = 0, the worked example.
+    """
+    z = np.asarray(z, dtype=np.float32)
+    c = np.float32(clip_c)
+    y = np.minimum(np.maximum(z, -c), c)
+    if y.shape[1] == 0:
+        amax = np.zeros(y.shape[0], dtype=np.float32)
+    else:
+        amax = np.abs(y).max(axis=1).astype(np.float32)
+    scale = (amax / np.float32(127.0)).astype(np.float32)
+    pos = scale > 0
+    t = np.zeros_like(y)
+    np.divide(y, scale[:, None], out=t, where=pos[:, None])
+    q = np.clip(np.rint(t), -127, 127).astype(np.int8)
+    q[~pos] = 0
+    return {"y": y, "amax": amax, "scale": scale, "t": t, "q": q}
+
+
+# ---------------------------------------------------------------------------
+# eq. 11 restricted to S: the endpoint partial
+# ---------------------------------------------------------------------------
+
+
+def endpoint_partial_logits(h_bits, d_end, subset, w_end_bits, rows=None, with_abs=False,
+                            chunk=8192):
+    """z_end[m, j] = fp32( sum_{i < D_end} h_end[m, i] * W_end[S_j, i] ).
+
+    Eq. 11 evaluated on the subset ids (Section 5.4, the endpoint computes
+    the matching local component z_end[V_l]; Algorithm 1, first step of the
+    decoding loop).  fp64 accumulation, one rounding to fp32.  D_end = 0
+    gives zeros.  Returns (z_end fp32 [M, n], absdot or None).
+    Pinned by: the split identity and the worked example.
+    """
+    h_bits = np.asarray(h_bits)
+    if rows is not None:
+        h_bits = h_bits[np.asarray(rows)]
+    H = decode_bf16(h_bits[:, :d_end])
+    subset = np.asarray(subset, dtype=np.int64)
+    n = subset.size
+    z = np.zeros((H.shape[0], n), dtype=np.float32)
+    absdot = np.zeros((H.shape[0], n), dtype=np.float64) if with_abs else None
+    if d_end == 0:
+        return z, absdot
+    for j0 in range(0, n, chunk):
+        ids = subset[j0:j0 + chunk]
+        W = decode_bf16(np.asarray(w_end_bits)[ids])
+        z[:, j0:j0 + len(ids)] = _to_f32(H @ W.T)
+        if with_abs:
+            absdot[:, j0:j0 + len(ids)] = np.abs(H) @ np.abs(W).T
+    return z, absdot
+
+
+# ---------------------------------------------------------------------------
+# eq. 13-14: dequantise, fuse, mask
+# ---------------------------------------------------------------------------
+
+
+def round_sum_to_f32(a, b) -> np.ndarray:
+    """fp32 nearest (ties to even) to the exact sum a + b of fp64 values.
+
+    The fp64 sum s = a + b may itself be rounded; TwoSum recovers the exact
+    error e with s + e = a + b.  Rounding s to fp32 is then wrong only when
+    s sits exactly halfway between two fp32 values and e != 0, in which case
+    the exact sum lies on the side of e.
+    Pinned by: exact rational arithmetic (fractions.Fraction) in a test.
+    """
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    s = a + b
+    bb = s - a
+    e = (a - (s - bb)) + (b - bb)
+    r = s.astype(np.float32)
+    r64 = r.astype(np.float64)
+    toward = np.where(s > r64, np.float32(np.inf), np.float32(-np.inf)).astype(np.float32)
+    other = np.nextafter(r, toward)
+    mid = (r64 + other.astype(np.float64)) * 0.5
+    tie = (s != r64) & (s == mid) & (e != 0)
+    up = np.maximum(r, other)
+    down = np.minimum(r, other)
+    return np.where(tie, np.where(e > 0, up, down), r).astype(np.float32)
+
+
+def fuse_masked(q, scale, z_end) -> np.ndarray:
+    """f[m, j] = fp32(q[m, j] * s_m + z_end[m, j]) for j in S (eq. 13-14).
+
+    The payload is dequantised as q * s (exact in fp64) and added to the
+    endpoint partial with a single rounding.  Ids outside S carry -inf in
+    eq. 14; they are simply absent here, so they can never be selected.
+    """
+    q = np.asarray(q, dtype=np.int8).astype(np.float64)
+    s = np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
+    return round_sum_to_f32(q * s, np.asarray(z_end, dtype=np.float32).astype(np.float64))
+
+
+# ---------------------------------------------------------------------------
+# selection
+# ---------------------------------------------------------------------------
+
+
+def greedy_select(f, subset):
+    """Greedy token per row: the subset id with the largest fused logit.
+
+    The zero-temperature limit of eq. 15 (Algorithm 1: the endpoint picks
+    y_t from the fused, masked logits).  Ties go to the lowest id, which is
+    the lowest subset position because S is ascending.  Also returns the gap
+    between the best and the runner-up logit (0 on a tie, inf for |S| = 1).
+    """
+    f = np.asarray(f, dtype=np.float32)
+    pos = np.argmax(f, axis=1)
+    best = f[np.arange(f.shape[0]), pos].astype(np.float64)
+    if f.shape[1] > 1:
+        g = f.astype(np.float64).copy()
+        g[np.arange(f.shape[0]), pos] = -np.inf
+        gap = best - g.max(axis=1)
+    else:
+        gap = np.full(f.shape[0], np.inf)
+    return np.asarray(subset, dtype=np.int32)[pos], pos, gap
+
+
+_PHILOX_M0 = 0xD2511F53
+_PHILOX_M1 = 0xCD9E8D57
+_PHILOX_W0 = 0x9E3779B9
+_PHILOX_W1 = 0xBB67AE85
+_MASK32 = 0xFFFFFFFF
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11).
+
+    Each round multiplies words 0 and 2 by the two round constants, keeps
+    the 64-bit products' high and low halves, and permutes:
+        (c0, c1, c2, c3) -> (hi(M1*c2) ^ c1 ^ k0, lo(M1*c2),
+                             hi(M0*c0) ^ c3 ^ k1, lo(M0*c0))
+    with the key bumped by the Weyl constants between rounds.
+    Pinned by: the published known-answer vectors of Philox4x32-10.
+    """
+    c0, c1, c2, c3 = (int(x) & _MASK32 for x in ctr)
+    k0, k1 = (int(x) & _MASK32 for x in key)
+    for rnd in range(10):
+        if rnd:
+            k0 = (k0 + _PHILOX_W0) & _MASK32
+            k1 = (k1 + _PHILOX_W1) & _MASK32
+        p0 = _PHILOX_M0 * c0
+        p1 = _PHILOX_M1 * c2
+        c0, c1, c2, c3 = ((p1 >> 32) ^ c1 ^ k0, p1 & _MASK32,
+                          (p0 >> 32) ^ c3 ^ k1, p0 & _MASK32)
+    return c0, c1, c2, c3
+
+
+def philox_uniform(seed: int, row_in_session: int, session: int) -> float:
+    """u in [0, 1) for one verification row: the top 24 bits of word 0 of
+    Philox4x32-10 with key (lo32(seed), hi32(seed)) and counter
+    (row, session, 0, 0), times 2^-24 (exact in fp32 and fp64)."""
+    seed = int(seed) & 0xFFFFFFFFFFFFFFFF
+    x0 = philox4x32_10((row_in_session, session, 0, 0), (seed & _MASK32, seed >> 32))[0]
+    return (x0 >> 8) * 2.0 ** -24
+
+
+def sample_select(f, subset, temperature, top_p, seed, rows_per_session):
+    """Temperature + top-p sample per row (eq. 15 with a nucleus cut).
+
+    p = softmax(f / tau) over S in fp64.  Order S by (p desc, id asc); the
+    nucleus N is the shortest prefix of that order whose mass reaches top_p
+    (all of S when top_p >= 1; never empty).  With u from ``philox_uniform``
+    and target = u * mass(N), walk N in ascending id order and take the
+    first member whose running mass exceeds the target (the last member if
+    rounding leaves none).
+
+    Returns (tokens int32 [M], info) where info holds, per row, the nucleus
+    size, the distance of top_p from the two cumulative masses around the cut
+    (inf without a cut) and the distance of the target from the nearest
+    boundary of the chosen member's CDF interval, both in probability units.
+    Pinned by: tau -> 0 and top_p -> 0 reduce to the greedy pick, a chi-square
+    test of the draws against the exact softmax, a hand-made nucleus.
+    """
+    f = np.asarray(f, dtype=np.float32)
+    subset = np.asarray(subset, dtype=np.int64)
+    M, n = f.shape
+    tau = float(np.float32(temperature))
+    tp = float(np.float32(top_p))
+    tokens = np.empty(M, dtype=np.int32)
+    ksize = np.empty(M, dtype=np.int64)
+    cut_margin = np.empty(M)
+    cdf_margin = np.empty(M)
+    for m in range(M):
+        x = f[m].astype(np.float64)
+        e = np.exp((x - x.max()) / tau)
+        p = e / e.sum()
+        order = np.lexsort((subset, -p))          # p descending, then id ascending
+        cum = np.cumsum(p[order])
+        if tp >= 1.0:
+            K = n
+            cut_margin[m] = np.inf
+        else:
+            K = min(int(np.searchsorted(cum, tp, side="left")) + 1, n)
+            above = cum[K - 1] - tp
+            below = tp - cum[K - 2] if K >= 2 else np.inf
+            cut_margin[m] = min(above, below)
+        ksize[m] = K
+        members = np.sort(order[:K])              # positions in S, ascending id
+        run = np.cumsum(p[members])
+        mass = run[-1]
+        u = philox_uniform(seed, m % rows_per_session, m // rows_per_session)
+        target = u * mass
+        hit = np.flatnonzero(run > target)
+        i = int(hit[0]) if hit.size else K - 1
+        before = run[i - 1] if i > 0 else 0.0
+        cdf_margin[m] = min(target - before, run[i] - target)
+        tokens[m] = subset[members[i]]
+    return tokens, {"nucleus": ksize, "cut_margin": cut_margin, "cdf_margin": cdf_margin}
+
+
+# ---------------------------------------------------------------------------
+# verification of the drafts (Section 5.5, Algorithm 1)
+# ---------------------------------------------------------------------------
+
+
+def accept_lengths(tokens, drafts, n_sessions, rows_per_session) -> np.ndarray:
+    """Accepted draft-prefix length per session.
+
+    Session s verifies rows s*R .. s*R+R-1 (R = k + 1).  Row r produces the
+    token that draft r must equal; the session keeps the longest prefix of
+    drafts that all match, a_s in [0, k].  Committed tokens are then drafts
+    [0, a_s) followed by the token of row a_s (the correction, or the bonus
+    token when every draft matched).
+    """
+    R = int(rows_per_session)
+    k = R - 1
+    tokens = np.asarray(tokens).reshape(n_sessions, R)
+    out = np.zeros(n_sessions, dtype=np.int32)
+    if k == 0:
+        return out
+    drafts = np.asarray(drafts).reshape(n_sessions, k)
+    for s in range(n_sessions):
+        a = 0
+        while a < k and tokens[s, a] == drafts[s, a]:
+            a += 1
+        out[s] = a
+    return out
+
+
+# ---------------------------------------------------------------------------
+# whole calls
+# ---------------------------------------------------------------------------
+
+
+def cloud_call(h_bits, d_end, subset, clip_c, w_cloud_bits=None, w_cloud_codes=None,
+               w_cloud_scale=None, bias=None, rows=None, with_abs=False):
+    """The cloud half of one decoding step (Algorithm 1, cloud partial):
+    eq. 12 on S, then clip and int8 quantisation of each row."""
+    z, absdot = cloud_partial_logits(h_bits, d_end, subset, w_cloud_bits, w_cloud_codes,
+                                     w_cloud_scale, bias, rows=rows, with_abs=with_abs)
+    out = clip_quantize(z, clip_c)
+    out["z"] = z
+    out["absdot"] = absdot
+    return out
+
+
+def endpoint_call(q, scale, h_bits, d_end, subset, w_end_bits, n_sessions, rows_per_session,
+                  drafts=None, mode="greedy", temperature=1.0, top_p=1.0, seed=0,
+                  with_abs=False):
+    """The endpoint half of one decoding step: eq. 11 on S, dequantise + fuse
+    + mask (eq. 13-14), select (eq. 15), then the accepted draft prefix."""
+    z_e, absdot = endpoint_partial_logits(h_bits, d_end, subset, w_end_bits, with_abs=with_abs)
+    f = fuse_masked(q, scale, z_e)
+    out = {"z_end": z_e, "absdot": absdot, "f": f}
+    if mode == "greedy":
+        tok, pos, gap = greedy_select(f, subset)
+        out.update(tokens=tok, pos=pos, gap=gap)
+    elif mode == "sample":
+        tok, info = sample_select(f, subset, temperature, top_p, seed, rows_per_session)
+        out.update(tokens=tok, **info)
+    else:
+        raise ValueError(mode)
+    out["accept"] = accept_lengths(out["tokens"], drafts, n_sessions, rows_per_session)
+    return out

@@ -1,0 +1,388 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each test names what fixes the expected value: a hand-worked example, a
+library routine for a special case, a closed form, an invariant, published
+known-answer vectors, exact rational arithmetic, or a statistical law.
+"""
+
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import (Config, f32_to_bf16_bits, make_workload, plant_masked_supertoken,
+                   scale_rows_bf16)
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bits(a):
+    return f32_to_bf16_bits(np.asarray(a, dtype=np.float32))
+
+
+# ---------------------------------------------------------------------------
+# input decodings vs library conversions
+# ---------------------------------------------------------------------------
+
+def test_bf16_decode_matches_torch_on_every_pattern():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    ours = oracle.decode_bf16(bits)
+    ref = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).float().double().numpy()
+    np.testing.assert_array_equal(np.isnan(ours), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    np.testing.assert_array_equal(ours[ok], ref[ok])
+
+
+def test_e4m3_decode_matches_torch_on_all_256_codes():
+    codes = np.arange(256, dtype=np.uint8)
+    ours = oracle.decode_e4m3(codes)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().double().numpy()
+    np.testing.assert_array_equal(np.isnan(ours), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    np.testing.assert_array_equal(ours[ok], ref[ok])
+    assert np.nanmax(ours) == 448.0 and np.isnan(ours).sum() == 2
+
+
+def test_generator_bf16_rounding_matches_torch():
+    x = np.random.default_rng(7).standard_normal(100000).astype(np.float32) * 3
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    np.testing.assert_array_equal(f32_to_bf16_bits(x), ref)
+
+
+# ---------------------------------------------------------------------------
+# Philox4x32-10
+# ---------------------------------------------------------------------------
+
+# Known-answer vectors published with the Random123 implementation of
+# Philox4x32-10 (Salmon et al., SC'11): (counter, key) -> output.
+PHILOX_KAT = [
+    ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF,) * 4, (0xFFFFFFFF,) * 2, (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+@pytest.mark.parametrize("ctr,key,out", PHILOX_KAT)
+def test_philox_known_answers(ctr, key, out):
+    assert oracle.philox4x32_10(ctr, key) == out
+
+
+def test_philox_uniform_is_uniform():
+    from scipy import stats
+    u = np.array([oracle.philox_uniform(0x1234_5678_9ABC_DEF0, r, s)
+                  for s in range(400) for r in range(10)])
+    assert u.min() >= 0 and u.max() < 1
+    assert stats.kstest(u, "uniform").pvalue > 1e-3
+    assert np.all(u * 2 ** 24 == np.floor(u * 2 ** 24))  # 24-bit grid
+
+
+# ---------------------------------------------------------------------------
+# the hand-worked example (golden fixture)
+# ---------------------------------------------------------------------------
+
+def test_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "worked_example.json")))
+    W = np.array(g["weights_by_id"], dtype=np.float32)
+    H = np.array(g["h"], dtype=np.float32)
+    S = np.array(g["subset"], dtype=np.int32)
+    de = g["d_end"]
+    wb, hb = _bits(W), _bits(H)
+    w_end, w_cloud = np.ascontiguousarray(wb[:, :de]), np.ascontiguousarray(wb[:, de:])
+
+    cl = oracle.cloud_call(hb, de, S, g["clip_c"], w_cloud_bits=w_cloud)
+    np.testing.assert_array_equal(cl["z"], np.array(g["z_cloud"], np.float32))
+    np.testing.assert_array_equal(cl["y"], np.array(g["y"], np.float32))
+    np.testing.assert_array_equal(cl["amax"], np.array(g["amax"], np.float32))
+    np.testing.assert_array_equal(cl["scale"], np.full(3, np.float32(30.0) / np.float32(127.0)))
+    np.testing.assert_array_equal(cl["q"], np.array(g["q"], np.int8))
+
+    z_e, _ = oracle.endpoint_partial_logits(hb, de, S, w_end)
+    np.testing.assert_array_equal(z_e, np.array(g["z_end"], np.float32))
+
+    # eq. 9 on the masked ids: they dominate the unmasked head
+    full = oracle.full_head_logits(hb, W.astype(np.float64))
+    np.testing.assert_array_equal(full[:, g["full_head_masked_ids"]["ids"]],
+                                  np.array(g["full_head_masked_ids"]["logits"], np.float64))
+
+    f = oracle.fuse_masked(cl["q"], cl["scale"], z_e)
+    exact = np.array(g["fused_exact_numerators_over_127"], np.float64) / 127.0
+    # s is the fp32 nearest to 30/127: |q| * |s - 30/127| <= 127 * 2^-26
+    np.testing.assert_allclose(f, exact, rtol=0, atol=4e-6)
+
+    tok, _, _ = oracle.greedy_select(f, S)
+    np.testing.assert_array_equal(tok, g["tokens"])
+    for case in g["verify_cases"]:
+        a = oracle.accept_lengths(tok, np.array([case["drafts"]]), 1, 3)
+        assert a[0] == case["accept"]
+        committed = list(case["drafts"][:a[0]]) + [int(tok[a[0]])]
+        assert committed == case["committed"]
+
+
+# ---------------------------------------------------------------------------
+# the split identity (eq. 9-13) and special cases that are library routines
+# ---------------------------------------------------------------------------
+
+def _small(seed, d=96, d_end=24, V=500, n=200, M=7, bias=True):
+    rng = np.random.default_rng(seed)
+    H = _bits(rng.standard_normal((M, d)))
+    W = _bits(rng.standard_normal((V, d)) / np.sqrt(d))
+    S = np.sort(rng.choice(V, n, replace=False)).astype(np.int32)
+    b = rng.standard_normal(V).astype(np.float32) if bias else None
+    return H, W, S, b
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_split_identity_against_unsplit_head(seed):
+    H, W, S, b = _small(seed)
+    de = 24
+    z_c, _ = oracle.cloud_partial_logits(H, de, S, w_cloud_bits=np.ascontiguousarray(W[:, de:]), bias=b)
+    z_e, _ = oracle.endpoint_partial_logits(H, de, S, np.ascontiguousarray(W[:, :de]))
+    full = oracle.full_head_logits(H, oracle.decode_bf16(W), bias=b)[:, S]
+    # each partial is one fp32 rounding of its exact value
+    err = np.abs(z_c.astype(np.float64) + z_e.astype(np.float64) - full)
+    bound = 2.0 ** -24 * (np.abs(z_c) + np.abs(z_e)) + 1e-30
+    assert np.all(err <= bound * 1.0000001)
+
+
+def test_split_identity_catches_a_swapped_split():
+    # the endpoint owns the FIRST d_end dims (eq. 10): swapping the halves breaks the identity
+    H, W, S, b = _small(3, bias=False)
+    de = 24
+    z_c, _ = oracle.cloud_partial_logits(H, de, S, w_cloud_bits=np.ascontiguousarray(W[:, de:]))
+    full = oracle.full_head_logits(H, oracle.decode_bf16(W))[:, S]
+    wrong, _ = oracle.endpoint_partial_logits(H[:, ::-1].copy(), de, S, np.ascontiguousarray(W[:, :de]))
+    assert np.abs(z_c + wrong - full).max() > 1e-2
+
+
+def test_d_end_zero_is_the_whole_head_via_torch_linear():
+    H, W, S, b = _small(4)
+    z_c, _ = oracle.cloud_partial_logits(H, 0, S, w_cloud_bits=W, bias=b)
+    z_e, _ = oracle.endpoint_partial_logits(H, 0, S, W[:, :0])
+    Ht = torch.from_numpy(oracle.decode_bf16(H))
+    Wt = torch.from_numpy(oracle.decode_bf16(W[S]))
+    ref = torch.nn.functional.linear(Ht, Wt, torch.from_numpy(b[S].astype(np.float64))).float().numpy()
+    np.testing.assert_allclose(z_c, ref, rtol=2 ** -23, atol=0)
+    assert not z_e.any()
+
+
+def test_full_vocab_subset_via_torch_linear():
+    H, W, _, _ = _small(5, bias=False)
+    S = np.arange(W.shape[0], dtype=np.int32)
+    de = 24
+    z_c, _ = oracle.cloud_partial_logits(H, de, S, w_cloud_bits=np.ascontiguousarray(W[:, de:]))
+    ref = torch.nn.functional.linear(torch.from_numpy(oracle.decode_bf16(H[:, de:])),
+                                     torch.from_numpy(oracle.decode_bf16(W[:, de:]))).float().numpy()
+    np.testing.assert_allclose(z_c, ref, rtol=2 ** -23, atol=0)
+
+
+def test_fp8_cloud_weights_via_torch_float8():
+    H, W, S, _ = _small(6, bias=False)
+    from synth import fp8_encode_rows
+    de = 24
+    codes, scale = fp8_encode_rows(np.ascontiguousarray(W[:, de:]))
+    z_c, _ = oracle.cloud_partial_logits(H, de, S, w_cloud_codes=codes, w_cloud_scale=scale)
+    Wq = torch.from_numpy(codes).view(torch.float8_e4m3fn).double() * torch.from_numpy(scale).double()[:, None]
+    ref = torch.nn.functional.linear(torch.from_numpy(oracle.decode_bf16(H[:, de:])), Wq[S]).float().numpy()
+    np.testing.assert_allclose(z_c, ref, rtol=2 ** -23, atol=0)
+
+
+def test_absdot_bounds_the_dot():
+    H, W, S, b = _small(8)
+    z, a = oracle.cloud_partial_logits(H, 24, S, w_cloud_bits=np.ascontiguousarray(W[:, 24:]),
+                                       bias=b, with_abs=True)
+    assert np.all(np.abs(z) <= a * (1 + 2 ** -23))
+
+
+# ---------------------------------------------------------------------------
+# clip + quantise (eq. 18 reading)
+# ---------------------------------------------------------------------------
+
+def test_quantizer_invariants():
+    rng = np.random.default_rng(11)
+    z = (rng.standard_normal((16, 3000)) * rng.uniform(0.1, 20, (16, 1))).astype(np.float32)
+    out = oracle.clip_quantize(z, 30.0)
+    y, s, q = out["y"], out["scale"], out["q"].astype(np.int32)
+    assert np.all(np.abs(y) <= 30)
+    assert np.all(np.abs(q) <= 127)
+    err = np.abs(q * s[:, None].astype(np.float64) - y.astype(np.float64))
+    assert np.all(err <= s[:, None] * (0.5 + 2 ** -20))
+    at = np.argmax(np.abs(y), axis=1)
+    assert np.all(np.abs(q[np.arange(16), at]) == 127)
+    assert np.all(np.sign(q) * np.sign(y) >= 0)
+
+
+def test_quantizer_rounds_half_to_even():
+    # amax = 127 gives s = 1 exactly, so t = y
+    z = np.array([[127, 2.5, 3.5, -2.5, -3.5, 0.5, 1.5, 126.5]], dtype=np.float32)
+    out = oracle.clip_quantize(z, 300.0)
+    assert out["scale"][0] == 1.0
+    np.testing.assert_array_equal(out["q"][0], [127, 2, 4, -2, -4, 0, 2, 126])
+
+
+def test_clip_and_zero_rows():
+    cfg = Config("t", 0, d=512, d_end=64, vocab=8192, n_sub=4096, subset_kind="perm",
+                 sessions=1, rows_per_session=3)
+    wl = make_workload(cfg)
+    h = scale_rows_bf16(wl.h_bits, [0], 10.0)
+    h[2] = 0
+    out = oracle.cloud_call(h, 64, wl.subset, 30.0, w_cloud_bits=wl.w_cloud_bits)
+    assert np.abs(out["z"][0]).max() > 30          # the scaled row does exceed the clip
+    assert out["amax"][0] == 30.0
+    assert out["scale"][0] == np.float32(30.0) / np.float32(127.0)
+    assert out["amax"][1] < 30                      # an ordinary row is not clipped
+    assert out["scale"][2] == 0 and not out["q"][2].any()
+
+
+# ---------------------------------------------------------------------------
+# fusion rounding
+# ---------------------------------------------------------------------------
+
+def _exact_round_f32(x: Fraction) -> np.float32:
+    """fp32 nearest to the rational x, ties to even, by exhaustive neighbours."""
+    f = np.float32(float(x))                   # within one ulp of the answer
+    cands = [np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))]
+    best = min(cands, key=lambda c: (abs(Fraction(float(c)) - x),
+                                     int(np.array(c, np.float32).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def test_round_sum_to_f32_is_a_single_rounding():
+    rng = np.random.default_rng(3)
+    q = rng.integers(-127, 128, 4000).astype(np.float64)
+    s = rng.uniform(1e-3, 1, 4000).astype(np.float32).astype(np.float64)
+    ze = (rng.standard_normal(4000) * 10.0 ** rng.integers(-12, 2, 4000)).astype(np.float32).astype(np.float64)
+    # crafted double-rounding cases: a = 1 (fp32), b = 2^-24 (1 + 2^-30) straddles a tie
+    q = np.concatenate([q, [1.0, 1.0, -1.0]])
+    s = np.concatenate([s, [1.0, 1.0, 1.0]])
+    ze = np.concatenate([ze, [2.0 ** -24 + 2.0 ** -60, 2.0 ** -24 - 2.0 ** -60, -(2.0 ** -24 + 2.0 ** -60)]])
+    got = oracle.round_sum_to_f32(q * s, ze)
+    want = np.array([_exact_round_f32(Fraction(a) + Fraction(b)) for a, b in zip(q * s, ze)])
+    np.testing.assert_array_equal(got, want)
+    assert got[-3] == np.nextafter(np.float32(1), np.float32(2))
+    assert got[-2] == np.float32(1)
+
+
+# ---------------------------------------------------------------------------
+# masking, greedy selection, verification
+# ---------------------------------------------------------------------------
+
+def test_masked_supertoken_is_never_emitted():
+    cfg = Config("t", 0, d=512, d_end=64, vocab=8192, n_sub=4096, subset_kind="perm",
+                 sessions=1, rows_per_session=3)
+    wl = make_workload(cfg)
+    we, wc = wl.w_end_bits.copy(), wl.w_cloud_bits.copy()
+    vid = plant_masked_supertoken(we, wc, wl.h_bits, 1, wl.subset)
+    Wfull = oracle.decode_bf16(np.concatenate([we, wc], axis=1))
+    assert np.argmax(oracle.full_head_logits(wl.h_bits, Wfull)[1]) == vid   # the plant works
+    cl = oracle.cloud_call(wl.h_bits, 64, wl.subset, 30.0, w_cloud_bits=wc)
+    for mode in ("greedy", "sample"):
+        ep = oracle.endpoint_call(cl["q"], cl["scale"], wl.h_bits, 64, wl.subset, we, 1, 3,
+                                  drafts=np.array([[vid, vid]]), mode=mode, temperature=5.0,
+                                  top_p=1.0, seed=1)
+        assert vid not in ep["tokens"] and np.all(np.isin(ep["tokens"], wl.subset))
+        assert ep["accept"][0] == 0
+
+
+def test_greedy_ties_go_to_lowest_id():
+    f = np.array([[1, 3, 3, 2], [5, 5, 5, 5]], dtype=np.float32)
+    tok, pos, gap = oracle.greedy_select(f, np.array([4, 7, 9, 12]))
+    np.testing.assert_array_equal(tok, [7, 4])
+    np.testing.assert_array_equal(gap, [0, 0])
+
+
+@pytest.mark.parametrize("k", [0, 1, 2, 4, 7])
+def test_accept_length_exhaustive_patterns(k):
+    R = k + 1
+    pats = list(range(1 << k))
+    n = len(pats)
+    rng = np.random.default_rng(k)
+    tokens = rng.integers(0, 1000, size=n * R).astype(np.int32)
+    drafts = np.empty((n, k), dtype=np.int32)
+    want = np.empty(n, dtype=np.int32)
+    for s, bits in enumerate(pats):
+        lead = 0
+        while lead < k and (bits >> lead) & 1:
+            lead += 1
+        want[s] = lead
+        for r in range(k):
+            t = tokens[s * R + r]
+            drafts[s, r] = t if (bits >> r) & 1 else t + 1000   # + 1000 never equals a token
+    got = oracle.accept_lengths(tokens, drafts if k else None, n, R)
+    np.testing.assert_array_equal(got, want)
+
+
+# ---------------------------------------------------------------------------
+# sampling (eq. 15 + top-p)
+# ---------------------------------------------------------------------------
+
+def _rows(f, m):
+    return np.repeat(np.asarray(f, np.float32)[None, :], m, axis=0)
+
+
+def test_sampling_reduces_to_greedy():
+    rng = np.random.default_rng(5)
+    f = rng.standard_normal((40, 300)).astype(np.float32)
+    S = np.sort(rng.choice(5000, 300, replace=False))
+    g, _, gap = oracle.greedy_select(f, S)
+    t1, _ = oracle.sample_select(f, S, 1e-4, 1.0, 99, 5)     # tau -> 0
+    t2, info = oracle.sample_select(f, S, 0.7, 1e-7, 99, 5)   # top_p -> 0: nucleus = {argmax}
+    ok = gap > 1e-2
+    np.testing.assert_array_equal(t1[ok], g[ok])
+    np.testing.assert_array_equal(t2, g)
+    assert np.all(info["nucleus"] == 1)
+
+
+def test_sampling_chi_square_against_softmax():
+    from scipy import stats
+    tau = 0.7
+    f = np.array([0.3, -0.4, 1.1, 0.0], dtype=np.float32)
+    S = np.array([3, 8, 20, 21])
+    n = 6000
+    tok, _ = oracle.sample_select(_rows(f, n), S, tau, 1.0, 2026, 6)
+    p = np.exp(f.astype(np.float64) / np.float32(tau).astype(np.float64))
+    p /= p.sum()
+    counts = np.array([(tok == i).sum() for i in S])
+    assert stats.chisquare(counts, p * n).pvalue > 1e-4
+
+
+def test_sampling_nucleus_cut_and_renormalisation():
+    from scipy import stats
+    tau = 1.0
+    p = np.array([0.05, 0.5, 0.15, 0.3])
+    f = np.log(p).astype(np.float32)
+    S = np.array([1, 2, 3, 4])
+    n = 6000
+    tok, info = oracle.sample_select(_rows(f, n), S, tau, 0.78, 7, 4)
+    assert np.all(info["nucleus"] == 2)                       # 0.5 + 0.3 >= 0.78 > 0.5
+    assert set(np.unique(tok)) <= {2, 4}
+    counts = np.array([(tok == 2).sum(), (tok == 4).sum()])
+    assert stats.chisquare(counts, np.array([0.5, 0.3]) / 0.8 * n).pvalue > 1e-4
+
+
+def test_sampling_walks_in_ascending_id_order():
+    # p = (0.1, 0.2, 0.3, 0.4) on ids (10, 20, 30, 40): the inverse CDF in id order
+    # maps u in [0, .1) -> 10, [.1, .3) -> 20, [.3, .6) -> 30, [.6, 1) -> 40.
+    p = np.array([0.1, 0.2, 0.3, 0.4])
+    f = np.log(p).astype(np.float32)
+    S = np.array([10, 20, 30, 40])
+    m = 64
+    tok, _ = oracle.sample_select(_rows(f, m), S, 1.0, 1.0, 31337, 8)
+    pe = np.exp(f.astype(np.float64))
+    pe /= pe.sum()
+    edges = np.cumsum(pe)
+    for row in range(m):
+        u = oracle.philox_uniform(31337, row % 8, row // 8)
+        assert tok[row] == S[int(np.sum(edges <= u))]
+
+
+def test_philox_uniform_takes_the_top_24_bits_of_word_0():
+    # seed 0, row 0, session 0 is counter 0 / key 0: word 0 of the first known answer
+    assert oracle.philox_uniform(0, 0, 0) == (0x6627E8D5 >> 8) * 2.0 ** -24
+    # seed = all ones is key (0xffffffff, 0xffffffff); counter (row, session, 0, 0)
+    x0 = oracle.philox4x32_10((3, 5, 0, 0), (0xFFFFFFFF, 0xFFFFFFFF))[0]
+    assert oracle.philox_uniform(2 ** 64 - 1, 3, 5) == (x0 >> 8) * 2.0 ** -24
