@@ -1,0 +1,234 @@
+"""Benchmark of the split-head vocabulary projection on one MI355X.
+
+One step = one pass of the whole hot path over one batch: sph_cloud_partial
+(gathered partial logits, clip, per-row int8) then sph_fuse_verify (endpoint
+partial, dequantise + fuse + mask, greedy select, accepted draft prefix).
+
+Default workload: single-session decode, d=4096, d_end=256, V=128256, a
+49152-id language subset (one block of 32768 ids plus 16384 scattered ids),
+1 session x 5 rows (k=4 drafts), bf16 h/W, clip 30, int8 payload.
+
+Prints ONE JSON line.  `value` is rows*vocab/s = M*|S| / (seconds per step)
+with every input resident in HBM before the timed region; three copies of
+the weights are rotated from step to step so the gathered rows stream from
+HBM rather than from the 256 MB last-level cache.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+N_COPIES = 3
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "cloud_gemv_decode_traffic.txt")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default="decode")
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="bound on the oracle's CPU baseline run (0 to skip)")
+    return p.parse_args()
+
+
+def algorithmic_bytes(cfg, n):
+    """Algorithmic HBM bytes of one cloud projection launch (all M rows):
+    every gathered weight row once, its id, and the rows of h_cloud."""
+    wbytes = 2 if cfg.wtype == "bf16" else 1
+    per_id = cfg.d_cloud * wbytes + 4 + (4 if cfg.wtype == "fp8" else 0)
+    return n * per_id + cfg.M * cfg.d_cloud * 2
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for name in ("gemv.hip", "sph_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_13093_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(digest):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
+    try:
+        kv = {}
+        with open(TRAFFIC_PROFILE) as f:
+            for line in f:
+                if ":" in line:
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel_source_sha256_16") != digest:
+            return None
+        return float(kv["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, seconds):
+    """The oracle, as it stands, on whole decode steps until `seconds` pass."""
+    import numpy as np
+
+    import oracle
+    cfg = wl.cfg
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    drafts = np.zeros((cfg.sessions, cfg.k), np.int32)
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        orc = oracle.cloud_call(wl.h_bits, cfg.d_end, wl.subset, cfg.clip_c,
+                                w_cloud_bits=wl.w_cloud_bits, w_cloud_codes=wl.w_cloud_codes,
+                                w_cloud_scale=wl.w_cloud_scale, bias=wl.bias)
+        oracle.endpoint_call(orc["q"], orc["scale"], wl.h_bits, cfg.d_end, wl.subset,
+                             wl.w_end_bits, cfg.sessions, cfg.rows_per_session, drafts=drafts)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= seconds:
+            break
+    return {"value": cfg.M * len(wl.subset) * reps / dt, "unit": "rows*vocab/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{reps} whole {cfg.name} steps (cloud + endpoint oracle, fp64 NumPy), {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_13093_amd as sph
+    from synth import CONFIGS, make_drafts, make_workload
+
+    cfg = CONFIGS[args.workload]
+    wl = make_workload(cfg)
+    n = len(wl.subset)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def up(a, dt=None):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        return (t.view(dt) if dt is not None else t).to(dev)
+
+    h = up(wl.h_bits.view(np.int16), torch.bfloat16)
+    if cfg.wtype == "bf16":
+        wc = [up(wl.w_cloud_bits.view(np.int16), torch.bfloat16) for _ in range(N_COPIES)]
+        wsc = None
+    else:
+        wc = [up(wl.w_cloud_codes, torch.uint8) for _ in range(N_COPIES)]
+        wsc = up(wl.w_cloud_scale)
+    we = [up(wl.w_end_bits.view(np.int16), torch.bfloat16) for _ in range(N_COPIES)]
+    sub = sph.Subset(vocab=cfg.vocab, full=True) if wl.full_vocab else sph.Subset(wl.subset, vocab=cfg.vocab)
+    mode = sph.GREEDY if cfg.mode == "greedy" else sph.SAMPLE
+    M, de = cfg.M, cfg.d_end
+    h_c, h_e = h[:, de:], h[:, :de]
+    q = torch.empty((M, n), dtype=torch.int8, device=dev)
+    s = torch.empty((M,), dtype=torch.float32, device=dev)
+    tok = torch.empty((M,), dtype=torch.int32, device=dev)
+    acc = torch.empty((cfg.sessions,), dtype=torch.int32, device=dev)
+    ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
+    ws_f = torch.empty(max(1, sph.fuse_verify_workspace(M, sub, mode)), dtype=torch.uint8, device=dev)
+    drafts = torch.zeros((cfg.sessions, max(cfg.k, 1)), dtype=torch.int32, device=dev)
+
+    def step(i):
+        c = i % N_COPIES
+        sph.cloud_partial(h_c, wc[c], sub, cfg.clip_c, w_row_scale=wsc, workspace=ws_c,
+                          out=(q, s, None))
+        sph.fuse_verify(q, s, h_e, we[c], sub, cfg.sessions, cfg.rows_per_session,
+                        drafts if cfg.k else None, mode=mode, temperature=cfg.temperature,
+                        top_p=cfg.top_p, seed=cfg.philox_seed, workspace=ws_f,
+                        out=(tok, acc, None))
+
+    # drafts: a fair coin between the GPU's own token for the row and a random subset id
+    step(0)
+    torch.cuda.synchronize()
+    if cfg.k:
+        drafts.copy_(torch.from_numpy(make_drafts(cfg, tok.cpu().numpy(), wl.subset)))
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    per_step = 4  # launches per step on the skinny path: gemv, quantise, gemv, finalise
+    sph.trace_start(per_step * args.steps + 16)
+    stream = torch.cuda.current_stream(dev)
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    t_stop.record(stream)
+    torch.cuda.synchronize()
+    recs = sph.trace_collect(per_step * args.steps + 16)
+    ms_step = t_start.elapsed_time(t_stop) / args.steps
+
+    by = {}
+    for name, ms in recs:
+        by.setdefault(name, []).append(ms)
+    gemv_ms = float(np.mean(by["cloud_gemv"]))
+    nbytes = algorithmic_bytes(cfg, n)
+    achieved = nbytes / (gemv_ms * 1e-3) / 1e9
+    digest = source_digest()
+    traffic = read_traffic(digest)
+
+    out = {
+        "metric": "split-head rows*vocab/s",
+        "value": M * n / (ms_step * 1e-3),
+        "unit": "rows*vocab/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: d={cfg.d} d_end={cfg.d_end} V={cfg.vocab} |S|={n} "
+                        f"sessions={cfg.sessions} rows={cfg.rows_per_session} {cfg.wtype} "
+                        f"{cfg.mode} clip={cfg.clip_c}",
+            "rows": M,
+            "subset": n,
+            "payload_bytes_per_row": n + 4,
+        },
+        "roofline": {
+            "kernel": "cloud_gemv",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": nbytes,
+            "avg_launch_ms": gemv_ms,
+            "kernel_source_sha256_16": digest,
+        },
+        "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,198 @@
+/*
+ * sph.h - split-head vocabulary projection on one MI355X (gfx950).
+ *
+ * The LM head z = h' W_lm + b is split along the hidden dimension into an
+ * endpoint half (the first d_end dimensions) and a cloud half (the remaining
+ * d_cloud dimensions), eq. 10 of Section 5.4.  Two calls cover one decoding
+ * step of the collaborative loop (Algorithm 1):
+ *
+ *   sph_cloud_partial  eq. 12 on the language subset S = V_l, then the clip
+ *                      and the per-row int8 payload of Section 5.4 / eq. 18.
+ *   sph_fuse_verify    eq. 11 on S, dequantise + fuse + mask (eq. 13-14),
+ *                      greedy or temperature/top-p selection (eq. 15) and the
+ *                      accepted draft prefix of each session (Section 5.5).
+ *
+ * Conventions shared by every call:
+ *  - Tensors are caller-owned HIP device memory unless a parameter says
+ *    "host".  The library never frees them.
+ *  - Weights are vocab-major: row v holds the d weights of vocabulary id v
+ *    (column v of the paper's D x V matrix).  bf16 tensors are passed as raw
+ *    16-bit patterns; fp8 weights use the OCP E4M3 encoding.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ *    enqueue work on it and return without synchronising; outputs are valid
+ *    once the stream has completed.  Calls on one stream are ordered; calls
+ *    that share a workspace must not overlap.
+ *  - A negative return value is an error; nothing has been enqueued.  The
+ *    message is available from sph_last_error() on the same thread.  Device
+ *    contents (NaN inputs, draft ids) are never validated; inputs are
+ *    assumed finite.
+ *  - Rows of h are independent; M = n_sessions * rows_per_session rows form
+ *    the verification windows of the sessions: row r of session s is row
+ *    s * rows_per_session + r.
+ */
+#ifndef SPH_H
+#define SPH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPH_ABI_VERSION 1
+
+/* status codes */
+#define SPH_OK             0
+#define SPH_E_INVALID_ARG (-1) /* bad pointer, size, stride, enum or scalar */
+#define SPH_E_SUBSET      (-2) /* subset ids not strictly ascending / out of range / empty */
+#define SPH_E_UNSUPPORTED (-3) /* valid request this build cannot run */
+#define SPH_E_DEVICE      (-4) /* a HIP runtime call failed; message has the HIP error */
+#define SPH_E_WORKSPACE   (-5) /* workspace missing or smaller than required */
+
+/* weight encodings of the cloud slice */
+#define SPH_W_BF16     0
+#define SPH_W_FP8_E4M3 1  /* OCP E4M3, with one fp32 scale per vocabulary row */
+
+/* selection modes */
+#define SPH_GREEDY 0
+#define SPH_SAMPLE 1
+
+/* Version of this interface (SPH_ABI_VERSION of the built library). */
+int sph_abi_version(void);
+
+/* Message of the last failing call on this thread ("" if none).  Valid until
+ * the next sph_* call on the thread. */
+const char* sph_last_error(void);
+
+/*
+ * Vocabulary subset plan: the language-restricted subset V_l of Section 5.4
+ * (the endpoint names it by a subset identifier; Section 6.2 precomputes the
+ * mapping from tokenizer metadata).  A plan is an immutable device copy of
+ * the ids, created once and reused by any number of calls on any stream of
+ * the device that was current at creation.
+ */
+typedef struct sph_subset_s* sph_subset;
+
+/* host_ids: host int32 [n], strictly ascending, 0 <= id < vocab, n >= 1
+ * (SPH_E_SUBSET otherwise).  Allocates device memory, copies the ids on
+ * `stream` and waits for the copy, so host_ids may be freed on return. */
+int sph_subset_create(const int32_t* host_ids, int64_t n, int64_t vocab, void* stream,
+                      sph_subset* out);
+
+/* The whole vocabulary [0, vocab): mixed-language mode, no mask (Section 5.4). */
+int sph_subset_create_full(int64_t vocab, void* stream, sph_subset* out);
+
+/* Number of ids and vocabulary size of a plan. */
+int sph_subset_size(sph_subset subset, int64_t* n, int64_t* vocab);
+
+/* Device pointer to the plan's int32 ids (read-only, owned by the plan). */
+int sph_subset_device_ids(sph_subset subset, const int32_t** ids);
+
+/* Frees the plan once the device is idle with respect to calls using it.
+ * NULL is ignored. */
+void sph_subset_destroy(sph_subset subset);
+
+/*
+ * Workspace sizes in bytes (256-byte aligned device memory, caller-owned).
+ * The cloud workspace holds the fp32 partial logits (unless z_out is given,
+ * the region is still reserved) and per-block row maxima; the fuse
+ * workspace holds per-block argmax candidates and, for SPH_SAMPLE, the fused
+ * fp32 logits.  Returns 0 for M == 0.
+ */
+size_t sph_cloud_partial_workspace(int64_t M, sph_subset subset);
+size_t sph_fuse_verify_workspace(int64_t M, sph_subset subset, int mode);
+
+/*
+ * Cloud half (eq. 12 on S, then clip and per-row int8; Section 5.4, eq. 18).
+ *
+ *   z[m, j] = sum_{i < d_cloud} h_cloud[m, i] * Wc[S_j, i] * s_{S_j} + b[S_j]
+ *   y       = clamp(z, -clip_c, clip_c)
+ *   a_m     = max_j |y[m, j]|,   scale[m] = fp32(a_m / 127)   (0 if a_m == 0)
+ *   q[m, j] = clamp(rint_half_even(fp32(y / scale[m])), -127, 127)  (0 if scale == 0)
+ *
+ * h_cloud     bf16 [M, d_cloud], row stride ldh elements (pass h + d_end with
+ *             ldh = d to read the cloud columns of a full [M, d] hidden state)
+ * w_cloud     [V, d_cloud] vocab-major, row stride ldw elements; bf16 bit
+ *             patterns for SPH_W_BF16, E4M3 bytes for SPH_W_FP8_E4M3.  Must
+ *             hold every row named by the subset.
+ * w_row_scale fp32 [V]: required for SPH_W_FP8_E4M3 (s_v above), NULL for bf16
+ * bias        fp32 [V] or NULL; added once, on the cloud side, before the clip
+ * subset      plan; n_sub = its size
+ * clip_c      > 0 and finite
+ * q_out       int8 [M, n_sub] row-major: the payload codes
+ * scale_out   fp32 [M]: the payload scales
+ * z_out       fp32 [M, n_sub] or NULL: the pre-clip partial logits exactly as
+ *             quantised (validation)
+ * workspace   >= sph_cloud_partial_workspace(M, subset) bytes
+ * The payload of one row is n_sub + 4 bytes (eq. 21 without transport
+ * overhead).  M == 0 is a no-op.
+ */
+int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                      const void* w_cloud, int64_t ldw, int wtype, const float* w_row_scale,
+                      const float* bias, sph_subset subset, float clip_c,
+                      int8_t* q_out, float* scale_out, float* z_out,
+                      void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Endpoint half: eq. 11 on S, fusion with the dequantised payload and the
+ * mask (eq. 13-14), selection (eq. 15) and verification (Section 5.5).
+ *
+ *   f[m, j]  = fmaf(q[m, j], scale[m], sum_{i < d_end} h_end[m, i] * We[S_j, i])
+ *   GREEDY:  token[m] = S[argmax_j f[m, j]], ties to the lowest id
+ *   SAMPLE:  p = softmax(f / temperature) over S; the nucleus is the
+ *            shortest prefix of S ordered by (p desc, id asc) whose mass
+ *            reaches top_p; u = top 24 bits of word 0 of Philox4x32-10 with
+ *            key (lo32(seed), hi32(seed)) and counter (r, s, 0, 0) times
+ *            2^-24; the token is the first nucleus member in ascending id
+ *            order whose running mass exceeds u * mass(nucleus).
+ *   accept_len[s] = largest a <= k with token[s*R + r] == drafts[s, r] for
+ *            all r < a (R = rows_per_session, k = R - 1).  The committed
+ *            tokens of session s are drafts[s, 0..a) then token[s*R + a].
+ *
+ * q, scale    the payload of sph_cloud_partial for the same rows and subset
+ * h_end       bf16 [M, d_end], row stride ldh (may be NULL if d_end == 0)
+ * w_end       bf16 [V, d_end] vocab-major, row stride ldw (NULL if d_end == 0)
+ * drafts      int32 [n_sessions, k]; required when k > 0.  Ids outside S
+ *             are legal and never match.
+ * mode        SPH_GREEDY (temperature, top_p, seed ignored) or SPH_SAMPLE
+ *             (temperature > 0, 0 < top_p <= 1)
+ * tokens_out  int32 [M] vocabulary ids, always members of S
+ * accept_len_out int32 [n_sessions], in [0, k]
+ * fused_out   fp32 [M, n_sub] or NULL: f (validation)
+ * workspace   >= sph_fuse_verify_workspace(M, subset, mode) bytes
+ */
+int sph_fuse_verify(const int8_t* q, const float* scale,
+                    const void* h_end, int64_t ldh, int64_t d_end,
+                    const void* w_end, int64_t ldw, sph_subset subset,
+                    int64_t n_sessions, int64_t rows_per_session, const int32_t* drafts,
+                    int mode, float temperature, float top_p, uint64_t seed,
+                    int32_t* tokens_out, int32_t* accept_len_out, float* fused_out,
+                    void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Kernel tracing.  While a trace is active, every kernel the library
+ * launches is bracketed by two HIP events recorded on the launch stream, so
+ * the durations are those of the kernels as they ran in the caller's
+ * workload.  Tracing is process-wide and costs two event records per launch.
+ */
+#define SPH_TRACE_NAME_LEN 32
+typedef struct {
+  char kernel[SPH_TRACE_NAME_LEN]; /* "cloud_gemv", "cloud_quantize", "fuse_gemv", ... */
+  float ms;                        /* duration on the GPU */
+} sph_trace_record;
+
+/* Start recording up to `capacity` launches (capacity >= 1); restarts any
+ * active trace.  Launches beyond the capacity are not recorded. */
+int sph_trace_start(int capacity);
+
+/* Stop recording, wait for the recorded events, and copy up to max_records
+ * records (launch order) to `out` (host memory); *n_out gets the number of
+ * recorded launches.  Frees the trace's events. */
+int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPH_H */

@@ -1,0 +1,19 @@
+"""Split-head vocabulary projection (distributed LM head with speculative
+verification) as hand-written HIP kernels for MI355X / gfx950.
+
+The library is libsph.so (C ABI, include/sph.h); this package is its thin
+torch binding.  Importing it does not touch the GPU.
+"""
+
+from .api import (  # noqa: F401
+    GREEDY,
+    SAMPLE,
+    SphError,
+    Subset,
+    cloud_partial,
+    cloud_partial_workspace,
+    fuse_verify,
+    fuse_verify_workspace,
+    trace_collect,
+    trace_start,
+)

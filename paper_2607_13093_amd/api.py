@@ -1,0 +1,181 @@
+"""Thin torch-facing binding of libsph: argument marshalling only.
+
+torch supplies device memory and the current stream; every step of the
+computation runs in the library's HIP kernels.  Tensors must live on the GPU
+and be contiguous along their last dimension (row strides are passed on).
+"""
+
+from __future__ import annotations
+
+from typing import Optional
+
+import torch
+
+from . import _lib
+from ._lib import SphError, check  # noqa: F401
+
+GREEDY = _lib.SPH_GREEDY
+SAMPLE = _lib.SPH_SAMPLE
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _require_gpu(name: str, t: torch.Tensor) -> None:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dim() >= 1 and t.numel() > 0 and t.stride(-1) != 1:
+        raise ValueError(f"{name} must be contiguous along its last dimension")
+
+
+def _as_bits16(t: torch.Tensor) -> torch.Tensor:
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return t
+    raise TypeError(f"expected bf16 (or its 16-bit patterns), got {t.dtype}")
+
+
+class Subset:
+    """Device plan of a vocabulary subset V_l (strictly ascending ids)."""
+
+    def __init__(self, ids=None, vocab: int = 0, full: bool = False, device=None):
+        lib = _lib.load()
+        self._lib = lib
+        self.handle = ctypes_vp()
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        with torch.cuda.device(dev):
+            stream = _stream_handle(dev)
+            if full:
+                check(lib.sph_subset_create_full(int(vocab), stream, self.handle))
+            else:
+                import numpy as np
+                host = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+                check(lib.sph_subset_create(host.ctypes.data, host.size, int(vocab), stream,
+                                            self.handle))
+        n = _lib.c_i64()
+        v = _lib.c_i64()
+        check(lib.sph_subset_size(self.handle, n, v))
+        self.n, self.vocab = n.value, v.value
+        self.device = dev
+
+    def device_ids_ptr(self) -> int:
+        p = _lib.c_vp()
+        check(self._lib.sph_subset_device_ids(self.handle, p))
+        return p.value
+
+    def close(self) -> None:
+        if self.handle is not None and self.handle.value:
+            self._lib.sph_subset_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ctypes_vp():
+    return _lib.c_vp()
+
+
+def cloud_partial_workspace(M: int, subset: Subset) -> int:
+    return int(_lib.load().sph_cloud_partial_workspace(int(M), subset.handle))
+
+
+def fuse_verify_workspace(M: int, subset: Subset, mode: int = GREEDY) -> int:
+    return int(_lib.load().sph_fuse_verify_workspace(int(M), subset.handle, int(mode)))
+
+
+def cloud_partial(h_cloud: torch.Tensor, w_cloud: torch.Tensor, subset: Subset, clip_c: float,
+                  w_row_scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
+                  want_z: bool = False, workspace: Optional[torch.Tensor] = None, out=None):
+    """Cloud half: returns (q int8 [M, n], scale fp32 [M], z fp32 [M, n] or None).
+
+    h_cloud: bf16 [M, d_cloud] view (rows may be strided, e.g. h[:, d_end:]).
+    w_cloud: bf16 [V, d_cloud] or fp8 E4M3 (torch.float8_e4m3fn / uint8) with
+    w_row_scale fp32 [V].
+    """
+    lib = _lib.load()
+    _require_gpu("h_cloud", h_cloud)
+    _require_gpu("w_cloud", w_cloud)
+    h_cloud = _as_bits16(h_cloud)
+    if w_cloud.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        wtype = _lib.SPH_W_BF16
+    elif w_cloud.dtype in (torch.float8_e4m3fn, torch.uint8):
+        wtype = _lib.SPH_W_FP8_E4M3
+    else:
+        raise TypeError(f"unsupported weight dtype {w_cloud.dtype}")
+    M, d_cloud = h_cloud.shape
+    dev = h_cloud.device
+    if out is None:
+        q = torch.empty((M, subset.n), dtype=torch.int8, device=dev)
+        scale = torch.empty((M,), dtype=torch.float32, device=dev)
+        z = torch.empty((M, subset.n), dtype=torch.float32, device=dev) if want_z else None
+    else:
+        q, scale, z = out
+    need = cloud_partial_workspace(M, subset)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_cloud_partial(
+        h_cloud.data_ptr(), h_cloud.stride(0) if M > 0 else d_cloud, M, d_cloud,
+        w_cloud.data_ptr(), w_cloud.stride(0), wtype, _ptr(w_row_scale),
+        _ptr(bias), subset.handle, float(clip_c),
+        q.data_ptr(), scale.data_ptr(), _ptr(z),
+        workspace.data_ptr(), workspace.numel(), _stream_handle(dev)))
+    return q, scale, z
+
+
+def fuse_verify(q: torch.Tensor, scale: torch.Tensor, h_end: Optional[torch.Tensor],
+                w_end: Optional[torch.Tensor], subset: Subset, n_sessions: int,
+                rows_per_session: int, drafts: Optional[torch.Tensor], mode: int = GREEDY,
+                temperature: float = 1.0, top_p: float = 1.0, seed: int = 0,
+                want_fused: bool = False, workspace: Optional[torch.Tensor] = None, out=None):
+    """Endpoint half: returns (tokens int32 [M], accept_len int32 [S], fused fp32 or None)."""
+    lib = _lib.load()
+    dev = q.device
+    M = int(n_sessions) * int(rows_per_session)
+    if h_end is not None and h_end.shape[1] > 0:
+        _require_gpu("h_end", h_end)
+        _require_gpu("w_end", w_end)
+        h_end = _as_bits16(h_end)
+        w_end = _as_bits16(w_end)
+        d_end = h_end.shape[1]
+        hp, ldh, wp, ldw = h_end.data_ptr(), h_end.stride(0), w_end.data_ptr(), w_end.stride(0)
+    else:
+        d_end, hp, ldh, wp, ldw = 0, None, 0, None, 0
+    if out is None:
+        tokens = torch.empty((M,), dtype=torch.int32, device=dev)
+        accept = torch.empty((int(n_sessions),), dtype=torch.int32, device=dev)
+        fused = torch.empty((M, subset.n), dtype=torch.float32, device=dev) if want_fused else None
+    else:
+        tokens, accept, fused = out
+    need = fuse_verify_workspace(M, subset, mode)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_fuse_verify(
+        q.data_ptr(), scale.data_ptr(), hp, ldh, d_end, wp, ldw, subset.handle,
+        int(n_sessions), int(rows_per_session), _ptr(drafts),
+        int(mode), float(temperature), float(top_p), int(seed) & 0xFFFFFFFFFFFFFFFF,
+        tokens.data_ptr(), accept.data_ptr(), _ptr(fused),
+        workspace.data_ptr(), workspace.numel(), _stream_handle(dev)))
+    return tokens, accept, fused
+
+
+def trace_start(capacity: int) -> None:
+    """Record HIP events around the next `capacity` kernel launches."""
+    check(_lib.load().sph_trace_start(int(capacity)))
+
+
+def trace_collect(capacity: int):
+    """Stop tracing and return [(kernel name, milliseconds)] in launch order."""
+    import ctypes
+    lib = _lib.load()
+    recs = (_lib.TraceRecord * int(capacity))()
+    n = ctypes.c_int(0)
+    check(lib.sph_trace_stop(recs, int(capacity), n))
+    return [(recs[i].kernel.decode(), float(recs[i].ms)) for i in range(min(n.value, capacity))]

@@ -1,0 +1,401 @@
+// C-ABI host layer: argument validation, subset plans, workspace layout and
+// dispatch of the kernels on the caller's stream.  Nothing here touches
+// device data; every check happens before the first launch.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "sph.h"
+#include "sph_internal.h"
+
+struct sph_subset_s {
+  int32_t* d_ids;   // device int32 [n], strictly ascending
+  int64_t n;
+  int64_t vocab;
+  int device;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return SPH_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(SPH_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+constexpr int64_t kMaxIds = 0x7FFFFFFF;
+
+// ---- kernel tracing: event pairs around launches -------------------------
+struct TraceSlot {
+  const char* name;
+  hipEvent_t start, stop;
+};
+std::mutex g_trace_mu;
+std::vector<TraceSlot> g_trace;
+size_t g_trace_used = 0;
+bool g_tracing = false;
+
+void trace_free_locked() {
+  for (auto& t : g_trace) {
+    (void)hipEventDestroy(t.start);
+    (void)hipEventDestroy(t.stop);
+  }
+  g_trace.clear();
+  g_trace_used = 0;
+  g_tracing = false;
+}
+
+// Records the start event of a launch; returns the slot or -1.
+long trace_begin(const char* name, hipStream_t s) {
+  if (!g_tracing) return -1;
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  if (!g_tracing || g_trace_used >= g_trace.size()) return -1;
+  TraceSlot& t = g_trace[g_trace_used];
+  t.name = name;
+  if (hipEventRecord(t.start, s) != hipSuccess) return -1;
+  return (long)g_trace_used++;
+}
+
+void trace_end(long slot, hipStream_t s) {
+  if (slot < 0) return;
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  if ((size_t)slot < g_trace.size()) (void)hipEventRecord(g_trace[(size_t)slot].stop, s);
+}
+
+// Launch `body` (returning hipError_t) between two trace events.
+template <class F>
+hipError_t traced(const char* name, hipStream_t s, F&& body) {
+  const long slot = trace_begin(name, s);
+  const hipError_t e = body();
+  trace_end(slot, s);
+  return e;
+}
+
+int make_plan(const int32_t* host_ids, int64_t n, int64_t vocab, hipStream_t stream,
+              sph_subset* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int32_t* d = nullptr;
+  e = hipMalloc(&d, (size_t)n * sizeof(int32_t));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(subset)");
+  e = hipMemcpyAsync(d, host_ids, (size_t)n * sizeof(int32_t), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    (void)hipFree(d);
+    return hip_fail(e, "copying subset ids");
+  }
+  *out = new sph_subset_s{d, n, vocab, dev};
+  return ok();
+}
+
+// Cloud workspace: [fp32 z : M x n][fp32 row-max partials : M x kMaxBlocks]
+size_t cloud_ws(int64_t M, int64_t n) {
+  if (M <= 0) return 0;
+  return align256((size_t)M * n * 4) + align256((size_t)M * sph::kMaxBlocks * 4);
+}
+
+// Fuse workspace: [argmax keys : M x kMaxBlocks][sample: fp32 f : M x n]
+size_t fuse_ws(int64_t M, int64_t n, int mode) {
+  if (M <= 0) return 0;
+  size_t b = align256((size_t)M * sph::kMaxBlocks * 8);
+  if (mode == SPH_SAMPLE) b += align256((size_t)M * n * 4);
+  return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sph_abi_version(void) { return SPH_ABI_VERSION; }
+
+const char* sph_last_error(void) { return g_err.c_str(); }
+
+int sph_subset_create(const int32_t* host_ids, int64_t n, int64_t vocab, void* stream,
+                      sph_subset* out) {
+  if (!out) return fail(SPH_E_INVALID_ARG, "sph_subset_create: out is NULL");
+  *out = nullptr;
+  if (!host_ids) return fail(SPH_E_INVALID_ARG, "sph_subset_create: host_ids is NULL");
+  if (vocab < 1 || vocab > kMaxIds)
+    return fail(SPH_E_INVALID_ARG, "sph_subset_create: vocab %lld out of range", (long long)vocab);
+  if (n < 1 || n > vocab)
+    return fail(SPH_E_SUBSET, "sph_subset_create: size %lld not in [1, vocab=%lld]", (long long)n,
+                (long long)vocab);
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t id = host_ids[i];
+    if (id < 0 || id >= vocab)
+      return fail(SPH_E_SUBSET, "sph_subset_create: id %lld at %lld outside [0, %lld)",
+                  (long long)id, (long long)i, (long long)vocab);
+    if (i > 0 && id <= host_ids[i - 1])
+      return fail(SPH_E_SUBSET, "sph_subset_create: ids not strictly ascending at %lld (%d after %d)",
+                  (long long)i, (int)id, (int)host_ids[i - 1]);
+  }
+  return make_plan(host_ids, n, vocab, (hipStream_t)stream, out);
+}
+
+int sph_subset_create_full(int64_t vocab, void* stream, sph_subset* out) {
+  if (!out) return fail(SPH_E_INVALID_ARG, "sph_subset_create_full: out is NULL");
+  *out = nullptr;
+  if (vocab < 1 || vocab > kMaxIds)
+    return fail(SPH_E_INVALID_ARG, "sph_subset_create_full: vocab %lld out of range",
+                (long long)vocab);
+  std::vector<int32_t> ids((size_t)vocab);
+  for (int64_t i = 0; i < vocab; ++i) ids[(size_t)i] = (int32_t)i;
+  return make_plan(ids.data(), vocab, vocab, (hipStream_t)stream, out);
+}
+
+int sph_subset_size(sph_subset subset, int64_t* n, int64_t* vocab) {
+  if (!subset) return fail(SPH_E_INVALID_ARG, "sph_subset_size: subset is NULL");
+  if (n) *n = subset->n;
+  if (vocab) *vocab = subset->vocab;
+  return ok();
+}
+
+int sph_subset_device_ids(sph_subset subset, const int32_t** ids) {
+  if (!subset || !ids) return fail(SPH_E_INVALID_ARG, "sph_subset_device_ids: NULL argument");
+  *ids = subset->d_ids;
+  return ok();
+}
+
+void sph_subset_destroy(sph_subset subset) {
+  if (!subset) return;
+  (void)hipFree(subset->d_ids);
+  delete subset;
+}
+
+size_t sph_cloud_partial_workspace(int64_t M, sph_subset subset) {
+  if (!subset || M < 0) return 0;
+  return cloud_ws(M, subset->n);
+}
+
+size_t sph_fuse_verify_workspace(int64_t M, sph_subset subset, int mode) {
+  if (!subset || M < 0) return 0;
+  return fuse_ws(M, subset->n, mode);
+}
+
+int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                      const void* w_cloud, int64_t ldw, int wtype, const float* w_row_scale,
+                      const float* bias, sph_subset subset, float clip_c, int8_t* q_out,
+                      float* scale_out, float* z_out, void* workspace, size_t ws_bytes,
+                      void* stream) {
+  const char* fn = "sph_cloud_partial";
+  if (M < 0 || M > (1 << 24)) return fail(SPH_E_INVALID_ARG, "%s: M=%lld out of range", fn, (long long)M);
+  if (d_cloud < 0 || d_cloud > (1 << 20))
+    return fail(SPH_E_INVALID_ARG, "%s: d_cloud=%lld out of range", fn, (long long)d_cloud);
+  if (wtype != SPH_W_BF16 && wtype != SPH_W_FP8_E4M3)
+    return fail(SPH_E_INVALID_ARG, "%s: unknown weight type %d", fn, wtype);
+  if (wtype == SPH_W_FP8_E4M3 && !w_row_scale)
+    return fail(SPH_E_INVALID_ARG, "%s: fp8 weights need w_row_scale", fn);
+  if (wtype == SPH_W_BF16 && w_row_scale)
+    return fail(SPH_E_INVALID_ARG, "%s: w_row_scale is only for fp8 weights", fn);
+  if (!(clip_c > 0.0f) || !std::isfinite(clip_c))
+    return fail(SPH_E_INVALID_ARG, "%s: clip_c must be positive and finite", fn);
+  if (ldh < d_cloud || ldw < d_cloud)
+    return fail(SPH_E_INVALID_ARG, "%s: row strides (ldh=%lld, ldw=%lld) below d_cloud=%lld", fn,
+                (long long)ldh, (long long)ldw, (long long)d_cloud);
+  if (!subset) return fail(SPH_E_INVALID_ARG, "%s: subset is NULL", fn);
+  if (M == 0) return ok();
+  if (!h_cloud && d_cloud > 0) return fail(SPH_E_INVALID_ARG, "%s: h_cloud is NULL", fn);
+  if (!w_cloud) return fail(SPH_E_INVALID_ARG, "%s: w_cloud is NULL", fn);
+  if (!q_out || !scale_out) return fail(SPH_E_INVALID_ARG, "%s: q_out/scale_out is NULL", fn);
+  const int64_t n = subset->n;
+  const size_t need = cloud_ws(M, n);
+  if (!workspace || ws_bytes < need)
+    return fail(SPH_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                workspace ? ws_bytes : (size_t)0);
+  const int wbytes = wtype == SPH_W_BF16 ? 2 : 1;
+  const int epc = wtype == SPH_W_BF16 ? 8 : 16;
+  const int64_t Kp = round_up(d_cloud, epc);
+  if ((reinterpret_cast<uintptr_t>(w_cloud) & 15) != 0 || (ldw * wbytes) % 16 != 0 || d_cloud % epc != 0)
+    return fail(SPH_E_UNSUPPORTED,
+                "%s: weight rows must be 16-byte aligned and d_cloud a multiple of %d", fn, epc);
+  int mr = sph::kGemvMaxRows;
+  if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
+  if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_cloud=%lld too large", fn, (long long)d_cloud);
+
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* z = z_out ? z_out : reinterpret_cast<float*>(ws);
+  float* amax = reinterpret_cast<float*>(ws + align256((size_t)M * n * 4));
+
+  const int rpi = sph::gemv_rows_per_iter(sph::kEpiCloud, 64);
+  const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
+  for (int64_t m0 = 0; m0 < M; m0 += mr) {
+    const int rows = (int)std::min<int64_t>(mr, M - m0);
+    sph::GemvArgs a{};
+    a.h = static_cast<const uint16_t*>(h_cloud) + m0 * ldh;
+    a.ldh = ldh;
+    a.K = (int)d_cloud;
+    a.Kp = (int)Kp;
+    a.w = static_cast<const uint8_t*>(w_cloud);
+    a.ldw_bytes = ldw * wbytes;
+    a.wscale = w_row_scale;
+    a.ids = subset->d_ids;
+    a.n = (int)n;
+    a.nblk = nblk;
+    a.bias = bias;
+    a.clip = clip_c;
+    a.z = z + m0 * n;
+    a.amax_part = amax + m0 * sph::kMaxBlocks;
+    hipError_t e = traced("cloud_gemv", s, [&] { return sph::launch_gemv(sph::kEpiCloud, wtype, rows, 64, a, s); });
+    if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
+  }
+  hipError_t e = traced("cloud_quantize", s, [&] {
+    return sph::launch_quantize(z, amax, nblk, (int)M, (int)n, clip_c, q_out, scale_out, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "quantiser launch");
+  return ok();
+}
+
+int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int64_t ldh,
+                    int64_t d_end, const void* w_end, int64_t ldw, sph_subset subset,
+                    int64_t n_sessions, int64_t rows_per_session, const int32_t* drafts, int mode,
+                    float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                    int32_t* accept_len_out, float* fused_out, void* workspace, size_t ws_bytes,
+                    void* stream) {
+  const char* fn = "sph_fuse_verify";
+  (void)seed;
+  if (n_sessions < 0 || rows_per_session < 1 || rows_per_session > 1024)
+    return fail(SPH_E_INVALID_ARG, "%s: n_sessions=%lld / rows_per_session=%lld out of range", fn,
+                (long long)n_sessions, (long long)rows_per_session);
+  const int64_t M = n_sessions * rows_per_session;
+  if (M > (1 << 24)) return fail(SPH_E_INVALID_ARG, "%s: M=%lld too large", fn, (long long)M);
+  if (d_end < 0 || d_end > (1 << 20))
+    return fail(SPH_E_INVALID_ARG, "%s: d_end=%lld out of range", fn, (long long)d_end);
+  if (mode != SPH_GREEDY && mode != SPH_SAMPLE)
+    return fail(SPH_E_INVALID_ARG, "%s: unknown mode %d", fn, mode);
+  if (mode == SPH_SAMPLE) {
+    if (!(temperature > 0.0f) || !std::isfinite(temperature))
+      return fail(SPH_E_INVALID_ARG, "%s: temperature must be positive and finite", fn);
+    if (!(top_p > 0.0f && top_p <= 1.0f))
+      return fail(SPH_E_INVALID_ARG, "%s: top_p must be in (0, 1]", fn);
+  }
+  if (d_end > 0 && (ldh < d_end || ldw < d_end))
+    return fail(SPH_E_INVALID_ARG, "%s: row strides (ldh=%lld, ldw=%lld) below d_end=%lld", fn,
+                (long long)ldh, (long long)ldw, (long long)d_end);
+  const int64_t k = rows_per_session - 1;
+  if (!subset) return fail(SPH_E_INVALID_ARG, "%s: subset is NULL", fn);
+  if (M == 0) return ok();
+  if (!q || !scale) return fail(SPH_E_INVALID_ARG, "%s: q/scale is NULL", fn);
+  if (d_end > 0 && (!h_end || !w_end)) return fail(SPH_E_INVALID_ARG, "%s: h_end/w_end is NULL", fn);
+  if (k > 0 && !drafts) return fail(SPH_E_INVALID_ARG, "%s: drafts is NULL with k=%lld", fn, (long long)k);
+  if (!tokens_out || !accept_len_out)
+    return fail(SPH_E_INVALID_ARG, "%s: tokens_out/accept_len_out is NULL", fn);
+  const int64_t n = subset->n;
+  const size_t need = fuse_ws(M, n, mode);
+  if (!workspace || ws_bytes < need)
+    return fail(SPH_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                workspace ? ws_bytes : (size_t)0);
+  if (mode == SPH_SAMPLE) return fail(SPH_E_UNSUPPORTED, "%s: sampling is not built yet", fn);
+  if (d_end > 0 && ((reinterpret_cast<uintptr_t>(w_end) & 15) != 0 || ldw % 8 != 0 || d_end % 8 != 0))
+    return fail(SPH_E_UNSUPPORTED, "%s: endpoint weight rows must be 16-byte aligned and d_end a multiple of 8",
+                fn);
+  const int64_t Kp = round_up(d_end, 8);
+  int mr = sph::kGemvMaxRows;
+  if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
+  if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_end=%lld too large", fn, (long long)d_end);
+
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint64_t* best = reinterpret_cast<uint64_t*>(ws);
+  const int lpr = sph::gemv_lpr(sph::kEpiFuse, (int)d_end, 0);
+  const int rpi = sph::gemv_rows_per_iter(sph::kEpiFuse, lpr);
+  const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
+  for (int64_t m0 = 0; m0 < M; m0 += mr) {
+    const int rows = (int)std::min<int64_t>(mr, M - m0);
+    sph::GemvArgs a{};
+    a.h = static_cast<const uint16_t*>(h_end) + (d_end > 0 ? m0 * ldh : 0);
+    a.ldh = ldh;
+    a.K = (int)d_end;
+    a.Kp = (int)Kp;
+    a.w = static_cast<const uint8_t*>(w_end);
+    a.ldw_bytes = ldw * 2;
+    a.ids = subset->d_ids;
+    a.n = (int)n;
+    a.nblk = nblk;
+    a.q = q + m0 * n;
+    a.qscale = scale + m0;
+    a.f = fused_out ? fused_out + m0 * n : nullptr;
+    a.best_part = best + m0 * sph::kMaxBlocks;
+    hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, lpr, a, s); });
+    if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
+  }
+  hipError_t e = traced("fuse_final_greedy", s, [&] {
+    return sph::launch_final_greedy(best, nblk, subset->d_ids, (int)n, (int)n_sessions,
+                                    (int)rows_per_session, drafts, tokens_out, accept_len_out, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "greedy finaliser launch");
+  return ok();
+}
+
+int sph_trace_start(int capacity) {
+  if (capacity < 1 || capacity > (1 << 22))
+    return fail(SPH_E_INVALID_ARG, "sph_trace_start: capacity %d out of range", capacity);
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  trace_free_locked();
+  g_trace.reserve((size_t)capacity);
+  for (int i = 0; i < capacity; ++i) {
+    TraceSlot t{nullptr, nullptr, nullptr};
+    hipError_t e = hipEventCreate(&t.start);
+    if (e == hipSuccess) {
+      e = hipEventCreate(&t.stop);
+      if (e != hipSuccess) (void)hipEventDestroy(t.start);
+    }
+    if (e != hipSuccess) {
+      trace_free_locked();
+      return hip_fail(e, "sph_trace_start: hipEventCreate");
+    }
+    g_trace.push_back(t);
+  }
+  g_tracing = true;
+  return ok();
+}
+
+int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  g_tracing = false;
+  const size_t used = g_trace_used;
+  int rc = SPH_OK;
+  for (size_t i = 0; i < used; ++i) {
+    hipError_t e = hipEventSynchronize(g_trace[i].stop);
+    float ms = 0.0f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, g_trace[i].start, g_trace[i].stop);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "sph_trace_stop: reading events");
+      break;
+    }
+    if (out && (int)i < max_records) {
+      std::memset(out[i].kernel, 0, SPH_TRACE_NAME_LEN);
+      std::strncpy(out[i].kernel, g_trace[i].name, SPH_TRACE_NAME_LEN - 1);
+      out[i].ms = ms;
+    }
+  }
+  if (n_out) *n_out = (int)used;
+  trace_free_locked();
+  return rc == SPH_OK ? ok() : rc;
+}
+
+}  // extern "C"

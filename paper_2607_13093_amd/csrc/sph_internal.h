@@ -1,0 +1,57 @@
+// Internal declarations shared by the host layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sph {
+
+// Per-block partial results are stored [M][kMaxBlocks]; the skinny kernels
+// never launch more column blocks than this.
+constexpr int kMaxBlocks = 1024;
+// Largest LDS footprint the skinny kernels give to the staged rows of h.
+constexpr int kGemvLdsBytes = 60 * 1024;
+// Largest row count handled by one skinny launch.
+constexpr int kGemvMaxRows = 8;
+
+// Arguments of the skinny (VALU) gathered projection.  One launch covers up
+// to kGemvMaxRows rows of h and every subset id.
+struct GemvArgs {
+  const uint16_t* h;      // bf16 [rows, ldh]
+  int64_t ldh;
+  int K;                  // reduction length (d_cloud or d_end)
+  int Kp;                 // K rounded up to the weight chunk (8 bf16 / 16 fp8)
+  const uint8_t* w;       // weight rows, vocab-major
+  int64_t ldw_bytes;      // row stride of w in bytes
+  const float* wscale;    // fp32 [V] for fp8 weights, else null
+  const int32_t* ids;     // subset ids [n]
+  int n;
+  int nblk;               // column blocks of this launch (stride of the partials)
+  // cloud epilogue
+  const float* bias;      // fp32 [V] or null
+  float clip;
+  float* z;               // fp32 [rows, n]
+  float* amax_part;       // fp32 [rows, kMaxBlocks]
+  // fuse epilogue
+  const int8_t* q;        // int8 [rows, n]
+  const float* qscale;    // fp32 [rows]
+  float* f;               // fp32 [rows, n] or null
+  uint64_t* best_part;    // argmax keys [rows, kMaxBlocks]
+};
+
+enum Epilogue { kEpiCloud = 0, kEpiFuse = 1 };
+
+// Launchers (return the HIP launch status).
+hipError_t launch_gemv(int epi, int wtype, int rows, int lpr, const GemvArgs& a, hipStream_t s);
+int gemv_rows_per_iter(int epi, int lpr);
+int gemv_lpr(int epi, int K, int wtype);
+
+hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
+                           float clip, int8_t* q, float* scale, hipStream_t s);
+
+hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_t* ids, int n,
+                               int n_sessions, int R, const int32_t* drafts,
+                               int32_t* tokens, int32_t* accept, hipStream_t s);
+
+}  // namespace sph

@@ -1,0 +1,143 @@
+"""The C-ABI library: it loads, exports what include/sph.h declares, and its
+host-side validation rejects bad arguments before touching any device."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_13093_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "sph.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sph_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared_functions()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with sph.h"
+
+
+def test_abi_version(lib):
+    assert lib.sph_abi_version() == 1
+    assert lib.sph_last_error() == b""
+
+
+def _create(lib, ids, vocab):
+    arr = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
+    out = ctypes.c_void_p(123)
+    rc = lib.sph_subset_create(arr.ctypes.data if arr.size else None, arr.size, vocab, None, out)
+    return rc, out
+
+
+@pytest.mark.parametrize("ids,vocab,code,msg", [
+    ([3, 2, 5], 10, _lib.SPH_E_SUBSET, "ascending"),
+    ([1, 1, 2], 10, _lib.SPH_E_SUBSET, "ascending"),
+    ([0, 4, 10], 10, _lib.SPH_E_SUBSET, "outside"),
+    ([-1, 4], 10, _lib.SPH_E_SUBSET, "outside"),
+    (list(range(11)), 10, _lib.SPH_E_SUBSET, "size"),
+    ([1, 2], 0, _lib.SPH_E_INVALID_ARG, "vocab"),
+])
+def test_subset_validation(lib, ids, vocab, code, msg):
+    rc, out = _create(lib, ids, vocab)
+    assert rc == code
+    assert msg in lib.sph_last_error().decode()
+    assert out.value is None  # nothing created
+
+
+def test_subset_empty_and_null(lib):
+    out = ctypes.c_void_p()
+    one = np.zeros(1, np.int32)
+    assert lib.sph_subset_create(one.ctypes.data, 0, 10, None, out) == _lib.SPH_E_SUBSET
+    assert lib.sph_subset_create(None, 3, 10, None, out) == _lib.SPH_E_INVALID_ARG
+    assert lib.sph_subset_create(one.ctypes.data, 1, 10, None, None) == _lib.SPH_E_INVALID_ARG
+    assert lib.sph_subset_create_full(0, None, out) == _lib.SPH_E_INVALID_ARG
+    assert lib.sph_subset_size(None, None, None) == _lib.SPH_E_INVALID_ARG
+    lib.sph_subset_destroy(None)
+    assert lib.sph_cloud_partial_workspace(5, None) == 0
+    assert lib.sph_fuse_verify_workspace(5, None, 0) == 0
+
+
+def _cloud(lib, **kw):
+    a = dict(h=1, ldh=64, M=3, d=64, w=16, ldw=64, wtype=_lib.SPH_W_BF16, ws_scale=None,
+             bias=None, subset=None, clip=30.0, q=1, s=1, z=None, work=1, nbytes=0)
+    a.update(kw)
+    return lib.sph_cloud_partial(a["h"], a["ldh"], a["M"], a["d"], a["w"], a["ldw"], a["wtype"],
+                                 a["ws_scale"], a["bias"], a["subset"], a["clip"], a["q"], a["s"],
+                                 a["z"], a["work"], a["nbytes"], None)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(M=-1), "M=-1"),
+    (dict(d=-4), "d_cloud"),
+    (dict(wtype=7), "weight type"),
+    (dict(wtype=_lib.SPH_W_FP8_E4M3), "w_row_scale"),
+    (dict(ws_scale=64), "only for fp8"),
+    (dict(clip=0.0), "clip_c"),
+    (dict(clip=float("inf")), "clip_c"),
+    (dict(clip=float("nan")), "clip_c"),
+    (dict(ldh=32), "row strides"),
+    (dict(ldw=32), "row strides"),
+    (dict(), "subset is NULL"),
+])
+def test_cloud_partial_validation(lib, kw, msg):
+    assert _cloud(lib, **kw) == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+
+
+def _fuse(lib, **kw):
+    a = dict(q=1, s=1, h=1, ldh=64, d=64, w=16, ldw=64, subset=None, S=2, R=3, drafts=1,
+             mode=_lib.SPH_GREEDY, temp=1.0, top_p=1.0, seed=0, tok=1, acc=1, f=None,
+             work=1, nbytes=0)
+    a.update(kw)
+    return lib.sph_fuse_verify(a["q"], a["s"], a["h"], a["ldh"], a["d"], a["w"], a["ldw"],
+                               a["subset"], a["S"], a["R"], a["drafts"], a["mode"], a["temp"],
+                               a["top_p"], a["seed"], a["tok"], a["acc"], a["f"], a["work"],
+                               a["nbytes"], None)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(S=-1), "n_sessions"),
+    (dict(R=0), "rows_per_session"),
+    (dict(R=5000), "rows_per_session"),
+    (dict(d=-1), "d_end"),
+    (dict(mode=9), "mode"),
+    (dict(mode=_lib.SPH_SAMPLE, temp=0.0), "temperature"),
+    (dict(mode=_lib.SPH_SAMPLE, temp=float("nan")), "temperature"),
+    (dict(mode=_lib.SPH_SAMPLE, top_p=0.0), "top_p"),
+    (dict(mode=_lib.SPH_SAMPLE, top_p=1.5), "top_p"),
+    (dict(ldh=16), "row strides"),
+    (dict(), "subset is NULL"),
+])
+def test_fuse_verify_validation(lib, kw, msg):
+    assert _fuse(lib, **kw) == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+
+
+def test_error_string_is_thread_local(lib):
+    import threading
+    assert _cloud(lib, M=-1) == _lib.SPH_E_INVALID_ARG
+    seen = {}
+
+    def other():
+        seen["msg"] = lib.sph_last_error()
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen["msg"] == b""
+    assert b"M=-1" in lib.sph_last_error()

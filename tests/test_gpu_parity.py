@@ -1,0 +1,206 @@
+"""GPU parity of libsph against the CPU oracle (staged: see tests/parity.py).
+
+Every test here calls the HIP library through its C ABI; none has a CPU
+fallback.  Case names are printed (and flushed) before each GPU step.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_13093_amd as sph
+from paper_2607_13093_amd import _lib
+from synth import (CONFIGS, Config, make_drafts, make_workload, plant_masked_supertoken,
+                   scale_rows_bf16)
+
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag=""):
+    """Full staged parity A-E of one greedy workload; returns the stats."""
+    cfg = wl.cfg
+    h_bits = wl.h_bits if h_bits is None else h_bits
+    w_end_bits = wl.w_end_bits if w_end_bits is None else w_end_bits
+    w_cloud_bits = wl.w_cloud_bits if w_cloud_bits is None else w_cloud_bits
+    orc = oracle.cloud_call(h_bits, cfg.d_end, wl.subset, cfg.clip_c, w_cloud_bits=w_cloud_bits,
+                            w_cloud_codes=wl.w_cloud_codes, w_cloud_scale=wl.w_cloud_scale,
+                            bias=wl.bias, with_abs=True)
+    ep = oracle.endpoint_call(orc["q"], orc["scale"], h_bits, cfg.d_end, wl.subset, w_end_bits,
+                              cfg.sessions, cfg.rows_per_session,
+                              drafts=np.zeros((cfg.sessions, cfg.k), np.int32))
+    drafts = make_drafts(cfg, ep["tokens"], wl.subset) if cfg.k else None
+
+    say(f"[gpu] {tag or cfg.name}: cloud_partial M={cfg.M} d={cfg.d} d_end={cfg.d_end} "
+        f"n={len(wl.subset)} wtype={cfg.wtype}")
+    dw = P.DeviceWorkload(wl, h_bits=h_bits, w_end_bits=w_end_bits, w_cloud_bits=w_cloud_bits)
+    q, s, z = dw.cloud()
+    torch.cuda.synchronize()
+    qh, sh, zh = P.host(q), P.host(s), P.host(z)
+    stats = {"A": P.stage_a(zh, orc)}
+    P.stage_b(zh, qh, sh, cfg.clip_c)
+    stats["C"] = P.stage_c(qh, sh, orc)
+
+    say(f"[gpu] {tag or cfg.name}: fuse_verify sessions={cfg.sessions} R={cfg.rows_per_session}")
+    tok, acc, f = dw.fuse(q, s, drafts)
+    torch.cuda.synchronize()
+    th, ah, fh = P.host(tok), P.host(acc), P.host(f)
+    wl2 = _with(wl, h_bits=h_bits, w_end_bits=w_end_bits)
+    stats["D"] = P.stage_d_greedy(qh, sh, fh, th, ah, wl2, drafts)
+    stats["E"] = P.stage_e_greedy(qh, sh, th, ah, orc, wl2, drafts)
+    say(f"[gpu] {tag or cfg.name}: ok {stats}")
+    return stats, (qh, sh, zh, th, ah, fh)
+
+
+def _with(wl, **kw):
+    import copy
+    w2 = copy.copy(wl)
+    for k, v in kw.items():
+        setattr(w2, k, v)
+    return w2
+
+
+# ---------------------------------------------------------------------------
+# the benchmark workloads
+# ---------------------------------------------------------------------------
+
+def test_tiny_full_pipeline():
+    run_greedy_case(make_workload(CONFIGS["tiny"]))
+
+
+def test_decode_full_pipeline():
+    run_greedy_case(make_workload(CONFIGS["decode"]))
+
+
+# ---------------------------------------------------------------------------
+# shapes: ragged tails, row groups, d_end = 0, bias, k = 0
+# ---------------------------------------------------------------------------
+
+RAGGED = [
+    # (sessions, R, d, d_end, V, n)
+    (1, 1, 64, 8, 300, 1),
+    (1, 2, 72, 16, 500, 7),
+    (1, 7, 520, 40, 3000, 1001),
+    (2, 4, 1032, 8, 4000, 2500),
+    (3, 3, 264, 0, 2000, 777),      # d_end = 0: the cloud computes the whole head
+    (13, 1, 136, 64, 1000, 333),    # 13 rows: two row groups
+    (4, 5, 4104, 520, 6000, 4097),  # d_end > 512 and a ragged subset
+]
+
+
+@pytest.mark.parametrize("shape", RAGGED, ids=[f"S{s}R{r}d{d}de{de}V{v}n{n}" for s, r, d, de, v, n in RAGGED])
+def test_ragged_shapes(shape):
+    S, R, d, de, V, n = shape
+    cfg = Config("ragged", 10 + sum(shape), d=d, d_end=de, vocab=V, n_sub=n, subset_kind="choice",
+                 sessions=S, rows_per_session=R)
+    run_greedy_case(make_workload(cfg), tag=f"ragged {shape}")
+
+
+def test_bias_is_added_once_on_the_cloud():
+    cfg = CONFIGS["tiny"].replace(name="tiny_bias", with_bias=True)
+    run_greedy_case(make_workload(cfg), tag="bias")
+
+
+def test_full_vocabulary_plan():
+    cfg = Config("full_small", 21, d=256, d_end=32, vocab=3000, n_sub=3000, subset_kind="full",
+                 sessions=2, rows_per_session=4)
+    run_greedy_case(make_workload(cfg), tag="full-vocab")
+
+
+def test_clip_zero_and_masked_supertoken_rows():
+    cfg = Config("edge", 22, d=512, d_end=64, vocab=8192, n_sub=4096, subset_kind="perm",
+                 sessions=2, rows_per_session=3)
+    wl = make_workload(cfg)
+    h = scale_rows_bf16(wl.h_bits, [0, 4], 10.0)     # clipped rows
+    h[2] = 0                                          # a zero row
+    we, wc = wl.w_end_bits.copy(), wl.w_cloud_bits.copy()
+    vid = plant_masked_supertoken(we, wc, h, 1, wl.subset)
+    stats, (q, s, z, tok, acc, f) = run_greedy_case(wl, h_bits=h, w_end_bits=we, w_cloud_bits=wc,
+                                                    tag="clip/zero/planted")
+    assert s[0] == np.float32(30.0) / np.float32(127.0) and s[4] == s[0]
+    assert s[2] == 0 and not q[2].any()
+    assert tok[2] == wl.subset[0]          # an all-zero row ties everywhere: lowest id wins
+    assert vid not in tok
+
+
+# ---------------------------------------------------------------------------
+# fp8 cloud weights
+# ---------------------------------------------------------------------------
+
+def test_fp8_decode_of_every_code_through_the_abi():
+    # W row v holds code v in column 0 and zeros elsewhere; h is the unit vector e_0,
+    # so z[v] = decode(code_v) * 1.0 exactly.  NaN codes are left out.
+    codes = np.array([c for c in range(256) if (c & 0x7F) != 0x7F], dtype=np.uint8)
+    V, K = codes.size, 16
+    w = np.zeros((V, K), np.uint8)
+    w[:, 0] = codes
+    h = np.zeros((1, K), np.uint16)
+    h[0, 0] = 0x3F80  # bf16 1.0
+    say("[gpu] fp8 decode: all finite E4M3 codes")
+    sub = sph.Subset(np.arange(V), vocab=V)
+    q, s, z = sph.cloud_partial(P.to_dev(h, torch.bfloat16), P.to_dev(w, torch.uint8), sub, 1000.0,
+                                w_row_scale=torch.ones(V, device="cuda"), want_z=True)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(P.host(z)[0], oracle.decode_e4m3(codes).astype(np.float32))
+
+
+def test_fp8_cloud_partial_skinny():
+    cfg = Config("fp8_small", 23, d=1056, d_end=32, vocab=5000, n_sub=2048, subset_kind="choice",
+                 sessions=1, rows_per_session=5, wtype="fp8")
+    run_greedy_case(make_workload(cfg), tag="fp8 skinny")
+
+
+# ---------------------------------------------------------------------------
+# edge cases of the interface
+# ---------------------------------------------------------------------------
+
+def test_k_zero_and_empty_batch():
+    cfg = Config("k0", 24, d=128, d_end=16, vocab=700, n_sub=300, subset_kind="choice",
+                 sessions=3, rows_per_session=1)
+    stats, (q, s, z, tok, acc, f) = run_greedy_case(make_workload(cfg), tag="k=0")
+    assert (acc == 0).all()
+    dw = P.DeviceWorkload(make_workload(cfg))
+    say("[gpu] empty batch")
+    q0, s0, _ = sph.cloud_partial(dw.h[:0, 16:], dw.w_cloud, dw.subset, 30.0)
+    t0, a0, _ = sph.fuse_verify(q0, s0, dw.h[:0, :16], dw.w_end, dw.subset, 0, 1, None)
+    torch.cuda.synchronize()
+    assert q0.shape == (0, 300) and t0.shape == (0,) and a0.shape == (0,)
+
+
+def test_workspace_and_alignment_errors():
+    cfg = Config("err", 25, d=128, d_end=16, vocab=700, n_sub=300, subset_kind="choice",
+                 sessions=1, rows_per_session=3)
+    dw = P.DeviceWorkload(make_workload(cfg))
+    say("[gpu] error paths")
+    small = torch.empty(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(sph.SphError) as e:
+        sph.cloud_partial(dw.h[:, 16:], dw.w_cloud, dw.subset, 30.0, workspace=small)
+    assert e.value.code == _lib.SPH_E_WORKSPACE
+    with pytest.raises(sph.SphError) as e:
+        sph.cloud_partial(dw.h[:, 16:], dw.w_cloud.view(-1)[1:1 + 699 * 112].view(699, 112),
+                          dw.subset, 30.0)
+    assert e.value.code == _lib.SPH_E_UNSUPPORTED
+
+
+def test_repeat_runs_are_bit_identical():
+    wl = make_workload(CONFIGS["tiny"])
+    dw = P.DeviceWorkload(wl)
+    say("[gpu] determinism")
+    outs = []
+    for _ in range(3):
+        q, s, z = dw.cloud()
+        tok, acc, f = dw.fuse(q, s, np.zeros((1, 2), np.int32))
+        torch.cuda.synchronize()
+        outs.append([P.host(x) for x in (q, s, z, tok, acc, f)])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            np.testing.assert_array_equal(a, b)
