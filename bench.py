@@ -40,7 +40,21 @@ def parse():
     p.add_argument("--workload", default="decode")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the oracle's CPU baseline run (0 to skip)")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run plain device copies of MIB MiB (to scale rocprofv3 "
+                        "FETCH_SIZE / WRITE_SIZE counters), then exit")
     return p.parse_args()
+
+
+def copy_calibration(mib):
+    import torch
+    src = torch.empty(mib << 20, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": mib << 20, "copies": 5}), flush=True)
 
 
 def algorithmic_bytes(cfg, n):
@@ -107,6 +121,9 @@ def cpu_baseline(wl, seconds):
 
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path", file=sys.stderr)
@@ -167,19 +184,27 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    per_step = 4  # launches per step on the skinny path: gemv, quantise, gemv, finalise
-    sph.trace_start(per_step * args.steps + 16)
     stream = torch.cuda.current_stream(dev)
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i)
-    t_stop.record(stream)
-    torch.cuda.synchronize()
-    recs = sph.trace_collect(per_step * args.steps + 16)
-    ms_step = t_start.elapsed_time(t_stop) / args.steps
+
+    def timed_loop():
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_stop = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for i in range(args.steps):
+            step(i)
+        t_stop.record(stream)
+        torch.cuda.synchronize()
+        return t_start.elapsed_time(t_stop) / args.steps
+
+    # Timed region: K steps, no instrumentation.
+    ms_step = timed_loop()
+    # Kernel durations: the same K steps again with the library's trace on
+    # (HIP events recorded on the launch stream around every kernel).
+    cap = 16 * args.steps + 16
+    sph.trace_start(cap)
+    ms_step_traced = timed_loop()
+    recs = sph.trace_collect(cap)
 
     by = {}
     for name, ms in recs:
@@ -224,6 +249,7 @@ def main():
             "kernel_source_sha256_16": digest,
         },
         "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
+        "ms_per_step_traced": ms_step_traced,
     }
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)

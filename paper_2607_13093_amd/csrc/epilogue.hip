@@ -74,31 +74,36 @@ __device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long x,
 }
 
 constexpr int kMaxRowsPerSession = 1024;
+constexpr int kFinalWaves = 16;  // rows of a session reduced in parallel
 
-// One block per session: fold the per-block argmax keys of each of its rows
-// into the greedy token (ties to the lowest subset position = lowest id),
-// then count the drafts that match the verification rows in order
-// (Section 5.5, Algorithm 1 verification step).
-__global__ __launch_bounds__(256) void k_final_greedy(const unsigned long long* __restrict__ best,
-                                                      int nblk, const int32_t* __restrict__ ids,
-                                                      int n, int R,
-                                                      const int32_t* __restrict__ drafts,
-                                                      int32_t* __restrict__ tokens,
-                                                      int32_t* __restrict__ accept) {
+// One block per session, one wave per verification row: fold the row's
+// per-block argmax keys (every lane loads its share of up to kMaxBlocks keys
+// at once) into the greedy token, ties to the lowest subset position = the
+// lowest id; then count the drafts that match the verification rows in
+// order (Section 5.5, Algorithm 1 verification step).
+__global__ __launch_bounds__(64 * kFinalWaves) void k_final_greedy(
+    const unsigned long long* __restrict__ best, int nblk, const int32_t* __restrict__ ids, int n,
+    int R, const int32_t* __restrict__ drafts, int32_t* __restrict__ tokens,
+    int32_t* __restrict__ accept) {
+  constexpr int PER_LANE = kMaxBlocks / 64;
   const int s = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ int32_t s_tok[kMaxRowsPerSession];
-  for (int r = wave; r < R; r += 4) {
+  for (int r = wave; r < R; r += kFinalWaves) {
     const int64_t m = (int64_t)s * R + r;
-    unsigned long long k = 0ull;
-    for (int i = lane; i < nblk; i += 64) {
-      const unsigned long long x = best[m * kMaxBlocks + i];
-      k = x > k ? x : k;
+    unsigned long long x[PER_LANE];
+#pragma unroll
+    for (int t = 0; t < PER_LANE; ++t) {
+      const int i = lane + 64 * t;
+      x[t] = i < nblk ? best[m * kMaxBlocks + i] : 0ull;
     }
+    unsigned long long k = x[0];
+#pragma unroll
+    for (int t = 1; t < PER_LANE; ++t) k = x[t] > k ? x[t] : k;
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
-      const unsigned long long x = shfl_xor_u64(k, o);
-      k = x > k ? x : k;
+      const unsigned long long y = shfl_xor_u64(k, o);
+      k = y > k ? y : k;
     }
     if (lane == 0) {
       // every position of the row produced a key, so pos < n; the clamp only
@@ -121,8 +126,9 @@ __global__ __launch_bounds__(256) void k_final_greedy(const unsigned long long* 
 hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_t* ids, int n,
                                int n_sessions, int R, const int32_t* drafts, int32_t* tokens,
                                int32_t* accept, hipStream_t s) {
-  if (R > kMaxRowsPerSession || n < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_final_greedy, dim3(n_sessions), dim3(256), 0, s,
+  if (R > kMaxRowsPerSession || n < 1 || nblk > kMaxBlocks) return hipErrorInvalidValue;
+  const int waves = R < kFinalWaves ? R : kFinalWaves;
+  hipLaunchKernelGGL(k_final_greedy, dim3(n_sessions), dim3(64 * waves), 0, s,
                      reinterpret_cast<const unsigned long long*>(best_part), nblk, ids, n, R,
                      drafts, tokens, accept);
   return hipGetLastError();

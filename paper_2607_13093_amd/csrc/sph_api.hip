@@ -241,7 +241,10 @@ int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_clo
   float* z = z_out ? z_out : reinterpret_cast<float*>(ws);
   float* amax = reinterpret_cast<float*>(ws + align256((size_t)M * n * 4));
 
-  const int rpi = sph::gemv_rows_per_iter(sph::kEpiCloud, 64);
+  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
+    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
+  const int lpr = sph::gemv_lpr((int)d_cloud, wtype);
+  const int rpi = sph::gemv_rows_per_iter(lpr);
   const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
   for (int64_t m0 = 0; m0 < M; m0 += mr) {
     const int rows = (int)std::min<int64_t>(mr, M - m0);
@@ -260,7 +263,7 @@ int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_clo
     a.clip = clip_c;
     a.z = z + m0 * n;
     a.amax_part = amax + m0 * sph::kMaxBlocks;
-    hipError_t e = traced("cloud_gemv", s, [&] { return sph::launch_gemv(sph::kEpiCloud, wtype, rows, 64, a, s); });
+    hipError_t e = traced("cloud_gemv", s, [&] { return sph::launch_gemv(sph::kEpiCloud, wtype, rows, a, s); });
     if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
   }
   hipError_t e = traced("cloud_quantize", s, [&] {
@@ -321,8 +324,10 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint64_t* best = reinterpret_cast<uint64_t*>(ws);
-  const int lpr = sph::gemv_lpr(sph::kEpiFuse, (int)d_end, 0);
-  const int rpi = sph::gemv_rows_per_iter(sph::kEpiFuse, lpr);
+  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
+    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
+  const int lpr = sph::gemv_lpr((int)d_end, 0);
+  const int rpi = sph::gemv_rows_per_iter(lpr);
   const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
   for (int64_t m0 = 0; m0 < M; m0 += mr) {
     const int rows = (int)std::min<int64_t>(mr, M - m0);
@@ -340,7 +345,7 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
     a.qscale = scale + m0;
     a.f = fused_out ? fused_out + m0 * n : nullptr;
     a.best_part = best + m0 * sph::kMaxBlocks;
-    hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, lpr, a, s); });
+    hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, a, s); });
     if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
   }
   hipError_t e = traced("fuse_final_greedy", s, [&] {

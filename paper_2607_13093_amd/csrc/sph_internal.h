@@ -14,6 +14,8 @@ constexpr int kMaxBlocks = 1024;
 constexpr int kGemvLdsBytes = 60 * 1024;
 // Largest row count handled by one skinny launch.
 constexpr int kGemvMaxRows = 8;
+// Largest contiguous share of subset positions one skinny block stages.
+constexpr int kGemvMaxIdsPerBlock = 2048;
 
 // Arguments of the skinny (VALU) gathered projection.  One launch covers up
 // to kGemvMaxRows rows of h and every subset id.
@@ -27,7 +29,9 @@ struct GemvArgs {
   const float* wscale;    // fp32 [V] for fp8 weights, else null
   const int32_t* ids;     // subset ids [n]
   int n;
-  int nblk;               // column blocks of this launch (stride of the partials)
+  int nblk;               // partial slots per row the consumer reads (<= kMaxBlocks);
+                          // the launch may use fewer blocks and zero-fills the rest
+  int rows_per_block;     // set by the launcher: contiguous positions per block
   // cloud epilogue
   const float* bias;      // fp32 [V] or null
   float clip;
@@ -43,9 +47,9 @@ struct GemvArgs {
 enum Epilogue { kEpiCloud = 0, kEpiFuse = 1 };
 
 // Launchers (return the HIP launch status).
-hipError_t launch_gemv(int epi, int wtype, int rows, int lpr, const GemvArgs& a, hipStream_t s);
-int gemv_rows_per_iter(int epi, int lpr);
-int gemv_lpr(int epi, int K, int wtype);
+hipError_t launch_gemv(int epi, int wtype, int rows, const GemvArgs& a, hipStream_t s);
+int gemv_rows_per_iter(int lpr);
+int gemv_lpr(int K, int wtype);
 
 hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
                            float clip, int8_t* q, float* scale, hipStream_t s);

@@ -94,6 +94,7 @@ RAGGED = [
     (3, 3, 264, 0, 2000, 777),      # d_end = 0: the cloud computes the whole head
     (13, 1, 136, 64, 1000, 333),    # 13 rows: two row groups
     (4, 5, 4104, 520, 6000, 4097),  # d_end > 512 and a ragged subset
+    (3, 1, 8192, 512, 3000, 2999),  # four passes over each cloud row
 ]
 
 
@@ -204,3 +205,29 @@ def test_repeat_runs_are_bit_identical():
     for o in outs[1:]:
         for a, b in zip(outs[0], o):
             np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("M", [5, 20])
+def test_stale_workspace_contents_are_never_read(M):
+    # Poisoned workspaces (huge values / max keys) must not change any result.
+    cfg = Config("poison", 26, d=4104, d_end=520, vocab=6000, n_sub=4097, subset_kind="choice",
+                 sessions=M // 5, rows_per_session=5)
+    wl = make_workload(cfg)
+    dw = P.DeviceWorkload(wl)
+    say(f"[gpu] poisoned workspace M={M}")
+    ref_c = sph.cloud_partial(dw.h[:, 520:], dw.w_cloud, dw.subset, 30.0, want_z=True,
+                              workspace=torch.zeros(sph.cloud_partial_workspace(M, dw.subset),
+                                                    dtype=torch.uint8, device="cuda"))
+    drafts = torch.zeros((cfg.sessions, cfg.k), dtype=torch.int32, device="cuda")
+    ref_f = sph.fuse_verify(ref_c[0], ref_c[1], dw.h[:, :520], dw.w_end, dw.subset, cfg.sessions, 5,
+                            drafts, workspace=torch.zeros(sph.fuse_verify_workspace(M, dw.subset),
+                                                          dtype=torch.uint8, device="cuda"))
+    for fill in (0x7F, 0xFF):
+        wc = torch.full((sph.cloud_partial_workspace(M, dw.subset),), fill, dtype=torch.uint8, device="cuda")
+        wf = torch.full((sph.fuse_verify_workspace(M, dw.subset),), fill, dtype=torch.uint8, device="cuda")
+        got_c = sph.cloud_partial(dw.h[:, 520:], dw.w_cloud, dw.subset, 30.0, want_z=True, workspace=wc)
+        got_f = sph.fuse_verify(got_c[0], got_c[1], dw.h[:, :520], dw.w_end, dw.subset, cfg.sessions, 5,
+                                drafts, workspace=wf)
+        torch.cuda.synchronize()
+        for a, b in zip(list(ref_c) + list(ref_f[:2]), list(got_c) + list(got_f[:2])):
+            np.testing.assert_array_equal(P.host(a), P.host(b))
