@@ -28,6 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16; fp8 weights are widened to bf16 before the MFMA
 N_COPIES = 3
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "cloud_gemv_decode_traffic.txt")
 
@@ -91,7 +92,8 @@ def read_traffic(digest):
 
 
 def cpu_baseline(wl, seconds):
-    """The oracle, as it stands, on whole decode steps until `seconds` pass."""
+    """The oracle, as it stands, on whole steps (one session's rows for the
+    batched workloads) until `seconds` pass."""
     import numpy as np
 
     import oracle
@@ -101,22 +103,26 @@ def cpu_baseline(wl, seconds):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         cores = len(os.sched_getaffinity(0))
-    drafts = np.zeros((cfg.sessions, cfg.k), np.int32)
+    sessions = cfg.sessions if cfg.M <= 8 else 1
+    h = wl.h_bits[:sessions * cfg.rows_per_session]
+    drafts = np.zeros((sessions, cfg.k), np.int32)
     reps = 0
     t0 = time.perf_counter()
     while True:
-        orc = oracle.cloud_call(wl.h_bits, cfg.d_end, wl.subset, cfg.clip_c,
+        orc = oracle.cloud_call(h, cfg.d_end, wl.subset, cfg.clip_c,
                                 w_cloud_bits=wl.w_cloud_bits, w_cloud_codes=wl.w_cloud_codes,
                                 w_cloud_scale=wl.w_cloud_scale, bias=wl.bias)
-        oracle.endpoint_call(orc["q"], orc["scale"], wl.h_bits, cfg.d_end, wl.subset,
-                             wl.w_end_bits, cfg.sessions, cfg.rows_per_session, drafts=drafts)
+        oracle.endpoint_call(orc["q"], orc["scale"], h, cfg.d_end, wl.subset, wl.w_end_bits,
+                             sessions, cfg.rows_per_session, drafts=drafts, mode=cfg.mode,
+                             temperature=cfg.temperature, top_p=cfg.top_p, seed=cfg.philox_seed)
         reps += 1
         dt = time.perf_counter() - t0
         if dt >= seconds:
             break
-    return {"value": cfg.M * len(wl.subset) * reps / dt, "unit": "rows*vocab/s", "cores": cores,
+    what = "whole steps" if sessions == cfg.sessions else f"steps of {sessions} session ({h.shape[0]} rows)"
+    return {"value": h.shape[0] * len(wl.subset) * reps / dt, "unit": "rows*vocab/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"{reps} whole {cfg.name} steps (cloud + endpoint oracle, fp64 NumPy), {dt:.1f} s"}
+            "sample": f"{reps} {what} of {cfg.name} (cloud + endpoint oracle, fp64 NumPy), {dt:.1f} s"}
 
 
 def main():
@@ -209,11 +215,27 @@ def main():
     by = {}
     for name, ms in recs:
         by.setdefault(name, []).append(ms)
-    gemv_ms = float(np.mean(by["cloud_gemv"]))
-    nbytes = algorithmic_bytes(cfg, n)
-    achieved = nbytes / (gemv_ms * 1e-3) / 1e9
-    digest = source_digest()
-    traffic = read_traffic(digest)
+    if "cloud_mfma" in by:
+        kern = "cloud_mfma"
+        k_ms = float(np.mean(by[kern]))
+        flops = 2.0 * M * n * cfg.d_cloud
+        achieved = flops / (k_ms * 1e-3) / 1e12
+        roof = {"kernel": kern, "bound": "mfma", "achieved": achieved,
+                "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                "algorithmic_flops_per_launch": flops,
+                "algorithmic_bytes_per_launch": algorithmic_bytes(cfg, n), "avg_launch_ms": k_ms}
+    else:
+        kern = "cloud_gemv"
+        k_ms = float(np.mean(by[kern]))
+        nbytes = algorithmic_bytes(cfg, n)
+        achieved = nbytes / (k_ms * 1e-3) / 1e9
+        digest = source_digest()
+        roof = {"kernel": kern, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                "traffic": read_traffic(digest) if args.workload == "decode" else None,
+                "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": k_ms,
+                "kernel_source_sha256_16": digest}
 
     out = {
         "metric": "split-head rows*vocab/s",
@@ -236,18 +258,7 @@ def main():
             "subset": n,
             "payload_bytes_per_row": n + 4,
         },
-        "roofline": {
-            "kernel": "cloud_gemv",
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": nbytes,
-            "avg_launch_ms": gemv_ms,
-            "kernel_source_sha256_16": digest,
-        },
+        "roofline": roof,
         "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
         "ms_per_step_traced": ms_step_traced,
     }

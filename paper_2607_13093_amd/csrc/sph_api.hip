@@ -232,39 +232,62 @@ int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_clo
   if ((reinterpret_cast<uintptr_t>(w_cloud) & 15) != 0 || (ldw * wbytes) % 16 != 0 || d_cloud % epc != 0)
     return fail(SPH_E_UNSUPPORTED,
                 "%s: weight rows must be 16-byte aligned and d_cloud a multiple of %d", fn, epc);
-  int mr = sph::kGemvMaxRows;
-  if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
-  if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_cloud=%lld too large", fn, (long long)d_cloud);
+  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
+    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
 
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* z = z_out ? z_out : reinterpret_cast<float*>(ws);
   float* amax = reinterpret_cast<float*>(ws + align256((size_t)M * n * 4));
 
-  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
-    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
-  const int lpr = sph::gemv_lpr((int)d_cloud, wtype);
-  const int rpi = sph::gemv_rows_per_iter(lpr);
-  const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
-  for (int64_t m0 = 0; m0 < M; m0 += mr) {
-    const int rows = (int)std::min<int64_t>(mr, M - m0);
-    sph::GemvArgs a{};
-    a.h = static_cast<const uint16_t*>(h_cloud) + m0 * ldh;
+  // Dense path: more rows than one skinny launch covers, 16-byte aligned h rows.
+  const bool h_vec = (reinterpret_cast<uintptr_t>(h_cloud) & 15) == 0 && ldh % 8 == 0;
+  int nblk;
+  if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks) {
+    sph::MfmaArgs a{};
+    a.h = static_cast<const uint16_t*>(h_cloud);
     a.ldh = ldh;
+    a.M = (int)M;
     a.K = (int)d_cloud;
-    a.Kp = (int)Kp;
     a.w = static_cast<const uint8_t*>(w_cloud);
     a.ldw_bytes = ldw * wbytes;
     a.wscale = w_row_scale;
     a.ids = subset->d_ids;
     a.n = (int)n;
-    a.nblk = nblk;
     a.bias = bias;
     a.clip = clip_c;
-    a.z = z + m0 * n;
-    a.amax_part = amax + m0 * sph::kMaxBlocks;
-    hipError_t e = traced("cloud_gemv", s, [&] { return sph::launch_gemv(sph::kEpiCloud, wtype, rows, a, s); });
+    a.z = z;
+    a.amax_part = amax;
+    hipError_t e = traced("cloud_mfma", s, [&] { return sph::launch_mfma(sph::kEpiCloud, wtype, a, s); });
     if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
+    nblk = sph::mfma_n_tiles((int)n);
+  } else {
+    int mr = sph::kGemvMaxRows;
+    if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
+    if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_cloud=%lld too large", fn, (long long)d_cloud);
+    const int lpr = sph::gemv_lpr((int)d_cloud, wtype);
+    const int rpi = sph::gemv_rows_per_iter(lpr);
+    nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
+    for (int64_t m0 = 0; m0 < M; m0 += mr) {
+      const int rows = (int)std::min<int64_t>(mr, M - m0);
+      sph::GemvArgs a{};
+      a.h = static_cast<const uint16_t*>(h_cloud) + m0 * ldh;
+      a.ldh = ldh;
+      a.K = (int)d_cloud;
+      a.Kp = (int)Kp;
+      a.w = static_cast<const uint8_t*>(w_cloud);
+      a.ldw_bytes = ldw * wbytes;
+      a.wscale = w_row_scale;
+      a.ids = subset->d_ids;
+      a.n = (int)n;
+      a.nblk = nblk;
+      a.bias = bias;
+      a.clip = clip_c;
+      a.z = z + m0 * n;
+      a.amax_part = amax + m0 * sph::kMaxBlocks;
+      hipError_t e = traced("cloud_gemv", s, [&] { return sph::launch_gemv(sph::kEpiCloud, wtype, rows, a, s); });
+      if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
+    }
   }
   hipError_t e = traced("cloud_quantize", s, [&] {
     return sph::launch_quantize(z, amax, nblk, (int)M, (int)n, clip_c, q_out, scale_out, s);
@@ -316,37 +339,58 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   if (d_end > 0 && ((reinterpret_cast<uintptr_t>(w_end) & 15) != 0 || ldw % 8 != 0 || d_end % 8 != 0))
     return fail(SPH_E_UNSUPPORTED, "%s: endpoint weight rows must be 16-byte aligned and d_end a multiple of 8",
                 fn);
+  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
+    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
   const int64_t Kp = round_up(d_end, 8);
-  int mr = sph::kGemvMaxRows;
-  if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
-  if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_end=%lld too large", fn, (long long)d_end);
 
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint64_t* best = reinterpret_cast<uint64_t*>(ws);
-  if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
-    return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
-  const int lpr = sph::gemv_lpr((int)d_end, 0);
-  const int rpi = sph::gemv_rows_per_iter(lpr);
-  const int nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
-  for (int64_t m0 = 0; m0 < M; m0 += mr) {
-    const int rows = (int)std::min<int64_t>(mr, M - m0);
-    sph::GemvArgs a{};
-    a.h = static_cast<const uint16_t*>(h_end) + (d_end > 0 ? m0 * ldh : 0);
+  const bool h_vec = d_end == 0 || ((reinterpret_cast<uintptr_t>(h_end) & 15) == 0 && ldh % 8 == 0);
+  int nblk;
+  if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks) {
+    sph::MfmaArgs a{};
+    a.h = static_cast<const uint16_t*>(h_end);
     a.ldh = ldh;
+    a.M = (int)M;
     a.K = (int)d_end;
-    a.Kp = (int)Kp;
     a.w = static_cast<const uint8_t*>(w_end);
     a.ldw_bytes = ldw * 2;
     a.ids = subset->d_ids;
     a.n = (int)n;
-    a.nblk = nblk;
-    a.q = q + m0 * n;
-    a.qscale = scale + m0;
-    a.f = fused_out ? fused_out + m0 * n : nullptr;
-    a.best_part = best + m0 * sph::kMaxBlocks;
-    hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, a, s); });
+    a.q = q;
+    a.qscale = scale;
+    a.f = fused_out;
+    a.best_part = best;
+    hipError_t e = traced("fuse_mfma", s, [&] { return sph::launch_mfma(sph::kEpiFuse, 0, a, s); });
     if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
+    nblk = sph::mfma_n_tiles((int)n);
+  } else {
+    int mr = sph::kGemvMaxRows;
+    if (Kp > 0) mr = (int)std::min<int64_t>(mr, sph::kGemvLdsBytes / (Kp * 2));
+    if (mr < 1) return fail(SPH_E_UNSUPPORTED, "%s: d_end=%lld too large", fn, (long long)d_end);
+    const int lpr = sph::gemv_lpr((int)d_end, 0);
+    const int rpi = sph::gemv_rows_per_iter(lpr);
+    nblk = (int)std::min<int64_t>((n + rpi - 1) / rpi, sph::kMaxBlocks);
+    for (int64_t m0 = 0; m0 < M; m0 += mr) {
+      const int rows = (int)std::min<int64_t>(mr, M - m0);
+      sph::GemvArgs a{};
+      a.h = static_cast<const uint16_t*>(h_end) + (d_end > 0 ? m0 * ldh : 0);
+      a.ldh = ldh;
+      a.K = (int)d_end;
+      a.Kp = (int)Kp;
+      a.w = static_cast<const uint8_t*>(w_end);
+      a.ldw_bytes = ldw * 2;
+      a.ids = subset->d_ids;
+      a.n = (int)n;
+      a.nblk = nblk;
+      a.q = q + m0 * n;
+      a.qscale = scale + m0;
+      a.f = fused_out ? fused_out + m0 * n : nullptr;
+      a.best_part = best + m0 * sph::kMaxBlocks;
+      hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, a, s); });
+      if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
+    }
   }
   hipError_t e = traced("fuse_final_greedy", s, [&] {
     return sph::launch_final_greedy(best, nblk, subset->d_ids, (int)n, (int)n_sessions,

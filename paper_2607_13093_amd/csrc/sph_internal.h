@@ -7,9 +7,9 @@
 
 namespace sph {
 
-// Per-block partial results are stored [M][kMaxBlocks]; the skinny kernels
-// never launch more column blocks than this.
-constexpr int kMaxBlocks = 1024;
+// Per-block / per-tile partial results are stored [M][kMaxBlocks]; no
+// projection launch produces more column partials than this.
+constexpr int kMaxBlocks = 2048;
 // Largest LDS footprint the skinny kernels give to the staged rows of h.
 constexpr int kGemvLdsBytes = 60 * 1024;
 // Largest row count handled by one skinny launch.
@@ -44,12 +44,41 @@ struct GemvArgs {
   uint64_t* best_part;    // argmax keys [rows, kMaxBlocks]
 };
 
+// Arguments of the dense (MFMA) gathered projection: C = h[M, K] * W[S]^T.
+struct MfmaArgs {
+  const uint16_t* h;      // bf16 [M, ldh], 16-byte aligned rows
+  int64_t ldh;
+  int M;
+  int K;                  // multiple of 8 (bf16 weights) or 16 (fp8 weights)
+  const uint8_t* w;       // weight rows, vocab-major, 16-byte aligned
+  int64_t ldw_bytes;
+  const float* wscale;    // fp32 [V] for fp8 weights, else null
+  const int32_t* ids;     // subset ids [n]
+  int n;
+  int m_tiles, n_tiles;   // set by the launcher
+  // cloud epilogue
+  const float* bias;
+  float clip;
+  float* z;               // fp32 [M, n]
+  float* amax_part;       // fp32 [M, kMaxBlocks], slot = n-tile
+  // fuse epilogue
+  const int8_t* q;        // int8 [M, n]
+  const float* qscale;    // fp32 [M]
+  float* f;               // fp32 [M, n] or null
+  uint64_t* best_part;    // argmax keys [M, kMaxBlocks], slot = n-tile
+};
+
+constexpr int kMfmaBN = 128;  // subset positions per MFMA tile
+
 enum Epilogue { kEpiCloud = 0, kEpiFuse = 1 };
 
 // Launchers (return the HIP launch status).
 hipError_t launch_gemv(int epi, int wtype, int rows, const GemvArgs& a, hipStream_t s);
 int gemv_rows_per_iter(int lpr);
 int gemv_lpr(int K, int wtype);
+
+hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s);
+int mfma_n_tiles(int n);
 
 hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
                            float clip, int8_t* q, float* scale, hipStream_t s);

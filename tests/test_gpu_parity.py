@@ -26,35 +26,46 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag=""):
-    """Full staged parity A-E of one greedy workload; returns the stats."""
+def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag="", sessions=None):
+    """Full staged parity A-E of one greedy workload; returns the stats.
+
+    The GPU always runs the whole workload (the launch configuration of the
+    benchmark); with `sessions` the oracle checks only those sessions' rows
+    (rows are independent, and whole sessions keep accept lengths checkable).
+    """
     cfg = wl.cfg
     h_bits = wl.h_bits if h_bits is None else h_bits
     w_end_bits = wl.w_end_bits if w_end_bits is None else w_end_bits
     w_cloud_bits = wl.w_cloud_bits if w_cloud_bits is None else w_cloud_bits
-    orc = oracle.cloud_call(h_bits, cfg.d_end, wl.subset, cfg.clip_c, w_cloud_bits=w_cloud_bits,
+    R = cfg.rows_per_session
+    sess = np.arange(cfg.sessions) if sessions is None else np.asarray(sessions)
+    rows = (sess[:, None] * R + np.arange(R)[None, :]).ravel()
+    h_chk = h_bits[rows]
+    orc = oracle.cloud_call(h_chk, cfg.d_end, wl.subset, cfg.clip_c, w_cloud_bits=w_cloud_bits,
                             w_cloud_codes=wl.w_cloud_codes, w_cloud_scale=wl.w_cloud_scale,
                             bias=wl.bias, with_abs=True)
-    ep = oracle.endpoint_call(orc["q"], orc["scale"], h_bits, cfg.d_end, wl.subset, w_end_bits,
-                              cfg.sessions, cfg.rows_per_session,
-                              drafts=np.zeros((cfg.sessions, cfg.k), np.int32))
-    drafts = make_drafts(cfg, ep["tokens"], wl.subset) if cfg.k else None
+    ep = oracle.endpoint_call(orc["q"], orc["scale"], h_chk, cfg.d_end, wl.subset, w_end_bits,
+                              len(sess), R, drafts=np.zeros((len(sess), cfg.k), np.int32))
+    ref_tok = np.zeros(cfg.M, np.int32)
+    ref_tok[rows] = ep["tokens"]
+    drafts_all = make_drafts(cfg, ref_tok, wl.subset) if cfg.k else None
+    drafts = drafts_all[sess] if cfg.k else None
 
     say(f"[gpu] {tag or cfg.name}: cloud_partial M={cfg.M} d={cfg.d} d_end={cfg.d_end} "
         f"n={len(wl.subset)} wtype={cfg.wtype}")
     dw = P.DeviceWorkload(wl, h_bits=h_bits, w_end_bits=w_end_bits, w_cloud_bits=w_cloud_bits)
     q, s, z = dw.cloud()
     torch.cuda.synchronize()
-    qh, sh, zh = P.host(q), P.host(s), P.host(z)
+    qh, sh, zh = P.host(q)[rows], P.host(s)[rows], P.host(z)[rows]
     stats = {"A": P.stage_a(zh, orc)}
     P.stage_b(zh, qh, sh, cfg.clip_c)
     stats["C"] = P.stage_c(qh, sh, orc)
 
-    say(f"[gpu] {tag or cfg.name}: fuse_verify sessions={cfg.sessions} R={cfg.rows_per_session}")
-    tok, acc, f = dw.fuse(q, s, drafts)
+    say(f"[gpu] {tag or cfg.name}: fuse_verify sessions={cfg.sessions} R={R}")
+    tok, acc, f = dw.fuse(q, s, drafts_all)
     torch.cuda.synchronize()
-    th, ah, fh = P.host(tok), P.host(acc), P.host(f)
-    wl2 = _with(wl, h_bits=h_bits, w_end_bits=w_end_bits)
+    th, ah, fh = P.host(tok)[rows], P.host(acc)[sess], P.host(f)[rows]
+    wl2 = _with(wl, h_bits=h_chk, w_end_bits=w_end_bits, cfg=cfg.replace(sessions=len(sess)))
     stats["D"] = P.stage_d_greedy(qh, sh, fh, th, ah, wl2, drafts)
     stats["E"] = P.stage_e_greedy(qh, sh, th, ah, orc, wl2, drafts)
     say(f"[gpu] {tag or cfg.name}: ok {stats}")
@@ -81,6 +92,16 @@ def test_decode_full_pipeline():
     run_greedy_case(make_workload(CONFIGS["decode"]))
 
 
+def test_batched_full_pipeline():
+    run_greedy_case(make_workload(CONFIGS["batched"]))
+
+
+@pytest.mark.parametrize("name", ["dense_full", "dense_sub"])
+def test_dense_sampled_sessions(name):
+    # the full 2048-row launch; the oracle checks 4 whole sessions (32 rows)
+    run_greedy_case(make_workload(CONFIGS[name]), sessions=[0, 77, 160, 255])
+
+
 # ---------------------------------------------------------------------------
 # shapes: ragged tails, row groups, d_end = 0, bias, k = 0
 # ---------------------------------------------------------------------------
@@ -95,6 +116,10 @@ RAGGED = [
     (13, 1, 136, 64, 1000, 333),    # 13 rows: two row groups
     (4, 5, 4104, 520, 6000, 4097),  # d_end > 512 and a ragged subset
     (3, 1, 8192, 512, 3000, 2999),  # four passes over each cloud row
+    # dense (MFMA) path: more than 8 rows
+    (3, 3, 520, 40, 3000, 1001),    # 9 rows, ragged m- and n-tiles
+    (8, 5, 1032, 0, 4000, 2500),    # 40 rows, d_end = 0
+    (13, 10, 2056, 8, 9000, 8193),  # 130 rows: two m-tiles, last n-tile of one column
 ]
 
 
@@ -158,6 +183,12 @@ def test_fp8_cloud_partial_skinny():
     cfg = Config("fp8_small", 23, d=1056, d_end=32, vocab=5000, n_sub=2048, subset_kind="choice",
                  sessions=1, rows_per_session=5, wtype="fp8")
     run_greedy_case(make_workload(cfg), tag="fp8 skinny")
+
+
+def test_fp8_cloud_partial_dense():
+    cfg = Config("fp8_dense", 27, d=1056, d_end=32, vocab=5000, n_sub=3001, subset_kind="choice",
+                 sessions=12, rows_per_session=5, wtype="fp8", with_bias=True)
+    run_greedy_case(make_workload(cfg), tag="fp8 dense")
 
 
 # ---------------------------------------------------------------------------
