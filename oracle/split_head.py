@@ -306,7 +306,7 @@ def philox_uniform(seed: int, row_in_session: int, session: int) -> float:
     return (x0 >> 8) * 2.0 ** -24
 
 
-def sample_select(f, subset, temperature, top_p, seed, rows_per_session):
+def sample_select(f, subset, temperature, top_p, seed, rows_per_session, row_index=None):
     """Temperature + top-p sample per row (eq. 15 with a nucleus cut).
 
     p = softmax(f / tau) over S in fp64.  Order S by (p desc, id asc); the
@@ -315,6 +315,9 @@ def sample_select(f, subset, temperature, top_p, seed, rows_per_session):
     and target = u * mass(N), walk N in ascending id order and take the
     first member whose running mass exceeds the target (the last member if
     rounding leaves none).
+
+    Row m of ``f`` is verification row row_index[m] of the batch (default m):
+    its counter is (row_index[m] % R, row_index[m] // R).
 
     Returns (tokens int32 [M], info) where info holds, per row, the nucleus
     size, the distance of top_p from the two cumulative masses around the cut
@@ -350,7 +353,8 @@ def sample_select(f, subset, temperature, top_p, seed, rows_per_session):
         members = np.sort(order[:K])              # positions in S, ascending id
         run = np.cumsum(p[members])
         mass = run[-1]
-        u = philox_uniform(seed, m % rows_per_session, m // rows_per_session)
+        g = m if row_index is None else int(row_index[m])
+        u = philox_uniform(seed, g % rows_per_session, g // rows_per_session)
         target = u * mass
         hit = np.flatnonzero(run > target)
         i = int(hit[0]) if hit.size else K - 1

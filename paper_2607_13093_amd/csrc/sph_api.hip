@@ -303,7 +303,6 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
                     int32_t* accept_len_out, float* fused_out, void* workspace, size_t ws_bytes,
                     void* stream) {
   const char* fn = "sph_fuse_verify";
-  (void)seed;
   if (n_sessions < 0 || rows_per_session < 1 || rows_per_session > 1024)
     return fail(SPH_E_INVALID_ARG, "%s: n_sessions=%lld / rows_per_session=%lld out of range", fn,
                 (long long)n_sessions, (long long)rows_per_session);
@@ -335,7 +334,6 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   if (!workspace || ws_bytes < need)
     return fail(SPH_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                 workspace ? ws_bytes : (size_t)0);
-  if (mode == SPH_SAMPLE) return fail(SPH_E_UNSUPPORTED, "%s: sampling is not built yet", fn);
   if (d_end > 0 && ((reinterpret_cast<uintptr_t>(w_end) & 15) != 0 || ldw % 8 != 0 || d_end % 8 != 0))
     return fail(SPH_E_UNSUPPORTED, "%s: endpoint weight rows must be 16-byte aligned and d_end a multiple of 8",
                 fn);
@@ -346,6 +344,10 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint64_t* best = reinterpret_cast<uint64_t*>(ws);
+  // Sampling needs the whole fused row: into fused_out, else the workspace.
+  float* fused = fused_out;
+  if (mode == SPH_SAMPLE && !fused)
+    fused = reinterpret_cast<float*>(ws + align256((size_t)M * sph::kMaxBlocks * 8));
   const bool h_vec = d_end == 0 || ((reinterpret_cast<uintptr_t>(h_end) & 15) == 0 && ldh % 8 == 0);
   int nblk;
   if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks) {
@@ -360,7 +362,7 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
     a.n = (int)n;
     a.q = q;
     a.qscale = scale;
-    a.f = fused_out;
+    a.f = fused;
     a.best_part = best;
     hipError_t e = traced("fuse_mfma", s, [&] { return sph::launch_mfma(sph::kEpiFuse, 0, a, s); });
     if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
@@ -386,11 +388,24 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
       a.nblk = nblk;
       a.q = q + m0 * n;
       a.qscale = scale + m0;
-      a.f = fused_out ? fused_out + m0 * n : nullptr;
+      a.f = fused ? fused + m0 * n : nullptr;
       a.best_part = best + m0 * sph::kMaxBlocks;
       hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, a, s); });
       if (e != hipSuccess) return hip_fail(e, "endpoint projection launch");
     }
+  }
+  if (mode == SPH_SAMPLE) {
+    hipError_t e = traced("fuse_sample", s, [&] {
+      return sph::launch_sample(fused, (int)M, (int)n, subset->d_ids, (int)rows_per_session,
+                                temperature, top_p, seed, tokens_out, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "sampling launch");
+    e = traced("fuse_accept", s, [&] {
+      return sph::launch_accept(tokens_out, drafts, (int)n_sessions, (int)rows_per_session,
+                                accept_len_out, s);
+    });
+    if (e != hipSuccess) return hip_fail(e, "verification launch");
+    return ok();
   }
   hipError_t e = traced("fuse_final_greedy", s, [&] {
     return sph::launch_final_greedy(best, nblk, subset->d_ids, (int)n, (int)n_sessions,

@@ -83,6 +83,12 @@ int mfma_n_tiles(int n);
 hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
                            float clip, int8_t* q, float* scale, hipStream_t s);
 
+hipError_t launch_sample(const float* f, int M, int n, const int32_t* ids, int R,
+                         float temperature, float top_p, uint64_t seed, int32_t* tokens,
+                         hipStream_t s);
+hipError_t launch_accept(const int32_t* tokens, const int32_t* drafts, int n_sessions, int R,
+                         int32_t* accept, hipStream_t s);
+
 hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_t* ids, int n,
                                int n_sessions, int R, const int32_t* drafts,
                                int32_t* tokens, int32_t* accept, hipStream_t s);
