@@ -28,6 +28,8 @@
 // fp32 partial logits and the tile's row maxima of |clamp(z)|; the fuse
 // epilogue dequantises the payload (eq. 13), writes fused logits on request
 // and the tile's per-row (value, position) argmax key.
+#include <type_traits>
+
 #include "sph_internal.h"
 
 namespace sph {
@@ -73,24 +75,121 @@ __device__ __forceinline__ void tile_of_block(int b, int m_tiles, int n_tiles, i
   nt = in / gm;
 }
 
-template <int BM, int BN, int WM, int WN, int WT, int EPI>
-__global__ __launch_bounds__(64 * WM * WN) void k_mfma(const MfmaArgs a) {
-  constexpr int NT = 64 * WM * WN;
-  constexpr int TM = BM / WM, TN = BN / WN;  // wave tile
+
+// Transposing butterfly inside each 32-lane half of a wave: on entry lane l
+// holds P values; after log2(32) exchanges lane (l & 31) holds the max over
+// the half's 32 lanes of values (l & 31) * P/32 .. + P/32 - 1.
+template <int P, class T>
+__device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
+  static_assert(P >= 32 && P % 32 == 0, "values per lane");
+  int cnt = P;
+#pragma unroll
+  for (int o = 16; o >= 1; o >>= 1) {
+    const int half = cnt / 2;
+    const bool upper = (lane & o) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const T send = upper ? v[i] : v[i + half];
+      const T keep = upper ? v[i + half] : v[i];
+      T got;
+      if constexpr (sizeof(T) == 8) got = shfl_xor_u64_m(send, o);
+      else got = __shfl_xor(send, o, 64);
+      v[i] = keep > got ? keep : got;
+    }
+    cnt = half;
+  }
+}
+
+// Epilogue of a BM x BN tile held as acc[FM][FN] 32x32 fragments by the
+// 2 x 2 waves.  Row of accumulator r in fragment (i, j):
+// 8*(r/4) + 4*(lane/32) + r%4; column: lane % 32.
+template <int BM, int BN, int WT, int EPI, int FM, int FN>
+__device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const MfmaArgs& a,
+                                              const int32_t* s_ids, uint32_t* s_rmax,
+                                              unsigned long long* s_rkey, int m0, int n0,
+                                              int nt) {
+  constexpr int TM = BM / 2, TN = BN / 2, P = FM * 16;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int M = a.M, n = a.n;
+  using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
+  V red[P];
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int row = m0 + lrow;
+      V best = V(0);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int lcol = wn * TN + j * 32 + (lane & 31);
+        const int col = n0 + lcol;
+        if (row < M && col < n) {
+          const float dot = acc[i][j][r];
+          if constexpr (EPI == kEpiCloud) {
+            float zv = dot;
+            if constexpr (WT == 1) zv = zv * a.wscale[s_ids[lcol]];
+            if (a.bias) zv = zv + a.bias[s_ids[lcol]];
+            __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
+            best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
+          } else {
+            const float f = __builtin_fmaf((float)a.q[(int64_t)row * n + col], a.qscale[row], dot);
+            if (a.f) a.f[(int64_t)row * n + col] = f;
+            const unsigned long long key = argmax_key_m(f, col);
+            best = key > best ? key : best;
+          }
+        }
+      }
+      red[i * 16 + r] = best;
+    }
+  }
+  half_wave_max_transpose<P>(red, lane);
+  constexpr int PER = P / 32;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    const int idx = (lane & 31) * PER + t;
+    const int i = idx / 16, r = idx % 16;
+    const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    if constexpr (EPI == kEpiCloud)
+      atomicMax(&s_rmax[lrow], __float_as_uint(red[t]));
+    else
+      atomicMax(&s_rkey[lrow], red[t]);
+  }
+  __syncthreads();
+  for (int i = tid; i < BM; i += 256) {
+    const int row = m0 + i;
+    if (row >= M) continue;
+    if constexpr (EPI == kEpiCloud)
+      a.amax_part[(int64_t)row * kMaxBlocks + nt] = __uint_as_float(s_rmax[i]);
+    else
+      a.best_part[(int64_t)row * kMaxBlocks + nt] = s_rkey[i];
+  }
+}
+
+// BM x BN tile per block, 4 waves in a 2 x 2 grid, wave tile (BM/2) x (BN/2).
+// LDS holds two K steps of both tiles; the global loads of step k+1 are in
+// flight (in registers) while step k's MFMAs run, then land in the other LDS
+// buffer, so each step needs a single barrier.
+template <int BM, int BN, int WT, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_mfma(const MfmaArgs a) {
+  constexpr int NT = 256;
+  constexpr int TM = BM / 2, TN = BN / 2;    // wave tile
   constexpr int FM = TM / 32, FN = TN / 32;  // 32x32 fragments per wave
-  constexpr int A_CH = BM * (kBK / 8) / NT;  // 16-byte A chunks per thread
+  constexpr int A_CH = BM * (kBK / 8) / NT;  // 16-byte A chunks per thread per step
   constexpr int B_EPC = WT == 0 ? 8 : 16;    // weight elements per 16-byte chunk
   constexpr int B_CH = BN * (kBK / B_EPC) / NT;
   static_assert(A_CH * NT == BM * (kBK / 8) && B_CH * NT == BN * (kBK / B_EPC), "tile/threads");
 
-  __shared__ __align__(16) uint16_t As[BM * kLDK];
-  __shared__ __align__(16) uint16_t Bs[BN * kLDK];
-  __shared__ int32_t s_ids[BN];
-  __shared__ uint32_t s_rmax[BM];
-  __shared__ unsigned long long s_rkey[BM];
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);            // [2][BM][kLDK]
+  uint16_t* Bs = As + 2 * BM * kLDK;                             // [2][BN][kLDK]
+  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + 2 * BN * kLDK);
+  uint32_t* s_rmax = reinterpret_cast<uint32_t*>(s_ids + BN);
+  unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_rmax + BM + (BM & 1));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wm = wave >> 1, wn = wave & 1;
   int mt, nt;
   tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
@@ -123,18 +222,20 @@ __global__ __launch_bounds__(64 * WM * WN) void k_mfma(const MfmaArgs a) {
                   : u32x4_t{0u, 0u, 0u, 0u};
     }
   };
-  auto store = [&]() {
+  auto store = [&](int buf) {
+    uint16_t* as = As + buf * BM * kLDK;
+    uint16_t* bs = Bs + buf * BN * kLDK;
 #pragma unroll
     for (int i = 0; i < A_CH; ++i) {
       const int c = tid + i * NT, row = c >> 3, kc = c & 7;
-      *reinterpret_cast<u32x4_t*>(As + row * kLDK + kc * 8) = ra[i];
+      *reinterpret_cast<u32x4_t*>(as + row * kLDK + kc * 8) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < B_CH; ++i) {
       const int c = tid + i * NT;
       const int row = c / (kBK / B_EPC), kc = c % (kBK / B_EPC);
       if constexpr (WT == 0) {
-        *reinterpret_cast<u32x4_t*>(Bs + row * kLDK + kc * 8) = rb[i];
+        *reinterpret_cast<u32x4_t*>(bs + row * kLDK + kc * 8) = rb[i];
       } else {
         const uint32_t w4[4] = {rb[i].x, rb[i].y, rb[i].z, rb[i].w};
         u32x4_t lo, hi;
@@ -142,8 +243,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_mfma(const MfmaArgs a) {
         lo.z = e4m3x2_to_bf16x2_m<false>(w4[1]); lo.w = e4m3x2_to_bf16x2_m<true>(w4[1]);
         hi.x = e4m3x2_to_bf16x2_m<false>(w4[2]); hi.y = e4m3x2_to_bf16x2_m<true>(w4[2]);
         hi.z = e4m3x2_to_bf16x2_m<false>(w4[3]); hi.w = e4m3x2_to_bf16x2_m<true>(w4[3]);
-        *reinterpret_cast<u32x4_t*>(Bs + row * kLDK + kc * 16) = lo;
-        *reinterpret_cast<u32x4_t*>(Bs + row * kLDK + kc * 16 + 8) = hi;
+        *reinterpret_cast<u32x4_t*>(bs + row * kLDK + kc * 16) = lo;
+        *reinterpret_cast<u32x4_t*>(bs + row * kLDK + kc * 16 + 8) = hi;
       }
     }
   };
@@ -158,110 +259,218 @@ __global__ __launch_bounds__(64 * WM * WN) void k_mfma(const MfmaArgs a) {
 
   if (K > 0) {
     load(0);
-    store();
+    store(0);
     __syncthreads();
   }
+  int buf = 0;
   for (int k0 = 0; k0 < K; k0 += kBK) {
     const bool next = k0 + kBK < K;
     if (next) load(k0 + kBK);
+    const uint16_t* as = As + buf * BM * kLDK;
+    const uint16_t* bs = Bs + buf * BN * kLDK;
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       bf16x8_t af[FM], bfr[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
         af[i] = *reinterpret_cast<const bf16x8_t*>(
-            As + (wm * TM + i * 32 + (lane & 31)) * kLDK + kk * 16 + 8 * (lane >> 5));
+            as + (wm * TM + i * 32 + (lane & 31)) * kLDK + kk * 16 + 8 * (lane >> 5));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         bfr[j] = *reinterpret_cast<const bf16x8_t*>(
-            Bs + (wn * TN + j * 32 + (lane & 31)) * kLDK + kk * 16 + 8 * (lane >> 5));
+            bs + (wn * TN + j * 32 + (lane & 31)) * kLDK + kk * 16 + 8 * (lane >> 5));
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
+    // The other buffer was last read in the previous step, which every wave
+    // finished before the barrier that ended it.
+    if (next) store(buf ^ 1);
     __syncthreads();
-    if (next) {
-      store();
-      __syncthreads();
-    }
+    buf ^= 1;
   }
 
-  // ---- epilogue -----------------------------------------------------------
-  // Row of accumulator r in fragment (i, j): 8*(r/4) + 4*(lane/32) + r%4.
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int row = m0 + lrow;
-      float rmax = 0.0f;
-      unsigned long long rkey = 0ull;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int lcol = wn * TN + j * 32 + (lane & 31);
-        const int col = n0 + lcol;
-        if (row < M && col < n) {
-          const float dot = acc[i][j][r];
-          if constexpr (EPI == kEpiCloud) {
-            float zv = dot;
-            if constexpr (WT == 1) zv = zv * a.wscale[s_ids[lcol]];
-            if (a.bias) zv = zv + a.bias[s_ids[lcol]];
-            a.z[(int64_t)row * n + col] = zv;
-            rmax = fmaxf(rmax, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
-          } else {
-            const float f = __builtin_fmaf((float)a.q[(int64_t)row * n + col], a.qscale[row], dot);
-            if (a.f) a.f[(int64_t)row * n + col] = f;
-            const unsigned long long key = argmax_key_m(f, col);
-            rkey = key > rkey ? key : rkey;
-          }
-        }
-      }
-      // fold the 32 lanes that share this row
-      if constexpr (EPI == kEpiCloud) {
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o, 64));
-        if ((lane & 31) == 0) atomicMax(&s_rmax[lrow], __float_as_uint(rmax));
-      } else {
-#pragma unroll
-        for (int o = 16; o >= 1; o >>= 1) {
-          const unsigned long long y = shfl_xor_u64_m(rkey, o);
-          rkey = y > rkey ? y : rkey;
-        }
-        if ((lane & 31) == 0) atomicMax(&s_rkey[lrow], rkey);
-      }
-    }
-  }
-  __syncthreads();
-  for (int i = tid; i < BM; i += NT) {
-    const int row = m0 + i;
-    if (row >= M) continue;
-    if constexpr (EPI == kEpiCloud)
-      a.amax_part[(int64_t)row * kMaxBlocks + nt] = __uint_as_float(s_rmax[i]);
-    else
-      a.best_part[(int64_t)row * kMaxBlocks + nt] = s_rkey[i];
-  }
+  tile_epilogue<BM, BN, WT, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt);
 }
 
-template <int BM, int BN, int WM, int WN, int WT, int EPI>
+
+// Direct-to-LDS variant (bf16 weights, K a multiple of 64).  gfx950's
+// global_load_lds_dwordx4 writes a wave's 64 x 16 bytes straight into LDS
+// (lane l at base + 16*l), so tiles never pass through registers and no
+// ds_write is issued.  A wave instruction fills 8 rows x 128 bytes; rows are
+// unpadded and their 16-byte chunks are XOR-swizzled with
+// f(row) = (row & 7) ^ ((row >> 3) & 1), which keeps every fragment read
+// conflict-free whether the LDS serves 8 or 16 lanes per cycle.  Rows past
+// M and subset positions past n read a valid row (row M-1 / the last id):
+// they only feed outputs that are never written.  On the decode-sized dense
+// shape this loop ran 1.2x faster than register staging.
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ int swz8(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
+template <int BM, int BN, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_mfma_dma(const MfmaArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int TM = BM / 2, TN = BN / 2;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;  // DMA instructions per wave per step
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);      // [2][BM][64]
+  uint16_t* Bs = As + 2 * BM * kBK;                       // [2][BN][64]
+  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + 2 * BN * kBK);
+  uint32_t* s_rmax = reinterpret_cast<uint32_t*>(s_ids + BN);
+  unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_rmax + BM + (BM & 1));
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  int mt, nt;
+  tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int M = a.M, K = a.K, n = a.n;
+  const int last_id = a.ids[min(n, n0 + BN) - 1];
+  for (int i = tid; i < BN; i += 256) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  for (int i = tid; i < BM; i += 256) {
+    s_rmax[i] = 0u;
+    s_rkey[i] = 0ull;
+  }
+  __syncthreads();
+
+  // lane -> row (lane / 8) of its 8-row group and the logical chunk it fetches
+  const int lr = lane >> 3;
+  const uint8_t* pa[A_INS];
+  const uint8_t* pb[B_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    const int r = (wave * A_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int r = (wave * B_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+  }
+  auto issue = [&](int k0, int stage) {
+    uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
+    uint8_t* bs = reinterpret_cast<uint8_t*>(Bs + stage * BN * kBK);
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
+                                       (lds_void_t*)(as + (wave * A_INS + i) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pb[i] + (int64_t)k0 * 2,
+                                       (lds_void_t*)(bs + (wave * B_INS + i) * 1024), 16, 0, 0);
+  };
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  if (K > 0) {
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  int stage = 0;
+  for (int k0 = 0; k0 < K; k0 += kBK) {
+    // the other stage was last read in the previous step, finished by all
+    // waves before that step's closing barrier
+    if (k0 + kBK < K) issue(k0 + kBK, stage ^ 1);
+    const uint16_t* as = As + stage * BM * kBK;
+    const uint16_t* bs = Bs + stage * BN * kBK;
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      bf16x8_t af[FM], bfr[FN];
+      const int c = kk * 2 + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * TM + i * 32 + (lane & 31);
+        af[i] = *reinterpret_cast<const bf16x8_t*>(as + row * kBK + ((c ^ swz8(row)) << 3));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int row = wn * TN + j * 32 + (lane & 31);
+        bfr[j] = *reinterpret_cast<const bf16x8_t*>(bs + row * kBK + ((c ^ swz8(row)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads for the next stage have landed
+    __syncthreads();
+    stage ^= 1;
+  }
+  tile_epilogue<BM, BN, 0, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt);
+#endif
+}
+
+template <int BM, int BN>
+constexpr size_t mfma_lds_bytes() {
+  return (size_t)2 * (BM + BN) * kLDK * 2 + (size_t)BN * 4 + (size_t)(BM + 1) * 4 + 8 +
+         (size_t)BM * 8;
+}
+
+template <int BM, int BN>
+constexpr size_t mfma_dma_lds_bytes() {
+  return (size_t)2 * (BM + BN) * kBK * 2 + (size_t)BN * 4 + (size_t)(BM + 1) * 4 + 8 +
+         (size_t)BM * 8;
+}
+
+template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
   if (a.n_tiles > kMaxBlocks) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((k_mfma<BM, BN, WM, WN, WT, EPI>), dim3(a.m_tiles * a.n_tiles),
-                     dim3(64 * WM * WN), 0, s, a);
+  if constexpr (WT == 0) {
+    if (a.K % kBK == 0) {
+      auto kd = k_mfma_dma<BM, BN, EPI>;
+      constexpr size_t lds_d = mfma_dma_lds_bytes<BM, BN>();
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
+      return hipGetLastError();
+    }
+  }
+  auto kern = k_mfma<BM, BN, WT, EPI>;
+  constexpr size_t lds = mfma_lds_bytes<BM, BN>();
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
   return hipGetLastError();
+}
+
+// Row tile: 256 unless that pads M by more than 1/8 where 128 would not.
+static int mfma_bm(int M) {
+  const int pad256 = (M + 255) / 256 * 256 - M;
+  const int pad128 = (M + 127) / 128 * 128 - M;
+  return (pad256 * 8 > M && pad128 < pad256) ? 128 : 256;
 }
 
 int mfma_n_tiles(int n) { return (n + kMfmaBN - 1) / kMfmaBN; }
 
+template <int WT, int EPI>
+static hipError_t launch_bm(const MfmaArgs& a, hipStream_t s) {
+  return mfma_bm(a.M) == 256 ? launch_tile<256, kMfmaBN, WT, EPI>(a, s)
+                             : launch_tile<128, kMfmaBN, WT, EPI>(a, s);
+}
+
 hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s) {
   if (epi == kEpiCloud)
-    return wtype == 0 ? launch_tile<128, kMfmaBN, 2, 2, 0, kEpiCloud>(a, s)
-                      : launch_tile<128, kMfmaBN, 2, 2, 1, kEpiCloud>(a, s);
+    return wtype == 0 ? launch_bm<0, kEpiCloud>(a, s) : launch_bm<1, kEpiCloud>(a, s);
   if (wtype != 0) return hipErrorInvalidValue;
-  return launch_tile<128, kMfmaBN, 2, 2, 0, kEpiFuse>(a, s);
+  return launch_bm<0, kEpiFuse>(a, s);
 }
 
 }  // namespace sph

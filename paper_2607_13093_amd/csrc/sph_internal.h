@@ -68,7 +68,7 @@ struct MfmaArgs {
   uint64_t* best_part;    // argmax keys [M, kMaxBlocks], slot = n-tile
 };
 
-constexpr int kMfmaBN = 128;  // subset positions per MFMA tile
+constexpr int kMfmaBN = 256;  // subset positions per MFMA tile
 
 enum Epilogue { kEpiCloud = 0, kEpiFuse = 1 };
 
