@@ -103,15 +103,40 @@ __device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
 // Epilogue of a BM x BN tile held as acc[FM][FN] 32x32 fragments by the
 // 2 x 2 waves.  Row of accumulator r in fragment (i, j):
 // 8*(r/4) + 4*(lane/32) + r%4; column: lane % 32.
+// For the fuse epilogue the payload tile q[m0:m0+BM, n0:n0+BN] and the row
+// scales are first staged in LDS the main loop no longer needs (s_q: BM*BN
+// bytes, s_qs: BM floats) with coalesced loads, instead of one byte load per
+// accumulator.  The caller has passed a barrier after its last LDS read.
 template <int BM, int BN, int WT, int EPI, int FM, int FN>
 __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const MfmaArgs& a,
                                               const int32_t* s_ids, uint32_t* s_rmax,
                                               unsigned long long* s_rkey, int m0, int n0,
-                                              int nt) {
+                                              int nt, int8_t* s_q, float* s_qs) {
   constexpr int TM = BM / 2, TN = BN / 2, P = FM * 16;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int M = a.M, n = a.n;
+  if constexpr (EPI == kEpiFuse) {
+    const bool vec = (n & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
+    if (vec) {
+      constexpr int CPR = BN / 16;  // 16-byte chunks per tile row
+      for (int c = tid; c < BM * CPR; c += 256) {
+        const int r = c / CPR, k = c % CPR;
+        const int row = m0 + r, col = n0 + k * 16;
+        u32x4_t v = {0u, 0u, 0u, 0u};
+        if (row < M && col < n) v = *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)row * n + col);
+        *reinterpret_cast<u32x4_t*>(s_q + r * BN + k * 16) = v;
+      }
+    } else {
+      for (int c = tid; c < BM * BN; c += 256) {
+        const int r = c / BN, k = c % BN;
+        const int row = m0 + r, col = n0 + k;
+        s_q[c] = (row < M && col < n) ? a.q[(int64_t)row * n + col] : (int8_t)0;
+      }
+    }
+    for (int r = tid; r < BM; r += 256) s_qs[r] = m0 + r < M ? a.qscale[m0 + r] : 0.0f;
+    __syncthreads();
+  }
   using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
   V red[P];
 #pragma unroll
@@ -134,8 +159,8 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
             __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
             best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
           } else {
-            const float f = __builtin_fmaf((float)a.q[(int64_t)row * n + col], a.qscale[row], dot);
-            if (a.f) a.f[(int64_t)row * n + col] = f;
+            const float f = __builtin_fmaf((float)s_q[lrow * BN + lcol], s_qs[lrow], dot);
+            if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
             const unsigned long long key = argmax_key_m(f, col);
             best = key > best ? key : best;
           }
@@ -292,7 +317,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     buf ^= 1;
   }
 
-  tile_epilogue<BM, BN, WT, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt);
+  tile_epilogue<BM, BN, WT, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+                                 reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
 }
 
 
@@ -410,7 +436,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __syncthreads();
     stage ^= 1;
   }
-  tile_epilogue<BM, BN, 0, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt);
+  tile_epilogue<BM, BN, 0, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+                                reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
 #endif
 }
 
