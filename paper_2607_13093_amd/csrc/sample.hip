@@ -1,41 +1,145 @@
 // Temperature + top-p sampling of each verification row, then the accepted
 // draft prefix of each session (eq. 15 with a nucleus cut; Section 5.5).
 //
-// One 1024-thread block per row of fused logits f (fp32, written by the
-// endpoint projection).  Thread t holds the contiguous positions
-// [t*CH, (t+1)*CH) of the row, i.e. a run of ascending vocabulary ids, so
-// every id-order quantity is a per-thread sequential pass plus a block scan.
+// One 512-thread block per row of fused logits f (fp32, written by the
+// endpoint projection, whose per-tile argmax keys also give the row maximum).
+// The row is walked in chunks of 256 positions, one per wave iteration (lane
+// l holds positions 4l .. 4l+3 of the chunk, loaded as one 16-byte vector),
+// so every pass is a short rolled loop of coalesced loads.
 //
-//   1. fmax = max f; softmax weights e_j = exp((f_j - fmax) / tau) in fp64,
-//      Z = sum e (per-thread sequential sums, fixed-order tree).
-//   2. Nucleus = shortest prefix of (p desc, id asc) reaching top_p.  Order
-//      by p equals order by f, so the cut is found by a radix select on the
-//      orderable 32-bit key of f with fp64 mass histograms, 12 + 10 + 10 bits
-//      (a first pass on the top 8 bits would put a row of N(0,1)-like logits
-//      into a handful of sign/exponent buckets and serialise the LDS
-//      atomics).  The crossing bucket is found by a block suffix scan.  The
-//      select yields the threshold key T, the mass of keys above T, and how
-//      many of the elements tied at T (in id order) complete the nucleus.
+// Weights.  e = exp((f - fmax) / tau) in fp64 by the table-driven method of
+// Tang (ACM TOMS 15(2), 1989): with t = (f - fmax) / (tau ln2) * 64,
+// N = rint(t), r = t - N (|r| <= 1/2), e = 2^(N>>6) * 2^((N&63)/64) * 2^(r/64),
+// the middle factor from a 64-entry table and 2^(r/64) a degree-5 Taylor
+// polynomial (truncation below 4e-17).  Every use of a weight evaluates the
+// same operations with contraction off, so a weight is bit-identical wherever
+// it is recomputed.
+//
+// Exact masses.  Each weight e in [0, 1] becomes E = floor(e * 2^63), held as
+// E = a * 2^32 + b (a <= 2^31, b < 2^32); sums of a and of b over at most 2^22
+// elements fit 64 bits, so every mass is an exact integer, every decision
+// (nucleus cut, inverse CDF) is exact for these weights and independent of
+// the order of summation, and the kernel is deterministic.  E misses
+// e * 2^63 by less than one unit (relative 2^-63 of the largest weight).
+//
+//   1. A mass histogram over 2048 value buckets of y = (fmax - f)/tau in
+//      [0, 40) (the last also takes y >= 40, whose elements each weigh below
+//      5e-18).  Bucket order is value order, so the nucleus -- the shortest
+//      prefix of (p desc, id asc) whose mass reaches top_p * Z -- ends in the
+//      first bucket b* whose running mass reaches the target.
+//   2. One pass adds the members of buckets before b* into per-segment masses
+//      (segments: runs of consecutive positions, at most 1024 per row) and
+//      collects the elements of b*.  Up to 1024 of them are sorted by
+//      (key desc, position asc) in LDS; a scan over that order finds the
+//      element completing the nucleus.  More (near-constant rows) go through
+//      an exact radix select over the 32-bit orderable key (11 + 11 + 10
+//      bits); the cut among elements tied at the threshold key is the c-th in
+//      id order.  Nucleus = {key > T} + {key == T, position <= cut}.
 //   3. u = top 24 bits of word 0 of Philox4x32-10 (key = seed halves,
-//      counter = (row in session, session, 0, 0)) times 2^-24; the token is
-//      the first nucleus member in ascending id order whose running mass
-//      exceeds u * mass(nucleus) (the last member if rounding leaves none).
-//
-// The weights are recomputed in fp64 in every pass instead of stored: a row
-// of 65536 fp64 weights does not fit the registers of a 1024-thread block,
-// and fp32 weights would move the nucleus cut by ~1e-8 of the row's mass.
-// Histogram bins are accumulated with LDS fp64 atomics; their order can
-// change the last bit of a bin, which matters only for rows whose cut lies
-// within ~1e-16 of a bin boundary.
+//      counter = (row in session, session, 0, 0)).  The token is the first
+//      nucleus member in id order whose running mass M has
+//      M * 2^24 > u24 * mass(nucleus): a scan over segment masses picks the
+//      segment, one wave scans inside it.
 #include "sph_internal.h"
 
 namespace sph {
 
-constexpr int kSampleThreads = 1024;
-constexpr int kSampleWaves = kSampleThreads / 64;
+constexpr int kSThreads = 512;
+constexpr int kSWaves = kSThreads / 64;
+constexpr int kBuckets = 2048;     // value buckets; also the widest key pass (11 bits)
+constexpr int kBPT = kBuckets / kSThreads;
+constexpr int kMaxSeg = 1024;      // segments per row
+constexpr int kSPT = kMaxSeg / kSThreads;
+constexpr int kMaxCand = 1024;     // elements of the cut bucket sorted directly
+constexpr int kChunk = 256;        // positions per wave iteration
+constexpr float kYSpan = 40.0f;    // buckets cover (fmax - f)/tau in [0, 40)
+static_assert(kMaxCand <= 2 * kSThreads, "one candidate pair per thread");
+
+// 2^(r/64) = exp(r * ln2/64): Taylor coefficients (ln2/64)^k / k!
+constexpr double kLn2 = 0.6931471805599453;
+constexpr double kL64 = kLn2 / 64.0;
+constexpr double kC1 = kL64;
+constexpr double kC2 = kL64 * kL64 / 2.0;
+constexpr double kC3 = kL64 * kL64 * kL64 / 6.0;
+constexpr double kC4 = kL64 * kL64 * kL64 * kL64 / 24.0;
+constexpr double kC5 = kL64 * kL64 * kL64 * kL64 * kL64 / 120.0;
+
+// ---------------------------------------------------------------------------
+// 128-bit unsigned integers (masses in units of 2^-63)
+
+struct U128 {
+  uint64_t lo, hi;
+};
+
+__device__ __forceinline__ U128 u128_add(U128 a, U128 b) {
+  U128 r;
+  r.lo = a.lo + b.lo;
+  r.hi = a.hi + b.hi + (r.lo < a.lo ? 1ull : 0ull);
+  return r;
+}
+
+__device__ __forceinline__ U128 u128_sub(U128 a, U128 b) {
+  U128 r;
+  r.lo = a.lo - b.lo;
+  r.hi = a.hi - b.hi - (a.lo < b.lo ? 1ull : 0ull);
+  return r;
+}
+
+__device__ __forceinline__ bool u128_lt(U128 a, U128 b) {
+  return a.hi < b.hi || (a.hi == b.hi && a.lo < b.lo);
+}
+
+__device__ __forceinline__ U128 u128_shl24(U128 a) {
+  return U128{a.lo << 24, (a.hi << 24) | (a.lo >> 40)};
+}
+
+__device__ __forceinline__ U128 u128_mul32(U128 a, uint32_t m) {
+  return U128{a.lo * m, a.hi * m + __umul64hi(a.lo, (uint64_t)m)};
+}
+
+// A * 2^32 + B
+__device__ __forceinline__ U128 u128_join(uint64_t A, uint64_t B) {
+  return u128_add(U128{A << 32, A >> 32}, U128{B, 0ull});
+}
+
+__device__ __forceinline__ double u128_to_f64(U128 a) {
+  return (double)a.hi * 0x1.0p64 + (double)a.lo;
+}
+
+// ceil(x) for finite x >= 0 (x < 2^127)
+__device__ U128 u128_ceil(double x) {
+  if (!(x > 0.0)) return U128{0ull, 0ull};
+  if (x < 1.0) return U128{1ull, 0ull};
+  const uint64_t bits = (uint64_t)__double_as_longlong(x);
+  const int e = (int)(bits >> 52) - 1023;
+  const uint64_t m = (bits & 0xFFFFFFFFFFFFFull) | 0x10000000000000ull;  // x = m * 2^(e-52)
+  if (e <= 52) {
+    const int sh = 52 - e;
+    uint64_t q = m >> sh;
+    if ((q << sh) != m) ++q;
+    return U128{q, 0ull};
+  }
+  const int sh = e - 52;
+  if (sh < 64) return U128{m << sh, m >> (64 - sh)};
+  return U128{0ull, m << (sh - 64)};
+}
+
+// E = floor(w * 2^63) = a * 2^32 + b from w31 = w * 2^31 in [0, 2^31].
+struct Fix {
+  uint32_t a, b;
+};
+
+__device__ __forceinline__ Fix fix_of(double w31) {
+#pragma clang fp contract(off)
+  const uint32_t a = (uint32_t)w31;
+  const double r = w31 - (double)a;  // exact, in [0, 1)
+  return Fix{a, (uint32_t)(r * 4294967296.0)};
+}
+
+// ---------------------------------------------------------------------------
 
 __device__ __forceinline__ uint32_t orderable(float v) {
-  v = v + 0.0f;
+  v = v + 0.0f;  // -0 -> +0
   const uint32_t u = __float_as_uint(v);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
@@ -43,6 +147,27 @@ __device__ __forceinline__ uint32_t orderable(float v) {
 __device__ __forceinline__ float from_orderable(uint32_t k) {
   const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
   return __uint_as_float(u);
+}
+
+// exp((x - fmax) / tau) * 2^31 with kk = 64 / (tau ln2); x <= fmax.
+__device__ __forceinline__ double weight31(float x, double dmax, double kk,
+                                           const double* __restrict__ tab) {
+#pragma clang fp contract(off)
+  double t = ((double)x - dmax) * kk;
+  t = fmax(t, -90000.0);  // 2^(-90000/64) is zero in fp64
+  const double nn = rint(t);
+  const double r = t - nn;  // exact, |r| <= 1/2
+  const double p = fma(r, fma(r, fma(r, fma(r, fma(r, kC5, kC4), kC3), kC2), kC1), 1.0);
+  const int j = (int)nn;
+  return ldexp(tab[j & 63] * p, (j >> 6) + 31);
+}
+
+// Value bucket of x: floor((fmax - x) * kb), kb = kBuckets / (kYSpan tau),
+// clamped to the last bucket.  Non-decreasing as x decreases.
+__device__ __forceinline__ int bucket_of(float x, float vmax, float kb) {
+#pragma clang fp contract(off)
+  const float y = (vmax - x) * kb;
+  return (int)fminf(y, (float)(kBuckets - 1));
 }
 
 // Philox4x32-10 (Salmon et al., SC'11), word 0 of the output block.
@@ -67,93 +192,115 @@ __device__ uint32_t philox_x0(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3
   return c0;
 }
 
-__device__ __forceinline__ double shfl_xor_f64(double x, int o) {
-  const unsigned long long b = __double_as_longlong(x);
-  const uint32_t lo = __shfl_xor((uint32_t)b, o, 64);
-  const uint32_t hi = __shfl_xor((uint32_t)(b >> 32), o, 64);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+// ---------------------------------------------------------------------------
+// wave and block primitives (fixed order)
+
+__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t x, int o) {
+  const uint32_t lo = __shfl_up((uint32_t)x, o, 64);
+  const uint32_t hi = __shfl_up((uint32_t)(x >> 32), o, 64);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ double shfl_up_f64(double x, int o) {
-  const unsigned long long b = __double_as_longlong(x);
-  const uint32_t lo = __shfl_up((uint32_t)b, o, 64);
-  const uint32_t hi = __shfl_up((uint32_t)(b >> 32), o, 64);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t x, int src) {
+  const uint32_t lo = __shfl((uint32_t)x, src, 64);
+  const uint32_t hi = __shfl((uint32_t)(x >> 32), src, 64);
+  return ((uint64_t)hi << 32) | lo;
 }
 
-constexpr int kRadixBuckets = 4096;  // widest pass: 12 bits
-constexpr int kBucketsPerThread = kRadixBuckets / kSampleThreads;
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
+  const uint32_t lo = __shfl_xor((uint32_t)x, o, 64);
+  const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), o, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
 
-struct SampleShared {
-  double hist[kRadixBuckets];
-  uint32_t cnt[kRadixBuckets];
-  double wred[kSampleWaves];
-  uint32_t ured[kSampleWaves];
-  float fred[kSampleWaves];
-  uint32_t bc_u[2];
-  int32_t pick;
-  int32_t last;
-};
-
-// Block-wide reductions and scans in a fixed order (deterministic).
-__device__ float block_max_f32(float v, SampleShared& sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  __syncthreads();
-  if (lane == 0) sh.fred[wave] = v;
-  __syncthreads();
-  float r = sh.fred[0];
-  for (int w = 1; w < kSampleWaves; ++w) r = fmaxf(r, sh.fred[w]);
-  return r;
+  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+  return v;
 }
 
-__device__ double block_sum_f64(double v, SampleShared& sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_f64(v, o);
-  __syncthreads();
-  if (lane == 0) sh.wred[wave] = v;
-  __syncthreads();
-  double r = 0.0;
-  for (int w = 0; w < kSampleWaves; ++w) r += sh.wred[w];
-  return r;
-}
-
-// Exclusive prefix sum over threads (thread order = id order); *total = sum.
-__device__ double block_exscan_f64(double v, SampleShared& sh, double* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double inc = v;
+__device__ __forceinline__ U128 wave_inscan_u128(U128 v) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const double y = shfl_up_f64(inc, o);
-    if (lane >= o) inc += y;
+    const U128 y{shfl_up_u64(v.lo, o), shfl_up_u64(v.hi, o)};
+    if (lane >= o) v = u128_add(v, y);
   }
+  return v;
+}
+
+__device__ __forceinline__ uint32_t wave_inscan_u32(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(v, o, 64);
+    if (lane >= o) v += y;
+  }
+  return v;
+}
+
+struct SampleShared {
+  union {
+    struct {
+      uint64_t a[kBuckets + 64];  // bucket masses: sums of a (units of 2^-31) and
+      uint64_t b[kBuckets + 64];  // of b (units of 2^-63); 64 per-lane spill slots
+      uint32_t cnt[kBuckets];     // element counts of the key passes
+    } h;
+    struct {
+      uint64_t key[kMaxCand];  // (~orderable key) << 32 | position: ascending = nucleus order
+      uint64_t a[kMaxCand];
+      uint64_t b[kMaxCand];
+    } c;
+  } u;
+  uint64_t seg_a[kMaxSeg];  // nucleus mass per segment
+  uint64_t seg_b[kMaxSeg];
+  uint32_t seg_t[kMaxSeg];  // elements tied at the threshold key per segment
+  double tab[64];
+  U128 xred[kSWaves];
+  uint64_t kred[kSWaves];
+  uint32_t ured[kSWaves];
+  U128 above, claim_base;
+  uint32_t tie_base;
+  int32_t bstar, sel, ncand, cut_idx, cut_pos, claim_seg, tie_seg;
+  uint32_t T;
+};
+
+__device__ unsigned long long block_max_u64(unsigned long long v, SampleShared& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = max(v, (unsigned long long)shfl_xor_u64(v, o));
   __syncthreads();
-  if (lane == 63) sh.wred[wave] = inc;
+  if (lane == 0) sh.kred[wave] = v;
   __syncthreads();
-  double base = 0.0, tot = 0.0;
-  for (int w = 0; w < kSampleWaves; ++w) {
-    if (w < wave) base += sh.wred[w];
-    tot += sh.wred[w];
+  unsigned long long r = sh.kred[0];
+  for (int w = 1; w < kSWaves; ++w) r = max(r, (unsigned long long)sh.kred[w]);
+  return r;
+}
+
+// Exclusive prefix sum over threads (thread order); *total = sum.
+__device__ U128 block_exscan_u128(U128 v, SampleShared& sh, U128* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const U128 inc = wave_inscan_u128(v);
+  __syncthreads();
+  if (lane == 63) sh.xred[wave] = inc;
+  __syncthreads();
+  U128 base{0ull, 0ull}, tot{0ull, 0ull};
+  for (int w = 0; w < kSWaves; ++w) {
+    if (w < wave) base = u128_add(base, sh.xred[w]);
+    tot = u128_add(tot, sh.xred[w]);
   }
   *total = tot;
-  return base + inc - v;
+  return u128_add(base, u128_sub(inc, v));
 }
 
 __device__ uint32_t block_exscan_u32(uint32_t v, SampleShared& sh, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t inc = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
+  const uint32_t inc = wave_inscan_u32(v);
   __syncthreads();
   if (lane == 63) sh.ured[wave] = inc;
   __syncthreads();
   uint32_t base = 0, tot = 0;
-  for (int w = 0; w < kSampleWaves; ++w) {
+  for (int w = 0; w < kSWaves; ++w) {
     if (w < wave) base += sh.ured[w];
     tot += sh.ured[w];
   }
@@ -161,206 +308,462 @@ __device__ uint32_t block_exscan_u32(uint32_t v, SampleShared& sh, uint32_t* tot
   return base + inc - v;
 }
 
-// Apply fn(i) to the thread's elements i = 0 .. cnt-1 in id order.  With
-// CH > 0 the loop is unrolled so register-held values are indexed statically.
-template <int CH, class F>
-__device__ __forceinline__ void for_each_elem(int cnt, F&& fn) {
-  if constexpr (CH > 0) {
+// The lane's four positions p .. p+3 of a chunk; out-of-row ones are invalid.
+template <bool VEC>
+__device__ __forceinline__ void load4(const float* __restrict__ row, int n, int p, float (&x)[4],
+                                      bool (&v)[4]) {
+  if (VEC && p + 3 < n) {
+    const float4 q = *reinterpret_cast<const float4*>(row + p);
+    x[0] = q.x;
+    x[1] = q.y;
+    x[2] = q.z;
+    x[3] = q.w;
 #pragma unroll
-    for (int i = 0; i < CH; ++i)
-      if (i < cnt) fn(i);
+    for (int e = 0; e < 4; ++e) v[e] = true;
   } else {
-    for (int i = 0; i < cnt; ++i) fn(i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = p + e < n;
+      x[e] = v[e] ? row[p + e] : 0.0f;
+    }
   }
 }
 
-// CH > 0: the thread's CH values live in registers (n <= 1024 * CH).
-// CH == 0: values are re-read from f in every pass (any n).
-template <int CH>
-__global__ __launch_bounds__(kSampleThreads) void k_sample(const float* __restrict__ f, int n,
-                                                           const int32_t* __restrict__ ids, int R,
-                                                           float temperature, float top_p,
-                                                           uint32_t seed_lo, uint32_t seed_hi,
-                                                           int32_t* __restrict__ tokens) {
+// VEC: rows start 16-byte aligned (n % 4 == 0), positions load as float4.
+template <bool VEC>
+__global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ f, int n,
+                                                      const unsigned long long* __restrict__ best,
+                                                      int nblk, const int32_t* __restrict__ ids,
+                                                      int R, float temperature, float top_p,
+                                                      uint32_t seed_lo, uint32_t seed_hi,
+                                                      int32_t* __restrict__ tokens) {
   __shared__ SampleShared sh;
   const int m = blockIdx.x;
-  const int t = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float* row = f + (int64_t)m * n;
-  const int ch = CH > 0 ? CH : (n + kSampleThreads - 1) / kSampleThreads;
-  const int p0 = t * ch;
-  const int cnt = max(0, min(n, p0 + ch) - p0);
+  // segments of G positions (a multiple of the chunk), at most kMaxSeg of them
+  const int G = kChunk * ((n + kChunk * kMaxSeg - 1) / (kChunk * kMaxSeg));
+  const int NS = (n + G - 1) / G;
+  const int NC = (n + kChunk - 1) / kChunk;
 
-  float vreg[CH > 0 ? CH : 1];
-  if constexpr (CH > 0) {
-#pragma unroll
-    for (int i = 0; i < CH; ++i) vreg[i] = i < cnt ? row[p0 + i] : 0.0f;
+  if (t < 64) sh.tab[t] = exp2((double)t * (1.0 / 64.0));
+  for (int s = t; s < kMaxSeg; s += kSThreads) {
+    sh.seg_a[s] = 0ull;
+    sh.seg_b[s] = 0ull;
+    sh.seg_t[s] = 0u;
   }
-  auto val = [&](int i) -> float {
-    if constexpr (CH > 0) return vreg[i];
-    else return row[p0 + i];
-  };
+  if (t == 0) {
+    sh.bstar = -1;
+    sh.sel = 0;
+    sh.ncand = 0;
+    sh.cut_idx = -1;
+    sh.cut_pos = n;
+    sh.claim_seg = -1;
+    sh.tie_seg = -1;
+    sh.T = 0u;
+  }
+  // row maximum from the projection's per-tile argmax keys
+  unsigned long long kmax = 0ull;
+  for (int i = t; i < nblk; i += kSThreads) kmax = max(kmax, best[(int64_t)m * kMaxBlocks + i]);
+  kmax = block_max_u64(kmax, sh);  // its barriers also publish the table and the zeroed state
+  const float vmax = from_orderable((uint32_t)(kmax >> 32));
+  const double dmax = (double)vmax;
+  const double kk = 64.0 / (kLn2 * (double)temperature);
+  const float kb = (float)kBuckets / (kYSpan * temperature);
+  const double* tab = sh.tab;
+  auto fix = [&](float x) { return fix_of(weight31(x, dmax, kk, tab)); };
 
-  // 1. max and partition function
-  float lmax = -INFINITY;
-  for_each_elem<CH>(cnt, [&](int i) { lmax = fmaxf(lmax, val(i)); });
-  const float fmax = block_max_f32(lmax, sh);
-  const double tau = (double)temperature;
-  const double dmax = (double)fmax;
-  auto weight = [&](float x) -> double { return exp(((double)x - dmax) / tau); };
-  double lsum = 0.0;
-  for_each_elem<CH>(cnt, [&](int i) { lsum += weight(val(i)); });
-  const double Z = block_sum_f64(lsum, sh);
-
-  // 2. nucleus threshold by radix select on the orderable key
-  const double tp = (double)top_p;
-  uint32_t T = 0u, mask = 0u;
-  double above = 0.0;  // mass of the elements whose key lies above the current prefix
-  uint32_t c_ties = 0u;
-  const bool all = tp >= 1.0;
+  const bool all = !(top_p < 1.0f);
+  int bstar = kBuckets;  // buckets below bstar are wholly inside the nucleus
+  U128 above{0ull, 0ull}, need{0ull, 0ull};
   if (!all) {
-    const double need = tp * Z;
-    constexpr int kShift[3] = {20, 10, 0};
-    constexpr int kBits[3] = {12, 10, 10};
+    for (int b = t; b < kBuckets + 64; b += kSThreads) {
+      sh.u.h.a[b] = 0ull;
+      sh.u.h.b[b] = 0ull;
+    }
+    __syncthreads();
+    // 1. value-bucket mass histogram; the crowded last bucket goes to
+    // per-lane slots folded in afterwards
+    for (int q = wave; q < NC; q += kSWaves) {
+      const int p = q * kChunk + 4 * lane;
+      float x[4];
+      bool v[4];
+      load4<VEC>(row, n, p, x, v);
 #pragma unroll
-    for (int pass = 0; pass < 3; ++pass) {
-      const int shift = kShift[pass], nb = 1 << kBits[pass];
-      for (int b = t; b < nb; b += kSampleThreads) {
-        sh.hist[b] = 0.0;
-        sh.cnt[b] = 0u;
+      for (int e = 0; e < 4; ++e) {
+        const Fix w = fix(x[e]);
+        int b = bucket_of(x[e], vmax, kb);
+        if (!v[e] || b == kBuckets - 1) b = kBuckets + lane;
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.a[b]),
+                  (unsigned long long)(v[e] ? w.a : 0u));
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.b[b]),
+                  (unsigned long long)(v[e] ? w.b : 0u));
       }
-      if (t == 0) {
-        sh.bc_u[0] = 0xFFFFFFFFu;
-        sh.bc_u[1] = 0xFFFFFFFFu;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const uint64_t ta = wave_sum_u64(sh.u.h.a[kBuckets + lane]);
+      const uint64_t tb = wave_sum_u64(sh.u.h.b[kBuckets + lane]);
+      if (lane == 0) {
+        sh.u.h.a[kBuckets - 1] += ta;
+        sh.u.h.b[kBuckets - 1] += tb;
       }
-      __syncthreads();
-      for_each_elem<CH>(cnt, [&](int i) {
-        const float x = val(i);
-        const uint32_t k = orderable(x);
-        if ((k & mask) == T) {
-          const int b = (k >> shift) & (nb - 1);
-          atomicAdd(&sh.hist[b], weight(x));
-          atomicAdd(&sh.cnt[b], 1u);
-        }
-      });
-      __syncthreads();
-      // Thread t owns buckets nb-1-(kBucketsPerThread*t + i): descending keys.
-      double local[kBucketsPerThread];
-      double lsb = 0.0;
+    }
+    __syncthreads();
+    U128 s[kBPT];
+    U128 ls{0ull, 0ull};
 #pragma unroll
-      for (int i = 0; i < kBucketsPerThread; ++i) {
-        const int b = nb - 1 - (kBucketsPerThread * t + i);
-        local[i] = b >= 0 ? sh.hist[b] : 0.0;
-        lsb += local[i];
-      }
-      double tot = 0.0;
-      double acc = above + block_exscan_f64(lsb, sh, &tot);
-      bool crossed = false;
+    for (int i = 0; i < kBPT; ++i) {
+      const int b = kBPT * t + i;
+      s[i] = u128_join(sh.u.h.a[b], sh.u.h.b[b]);
+      ls = u128_add(ls, s[i]);
+    }
+    U128 Z;
+    U128 acc = block_exscan_u128(ls, sh, &Z);
+    need = u128_ceil((double)top_p * u128_to_f64(Z));
+    if (need.lo == 0ull && need.hi == 0ull) need.lo = 1ull;
 #pragma unroll
-      for (int i = 0; i < kBucketsPerThread; ++i) {
-        const int b = nb - 1 - (kBucketsPerThread * t + i);
-        if (b >= 0 && !crossed && sh.cnt[b] != 0u) {
-          if (acc + local[i] >= need) {
-            atomicMin(&sh.bc_u[0], (uint32_t)(nb - 1 - b));  // the highest crossing bucket
-            crossed = true;
-          }
-        }
-        acc += local[i];
+    for (int i = 0; i < kBPT; ++i) {
+      const U128 nxt = u128_add(acc, s[i]);
+      if (u128_lt(acc, need) && !u128_lt(nxt, need)) {
+        sh.bstar = kBPT * t + i;
+        sh.above = acc;
       }
-#pragma unroll
-      for (int i = kBucketsPerThread - 1; i >= 0; --i) {  // lowest non-empty bucket
-        const int b = nb - 1 - (kBucketsPerThread * t + i);
-        if (b >= 0 && sh.cnt[b] != 0u) {
-          atomicMin(&sh.bc_u[1], (uint32_t)b);
-          break;
-        }
-      }
-      __syncthreads();
-      // A target that rounding left above the range's total takes everything.
-      const uint32_t sel =
-          sh.bc_u[0] != 0xFFFFFFFFu ? (uint32_t)(nb - 1) - sh.bc_u[0] : sh.bc_u[1];
-      double part = 0.0;
-#pragma unroll
-      for (int i = 0; i < kBucketsPerThread; ++i) {
-        const int b = nb - 1 - (kBucketsPerThread * t + i);
-        if (b > (int)sel) part += local[i];
-      }
-      above += block_sum_f64(part, sh);
-      T |= sel << shift;
-      mask |= (uint32_t)(nb - 1) << shift;
-      if (pass == 2) {
-        // smallest c in [1, ties] with above + c * e_T >= need
-        const uint32_t nt = sh.cnt[sel];
-        const double eT = weight(from_orderable(T));
-        double cd = ceil((need - above) / eT);
-        uint32_t c = cd < 1.0 ? 1u : (cd > (double)nt ? nt : (uint32_t)cd);
-        while (c > 1u && above + (double)(c - 1u) * eT >= need) --c;
-        while (c < nt && above + (double)c * eT < need) ++c;
-        c_ties = c;
-      }
-      __syncthreads();
+      acc = nxt;
+    }
+    __syncthreads();
+    if (sh.bstar >= 0) {
+      bstar = sh.bstar;
+      above = sh.above;
     }
   }
 
-  // tie ranks in id order, then member masses in id order
-  uint32_t my_ties = 0u;
-  if (!all) for_each_elem<CH>(cnt, [&](int i) { my_ties += orderable(val(i)) == T ? 1u : 0u; });
-  uint32_t tie_tot = 0u;
-  const uint32_t tie_base = block_exscan_u32(my_ties, sh, &tie_tot);
-  auto is_member = [&](float x, uint32_t& tie_seen) -> bool {
-    if (all) return true;
-    const uint32_t k = orderable(x);
-    if (k > T) return true;
-    if (k == T) return tie_base + tie_seen++ < c_ties;
-    return false;
-  };
-  double my_mass = 0.0;
-  int my_last = -1;
-  {
-    uint32_t ts = 0u;
-    for_each_elem<CH>(cnt, [&](int i) {
-      const float x = val(i);
-      if (is_member(x, ts)) {
-        my_mass += weight(x);
-        my_last = p0 + i;
-      }
-    });
-  }
-  double mass = 0.0;
-  const double base = block_exscan_f64(my_mass, sh, &mass);
-
-  // 3. inverse CDF in ascending id order
-  const uint32_t s_idx = (uint32_t)(m / R), r_idx = (uint32_t)(m % R);
-  const uint32_t x0 = philox_x0(r_idx, s_idx, 0u, 0u, seed_lo, seed_hi);
-  const double target = (double)(x0 >> 8) * 0x1.0p-24 * mass;
-  if (t == 0) {
-    sh.pick = 0x7FFFFFFF;
-    sh.last = -1;
-  }
-  __syncthreads();
-  if (my_mass > 0.0 && base <= target && target < base + my_mass) {
-    // The claimed interval comes from a scan whose rounding can differ from
-    // this walk's by an ulp; the walk falls back to its own last member.
-    double run = base;
-    uint32_t ts = 0u;
-    int pos = my_last;
-    bool found = false;
-    for_each_elem<CH>(cnt, [&](int i) {
-      const float x = val(i);
-      if (is_member(x, ts) && !found) {
-        run += weight(x);
-        if (run > target) {
-          pos = p0 + i;
-          found = true;
+  // 2. members of the buckets before b* into segment masses; collect b*
+  for (int q = wave; q < NC; q += kSWaves) {
+    const int p = q * kChunk + 4 * lane;
+    float x[4];
+    bool v[4];
+    load4<VEC>(row, n, p, x, v);
+    uint64_t A = 0ull, B = 0ull;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const Fix w = fix(x[e]);
+      const int b = bucket_of(x[e], vmax, kb);
+      const bool mem = v[e] && b < bstar;
+      A += mem ? w.a : 0u;
+      B += mem ? w.b : 0u;
+      const bool cand = v[e] && b == bstar;
+      const uint64_t bal = __ballot(cand);
+      if (bal) {
+        const int leader = __ffsll((unsigned long long)bal) - 1;
+        int base = 0;
+        if (lane == leader) base = atomicAdd(&sh.ncand, __popcll(bal));
+        base = __shfl(base, leader, 64);
+        if (cand) {
+          const int slot = base + __popcll(bal & ((1ull << lane) - 1ull));
+          if (slot < kMaxCand) {
+            sh.u.c.key[slot] = ((uint64_t)(~orderable(x[e])) << 32) | (uint32_t)(p + e);
+            sh.u.c.a[slot] = w.a;
+            sh.u.c.b[slot] = w.b;
+          }
         }
       }
-    });
-    atomicMin(&sh.pick, pos);
+    }
+    A = wave_sum_u64(A);
+    B = wave_sum_u64(B);
+    if (lane == 0 && (A | B)) {
+      const int sg = q * kChunk / G;
+      atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
+    }
   }
-  if (my_last >= 0) atomicMax(&sh.last, my_last);
   __syncthreads();
-  if (t == 0) {
-    const int pos = sh.pick != 0x7FFFFFFF ? sh.pick : sh.last;
-    tokens[m] = ids[pos >= 0 ? pos : 0];
+
+  if (bstar < kBuckets) {
+    const int nc = sh.ncand;
+    if (nc <= kMaxCand) {
+      // sort the cut bucket by (key desc, position asc), scan, cut
+      int P = 1;
+      while (P < nc) P <<= 1;
+      for (int i = nc + t; i < P; i += kSThreads) {
+        sh.u.c.key[i] = ~0ull;
+        sh.u.c.a[i] = 0ull;
+        sh.u.c.b[i] = 0ull;
+      }
+      __syncthreads();
+      for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+          if (t < P / 2) {
+            const int i = 2 * t - (t & (j - 1));
+            const int l = i + j;
+            const uint64_t ki = sh.u.c.key[i], kl = sh.u.c.key[l];
+            if ((ki > kl) == ((i & k) == 0)) {
+              sh.u.c.key[i] = kl;
+              sh.u.c.key[l] = ki;
+              const uint64_t ai = sh.u.c.a[i], bi = sh.u.c.b[i];
+              sh.u.c.a[i] = sh.u.c.a[l];
+              sh.u.c.b[i] = sh.u.c.b[l];
+              sh.u.c.a[l] = ai;
+              sh.u.c.b[l] = bi;
+            }
+          }
+          __syncthreads();
+        }
+      }
+      const int i0 = 2 * t, i1 = 2 * t + 1;
+      const U128 e0 = i0 < nc ? u128_join(sh.u.c.a[i0], sh.u.c.b[i0]) : U128{0ull, 0ull};
+      const U128 e1 = i1 < nc ? u128_join(sh.u.c.a[i1], sh.u.c.b[i1]) : U128{0ull, 0ull};
+      U128 tot;
+      const U128 ex0 = u128_add(above, block_exscan_u128(u128_add(e0, e1), sh, &tot));
+      const U128 ex1 = u128_add(ex0, e0);
+      if (i0 < nc && u128_lt(ex0, need) && !u128_lt(ex1, need)) sh.cut_idx = i0;
+      if (i1 < nc && u128_lt(ex1, need) && !u128_lt(u128_add(ex1, e1), need)) sh.cut_idx = i1;
+      __syncthreads();
+      const int jc = sh.cut_idx;
+      for (int i = t; i <= jc; i += kSThreads) {
+        const int pos = (int)(uint32_t)sh.u.c.key[i];
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[pos / G]),
+                  (unsigned long long)sh.u.c.a[i]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[pos / G]),
+                  (unsigned long long)sh.u.c.b[i]);
+      }
+      if (t == 0 && jc >= 0) {
+        sh.T = ~(uint32_t)(sh.u.c.key[jc] >> 32);
+        sh.cut_pos = (int)(uint32_t)sh.u.c.key[jc];
+      }
+    } else {
+      // exact radix select on the keys of bucket b*
+      uint32_t Tk = 0u, kmask = 0u, nt = 0u;
+      U128 ab = above;
+      constexpr int kShift[3] = {21, 10, 0};
+      constexpr int kBits[3] = {11, 11, 10};
+      for (int pass = 0; pass < 3; ++pass) {
+        const int shift = kShift[pass], nb = 1 << kBits[pass];
+        __syncthreads();  // earlier readers of the histogram are done
+        for (int b = t; b < nb; b += kSThreads) {
+          sh.u.h.a[b] = 0ull;
+          sh.u.h.b[b] = 0ull;
+          sh.u.h.cnt[b] = 0u;
+        }
+        __syncthreads();
+        for (int q = wave; q < NC; q += kSWaves) {
+          const int p = q * kChunk + 4 * lane;
+          float x[4];
+          bool v[4];
+          load4<VEC>(row, n, p, x, v);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const uint32_t key = orderable(x[e]);
+            if (v[e] && bucket_of(x[e], vmax, kb) == bstar && (key & kmask) == Tk) {
+              const int b = (int)((key >> shift) & (uint32_t)(nb - 1));
+              const Fix w = fix(x[e]);
+              atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.a[b]),
+                        (unsigned long long)w.a);
+              atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.b[b]),
+                        (unsigned long long)w.b);
+              atomicAdd(&sh.u.h.cnt[b], 1u);
+            }
+          }
+        }
+        __syncthreads();
+        // thread t owns key buckets nb-1-(kBPT t + i): descending keys
+        U128 ks[kBPT];
+        U128 kls{0ull, 0ull};
+#pragma unroll
+        for (int i = 0; i < kBPT; ++i) {
+          const int b = nb - 1 - (kBPT * t + i);
+          ks[i] = b >= 0 ? u128_join(sh.u.h.a[b], sh.u.h.b[b]) : U128{0ull, 0ull};
+          kls = u128_add(kls, ks[i]);
+        }
+        U128 ktot;
+        U128 kacc = u128_add(ab, block_exscan_u128(kls, sh, &ktot));
+#pragma unroll
+        for (int i = 0; i < kBPT; ++i) {
+          const U128 nxt = u128_add(kacc, ks[i]);
+          if (u128_lt(kacc, need) && !u128_lt(nxt, need)) {
+            sh.sel = nb - 1 - (kBPT * t + i);
+            sh.above = kacc;
+          }
+          kacc = nxt;
+        }
+        __syncthreads();
+        const int sel = min(max(sh.sel, 0), nb - 1);
+        ab = sh.above;
+        nt = sh.u.h.cnt[sel];
+        Tk |= (uint32_t)sel << shift;
+        kmask |= (uint32_t)(nb - 1) << shift;
+      }
+      // the c-th element tied at Tk in id order completes the nucleus:
+      // smallest c >= 1 with ab + c * E(Tk) >= need
+      const Fix wt = fix(from_orderable(Tk));
+      const U128 WT = u128_join(wt.a, wt.b);
+      const double cd = ceil(u128_to_f64(u128_sub(need, ab)) / u128_to_f64(WT));
+      uint32_t c = cd < 1.0 ? 1u : (cd > (double)nt ? nt : (uint32_t)cd);
+      while (c > 1u && !u128_lt(u128_add(ab, u128_mul32(WT, c - 1u)), need)) --c;
+      while (c < nt && u128_lt(u128_add(ab, u128_mul32(WT, c)), need)) ++c;
+      // ties per segment, then the segment and the lane holding the c-th
+      for (int q = wave; q < NC; q += kSWaves) {
+        const int p = q * kChunk + 4 * lane;
+        float x[4];
+        bool v[4];
+        load4<VEC>(row, n, p, x, v);
+        uint32_t ties = 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ties += (v[e] && orderable(x[e]) == Tk) ? 1u : 0u;
+        ties = (uint32_t)wave_sum_u64(ties);
+        if (lane == 0 && ties) atomicAdd(&sh.seg_t[q * kChunk / G], ties);
+      }
+      __syncthreads();
+      uint32_t tc[kSPT];
+      uint32_t tl = 0u;
+#pragma unroll
+      for (int i = 0; i < kSPT; ++i) {
+        const int sg = kSPT * t + i;
+        tc[i] = sg < NS ? sh.seg_t[sg] : 0u;
+        tl += tc[i];
+      }
+      uint32_t ttot;
+      uint32_t tb = block_exscan_u32(tl, sh, &ttot);
+#pragma unroll
+      for (int i = 0; i < kSPT; ++i) {
+        if (tb < c && c <= tb + tc[i]) {
+          sh.tie_seg = kSPT * t + i;
+          sh.tie_base = tb;
+        }
+        tb += tc[i];
+      }
+      __syncthreads();
+      if (wave == 0 && sh.tie_seg >= 0) {
+        const int sg = sh.tie_seg;
+        uint32_t run = sh.tie_base;
+        const int end = min(n, (sg + 1) * G);
+        for (int cb = sg * G; cb < end; cb += kChunk) {
+          const int p = cb + 4 * lane;
+          float x[4];
+          bool v[4];
+          load4<VEC>(row, n, p, x, v);
+          bool tie[4];
+          uint32_t lt = 0u;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            tie[e] = v[e] && orderable(x[e]) == Tk;
+            lt += tie[e] ? 1u : 0u;
+          }
+          const uint32_t inc = wave_inscan_u32(lt);
+          uint32_t seen = run + inc - lt;
+          int hit = -1;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (tie[e] && ++seen == c && hit < 0) hit = p + e;
+          }
+          const uint64_t bal = __ballot(hit >= 0);
+          if (bal) {
+            const int src = __ffsll((unsigned long long)bal) - 1;
+            const int pos = __shfl(hit, src, 64);
+            if (lane == 0) {
+              sh.T = Tk;
+              sh.cut_pos = pos;
+            }
+            break;
+          }
+          run += __shfl(inc, 63, 64);
+        }
+      }
+      __syncthreads();
+      // members of bucket b*
+      const uint32_t T = sh.T;
+      const int cut = sh.cut_pos;
+      for (int q = wave; q < NC; q += kSWaves) {
+        const int p = q * kChunk + 4 * lane;
+        float x[4];
+        bool v[4];
+        load4<VEC>(row, n, p, x, v);
+        uint64_t A = 0ull, B = 0ull;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t key = orderable(x[e]);
+          if (v[e] && bucket_of(x[e], vmax, kb) == bstar && (key > T || (key == T && p + e <= cut))) {
+            const Fix w = fix(x[e]);
+            A += w.a;
+            B += w.b;
+          }
+        }
+        A = wave_sum_u64(A);
+        B = wave_sum_u64(B);
+        if (lane == 0 && (A | B)) {
+          const int sg = q * kChunk / G;
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // Nucleus: key > T, or key == T and position <= cut (T = 0, cut = n: all).
+  const uint32_t T = sh.T;
+  const int cut = sh.cut_pos;
+
+  // 3. segment masses in id order, then the inverse CDF inside one segment
+  U128 sm[kSPT];
+  U128 sl{0ull, 0ull};
+#pragma unroll
+  for (int i = 0; i < kSPT; ++i) {
+    const int sg = kSPT * t + i;
+    sm[i] = sg < NS ? u128_join(sh.seg_a[sg], sh.seg_b[sg]) : U128{0ull, 0ull};
+    sl = u128_add(sl, sm[i]);
+  }
+  U128 mass;
+  U128 sb = block_exscan_u128(sl, sh, &mass);
+  const uint32_t s_idx = (uint32_t)(m / R), r_idx = (uint32_t)(m % R);
+  const uint32_t u24 = philox_x0(r_idx, s_idx, 0u, 0u, seed_lo, seed_hi) >> 8;
+  const U128 target = u128_mul32(mass, u24);
+#pragma unroll
+  for (int i = 0; i < kSPT; ++i) {
+    const U128 nxt = u128_add(sb, sm[i]);
+    if (!u128_lt(target, u128_shl24(sb)) && u128_lt(target, u128_shl24(nxt))) {
+      sh.claim_seg = kSPT * t + i;
+      sh.claim_base = sb;
+    }
+    sb = nxt;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int sg = sh.claim_seg;
+    int pick = -1;
+    if (sg >= 0) {
+      U128 run = sh.claim_base;
+      const int end = min(n, (sg + 1) * G);
+      for (int cb = sg * G; cb < end && pick < 0; cb += kChunk) {
+        const int p = cb + 4 * lane;
+        float x[4];
+        bool v[4];
+        load4<VEC>(row, n, p, x, v);
+        U128 li[4];
+        U128 l{0ull, 0ull};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t key = orderable(x[e]);
+          if (v[e] && (key > T || (key == T && p + e <= cut))) {
+            const Fix w = fix(x[e]);
+            l = u128_add(l, u128_join(w.a, w.b));
+          }
+          li[e] = l;
+        }
+        const U128 inc = wave_inscan_u128(l);
+        const U128 lb = u128_add(run, u128_sub(inc, l));
+        int hit = -1;
+#pragma unroll
+        for (int e = 3; e >= 0; --e)
+          if (u128_lt(target, u128_shl24(u128_add(lb, li[e])))) hit = e;
+        const uint64_t bal = __ballot(hit >= 0);
+        if (bal) {
+          const int src = __ffsll((unsigned long long)bal) - 1;
+          pick = cb + 4 * src + __shfl(hit, src, 64);
+        }
+        run = u128_add(run, U128{shfl_u64(inc.lo, 63), shfl_u64(inc.hi, 63)});
+      }
+    }
+    if (lane == 0) tokens[m] = ids[pick >= 0 ? pick : 0];
   }
 }
 
@@ -374,18 +777,19 @@ __global__ void k_accept(const int32_t* __restrict__ tokens, const int32_t* __re
   accept[s] = a;
 }
 
-hipError_t launch_sample(const float* f, int M, int n, const int32_t* ids, int R,
-                         float temperature, float top_p, uint64_t seed, int32_t* tokens,
-                         hipStream_t s) {
+hipError_t launch_sample(const float* f, int M, int n, const unsigned long long* best, int nblk,
+                         const int32_t* ids, int R, float temperature, float top_p, uint64_t seed,
+                         int32_t* tokens, hipStream_t s) {
+  if (n < 1 || nblk < 1 || nblk > kMaxBlocks) return hipErrorInvalidValue;
+  if ((int64_t)(n + kChunk * kMaxSeg - 1) / (kChunk * kMaxSeg) * kChunk * kMaxSeg >= (1ll << 31))
+    return hipErrorInvalidValue;
   const uint32_t lo = (uint32_t)seed, hi = (uint32_t)(seed >> 32);
-  if (n <= kSampleThreads * 16)
-    hipLaunchKernelGGL(k_sample<16>, dim3(M), dim3(kSampleThreads), 0, s, f, n, ids, R,
-                       temperature, top_p, lo, hi, tokens);
-  else if (n <= kSampleThreads * 64)
-    hipLaunchKernelGGL(k_sample<64>, dim3(M), dim3(kSampleThreads), 0, s, f, n, ids, R,
+  const bool vec = n % 4 == 0 && (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_sample<true>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
                        temperature, top_p, lo, hi, tokens);
   else
-    hipLaunchKernelGGL(k_sample<0>, dim3(M), dim3(kSampleThreads), 0, s, f, n, ids, R,
+    hipLaunchKernelGGL(k_sample<false>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
                        temperature, top_p, lo, hi, tokens);
   return hipGetLastError();
 }

@@ -396,8 +396,10 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   }
   if (mode == SPH_SAMPLE) {
     hipError_t e = traced("fuse_sample", s, [&] {
-      return sph::launch_sample(fused, (int)M, (int)n, subset->d_ids, (int)rows_per_session,
-                                temperature, top_p, seed, tokens_out, s);
+      return sph::launch_sample(fused, (int)M, (int)n,
+                                reinterpret_cast<const unsigned long long*>(best), nblk,
+                                subset->d_ids, (int)rows_per_session, temperature, top_p, seed,
+                                tokens_out, s);
     });
     if (e != hipSuccess) return hip_fail(e, "sampling launch");
     e = traced("fuse_accept", s, [&] {

@@ -83,9 +83,11 @@ int mfma_n_tiles(int n);
 hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
                            float clip, int8_t* q, float* scale, hipStream_t s);
 
-hipError_t launch_sample(const float* f, int M, int n, const int32_t* ids, int R,
-                         float temperature, float top_p, uint64_t seed, int32_t* tokens,
-                         hipStream_t s);
+// best/nblk: the endpoint projection's per-tile argmax keys of each row
+// (row stride kMaxBlocks), whose maximum gives the row's largest logit.
+hipError_t launch_sample(const float* f, int M, int n, const unsigned long long* best, int nblk,
+                         const int32_t* ids, int R, float temperature, float top_p, uint64_t seed,
+                         int32_t* tokens, hipStream_t s);
 hipError_t launch_accept(const int32_t* tokens, const int32_t* drafts, int n_sessions, int R,
                          int32_t* accept, hipStream_t s);
 

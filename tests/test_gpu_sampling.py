@@ -19,7 +19,7 @@ import torch
 
 import oracle
 import paper_2607_13093_amd as sph
-from synth import CONFIGS, Config, make_drafts, make_workload
+from synth import CONFIGS, Config, make_drafts, make_workload, scale_rows_bf16
 
 import parity as P
 
@@ -145,6 +145,35 @@ def test_sample_ties_at_the_nucleus_cut():
     assert not f.any()
     pos = np.searchsorted(wl.subset, tok)
     assert pos.max() <= 900 and stats["D"]["exempt"] == 0
+
+
+def test_sample_many_ties_radix_path():
+    # 5000 all-zero logits: the cut lies among more tied elements than are
+    # ranked directly, so the key radix select and the tie position decide;
+    # top_p = 0.9005 (0.90049999952 in fp32) keeps the first 4503 ids
+    cfg = Config("ties_many", 52, d=128, d_end=16, vocab=12000, n_sub=5000, subset_kind="choice",
+                 sessions=6, rows_per_session=2, mode="sample", temperature=0.7, top_p=0.9005,
+                 philox_seed=101)
+    wl = make_workload(cfg)
+    h = np.zeros_like(wl.h_bits)
+    stats, tok, f = run_sample_case(wl, h_bits=h, tag="ties (radix path)")
+    pos = np.searchsorted(wl.subset, tok)
+    assert pos.max() <= 4502 and stats["D"]["exempt"] == 0
+
+
+def test_sample_narrow_rows_radix_path():
+    # h scaled by 1e-4: every row's logits span far less than one value
+    # bucket ((max - min) / tau < 40 / 4096), so thousands of distinct keys
+    # share the cut bucket and the radix select over keys decides
+    cfg = Config("narrow", 53, d=256, d_end=32, vocab=9000, n_sub=6000, subset_kind="choice",
+                 sessions=4, rows_per_session=3, mode="sample", temperature=0.7, top_p=0.9,
+                 philox_seed=202)
+    wl = make_workload(cfg)
+    h = scale_rows_bf16(wl.h_bits, np.arange(cfg.M), 1e-4)
+    stats, tok, f = run_sample_case(wl, h_bits=h, tag="narrow rows (radix path)")
+    spread = (f.max(axis=1).astype(np.float64) - f.min(axis=1)) / np.float32(cfg.temperature)
+    assert (spread < 0.9 * 40.0 / 4096).all(), spread.max()
+    assert len(np.unique(f[0])) > 1024
 
 
 def test_sample_top_p_to_zero_is_greedy():
