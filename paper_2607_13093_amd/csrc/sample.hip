@@ -12,29 +12,36 @@
 // N = rint(t), r = t - N (|r| <= 1/2), e = 2^(N>>6) * 2^((N&63)/64) * 2^(r/64),
 // the middle factor from a 64-entry table and 2^(r/64) a degree-5 Taylor
 // polynomial (truncation below 4e-17).  Every use of a weight evaluates the
-// same operations with contraction off, so a weight is bit-identical wherever
-// it is recomputed.
+// same operations with contraction off, so it is bit-identical wherever it is
+// recomputed.
 //
-// Exact masses.  Each weight e in [0, 1] becomes E = floor(e * 2^63), held as
-// E = a * 2^32 + b (a <= 2^31, b < 2^32); sums of a and of b over at most 2^22
-// elements fit 64 bits, so every mass is an exact integer, every decision
-// (nucleus cut, inverse CDF) is exact for these weights and independent of
-// the order of summation, and the kernel is deterministic.  E misses
-// e * 2^63 by less than one unit (relative 2^-63 of the largest weight).
+// Exact masses.  Each weight e in [0, 1] becomes E = floor(e * 2^56), held as
+// E = a * 2^28 + b (a <= 2^28, b < 2^28).  Masses are exact integer sums of
+// E, so the nucleus cut and the inverse CDF are exact for these weights,
+// independent of summation order, and the kernel is deterministic.  E misses
+// e * 2^56 by less than one unit.
 //
-//   1. A mass histogram over 2048 value buckets of y = (fmax - f)/tau in
-//      [0, 40) (the last also takes y >= 40, whose elements each weigh below
-//      5e-18).  Bucket order is value order, so the nucleus -- the shortest
-//      prefix of (p desc, id asc) whose mass reaches top_p * Z -- ends in the
-//      first bucket b* whose running mass reaches the target.
-//   2. One pass adds the members of buckets before b* into per-segment masses
-//      (segments: runs of consecutive positions, at most 1024 per row) and
-//      collects the elements of b*.  Up to 1024 of them are sorted by
-//      (key desc, position asc) in LDS; a scan over that order finds the
-//      element completing the nucleus.  More (near-constant rows) go through
-//      an exact radix select over the 32-bit orderable key (11 + 11 + 10
-//      bits); the cut among elements tied at the threshold key is the c-th in
-//      id order.  Nucleus = {key > T} + {key == T, position <= cut}.
+//   1. An approximate histogram (fp32 weights, integer atomics) over 4096
+//      value buckets of y = (fmax - f)/tau in [0, 40) (the last bucket also
+//      takes y >= 40, whose elements each weigh below 5e-18) locates the
+//      bucket where the running mass reaches top_p * Z: bucket order is value
+//      order, so the nucleus -- the shortest prefix of (p desc, id asc)
+//      reaching the target -- ends there.  The window is that bucket, widened
+//      by a neighbour where the estimate lies near a bucket edge.
+//   2. One exact pass: Z; the masses of the buckets below the window, per
+//      segment (runs of consecutive positions, at most 512 per row); the
+//      window's elements into an LDS list.  An exact histogram of the list
+//      over 128 sub-buckets per bucket finds the sub-bucket holding the cut;
+//      one wave ranks its few elements by (key desc, position asc) to find
+//      the element completing the nucleus.  The nucleus is
+//      {key > T} + {key == T, position <= cut}.
+//      Should the window miss the cut or overflow the list, an exact
+//      histogram over groups of 4 buckets picks the group and the pass is
+//      redone on it; a sub-bucket holding more than 64 elements is ranked by
+//      a bitonic sort of the list, and a group with more than 1024 elements
+//      goes through an exact radix select over its keys (8 bits per pass),
+//      the cut among elements tied at the threshold key being the c-th in id
+//      order.
 //   3. u = top 24 bits of word 0 of Philox4x32-10 (key = seed halves,
 //      counter = (row in session, session, 0, 0)).  The token is the first
 //      nucleus member in id order whose running mass M has
@@ -46,14 +53,18 @@ namespace sph {
 
 constexpr int kSThreads = 512;
 constexpr int kSWaves = kSThreads / 64;
-constexpr int kBuckets = 2048;     // value buckets; also the widest key pass (11 bits)
+constexpr int kBuckets = 4096;     // value buckets of (fmax - f)/tau over [0, kYSpan)
 constexpr int kBPT = kBuckets / kSThreads;
-constexpr int kMaxSeg = 1024;      // segments per row
-constexpr int kSPT = kMaxSeg / kSThreads;
-constexpr int kMaxCand = 1024;     // elements of the cut bucket sorted directly
+constexpr int kCoarse = 1024;      // exact fallback histogram: 4 value buckets each
+constexpr int kSub = 128;          // sub-buckets per bucket of the window
+constexpr int kMaxSub = 4 * kSub;  // window of at most 4 buckets
+constexpr int kMaxSeg = kSThreads; // segments per row, one per thread in scans
+constexpr int kMaxCand = 1024;     // window elements held in LDS
 constexpr int kChunk = 256;        // positions per wave iteration
-constexpr float kYSpan = 40.0f;    // buckets cover (fmax - f)/tau in [0, 40)
-static_assert(kMaxCand <= 2 * kSThreads, "one candidate pair per thread");
+constexpr float kYSpan = 40.0f;
+static_assert(kMaxCand == 2 * kSThreads, "two list entries per thread");
+static_assert(kCoarse == 2 * kSThreads, "two coarse buckets per thread");
+static_assert(kMaxSub == kSThreads, "one sub-bucket per thread");
 
 // 2^(r/64) = exp(r * ln2/64): Taylor coefficients (ln2/64)^k / k!
 constexpr double kLn2 = 0.6931471805599453;
@@ -65,7 +76,7 @@ constexpr double kC4 = kL64 * kL64 * kL64 * kL64 / 24.0;
 constexpr double kC5 = kL64 * kL64 * kL64 * kL64 * kL64 / 120.0;
 
 // ---------------------------------------------------------------------------
-// 128-bit unsigned integers (masses in units of 2^-63)
+// 128-bit unsigned integers (masses in units of 2^-56)
 
 struct U128 {
   uint64_t lo, hi;
@@ -97,9 +108,9 @@ __device__ __forceinline__ U128 u128_mul32(U128 a, uint32_t m) {
   return U128{a.lo * m, a.hi * m + __umul64hi(a.lo, (uint64_t)m)};
 }
 
-// A * 2^32 + B
+// A * 2^28 + B
 __device__ __forceinline__ U128 u128_join(uint64_t A, uint64_t B) {
-  return u128_add(U128{A << 32, A >> 32}, U128{B, 0ull});
+  return u128_add(U128{A << 28, A >> 36}, U128{B, 0ull});
 }
 
 __device__ __forceinline__ double u128_to_f64(U128 a) {
@@ -124,16 +135,16 @@ __device__ U128 u128_ceil(double x) {
   return U128{0ull, m << (sh - 64)};
 }
 
-// E = floor(w * 2^63) = a * 2^32 + b from w31 = w * 2^31 in [0, 2^31].
+// E = floor(w * 2^56) = a * 2^28 + b from w28 = w * 2^28 in [0, 2^28].
 struct Fix {
   uint32_t a, b;
 };
 
-__device__ __forceinline__ Fix fix_of(double w31) {
+__device__ __forceinline__ Fix fix_of(double w28) {
 #pragma clang fp contract(off)
-  const uint32_t a = (uint32_t)w31;
-  const double r = w31 - (double)a;  // exact, in [0, 1)
-  return Fix{a, (uint32_t)(r * 4294967296.0)};
+  const uint32_t a = (uint32_t)w28;
+  const double r = w28 - (double)a;  // exact, in [0, 1)
+  return Fix{a, (uint32_t)(r * 268435456.0)};
 }
 
 // ---------------------------------------------------------------------------
@@ -149,25 +160,35 @@ __device__ __forceinline__ float from_orderable(uint32_t k) {
   return __uint_as_float(u);
 }
 
-// exp((x - fmax) / tau) * 2^31 with kk = 64 / (tau ln2); x <= fmax.
-__device__ __forceinline__ double weight31(float x, double dmax, double kk,
+// exp((x - fmax) / tau) * 2^28 with kk = 64 / (tau ln2), c0 = -fmax * kk.
+__device__ __forceinline__ double weight28(float x, double kk, double c0,
                                            const double* __restrict__ tab) {
 #pragma clang fp contract(off)
-  double t = ((double)x - dmax) * kk;
-  t = fmax(t, -90000.0);  // 2^(-90000/64) is zero in fp64
+  double t = fma((double)x, kk, c0);
+  t = fmin(fmax(t, -90000.0), 0.0);  // 2^(-90000/64) is zero in fp64; x <= fmax
   const double nn = rint(t);
   const double r = t - nn;  // exact, |r| <= 1/2
   const double p = fma(r, fma(r, fma(r, fma(r, fma(r, kC5, kC4), kC3), kC2), kC1), 1.0);
   const int j = (int)nn;
-  return ldexp(tab[j & 63] * p, (j >> 6) + 31);
+  return ldexp(tab[j & 63] * p, (j >> 6) + 28);
 }
 
-// Value bucket of x: floor((fmax - x) * kb), kb = kBuckets / (kYSpan tau),
-// clamped to the last bucket.  Non-decreasing as x decreases.
-__device__ __forceinline__ int bucket_of(float x, float vmax, float kb) {
+// (fmax - x) * kb with kb = kBuckets / (kYSpan tau): bucket units, >= 0.
+__device__ __forceinline__ float ypos(float x, float vmax, float kb) {
 #pragma clang fp contract(off)
-  const float y = (vmax - x) * kb;
+  return (vmax - x) * kb;
+}
+
+// Value bucket: floor(ypos), the last bucket taking everything beyond.
+// Non-decreasing as x decreases.
+__device__ __forceinline__ int bucket_of(float y) {
   return (int)fminf(y, (float)(kBuckets - 1));
+}
+
+// Sub-bucket: floor(ypos * kSub) (exact scaling), consistent with bucket_of:
+// bucket b holds sub-buckets [kSub b, kSub b + kSub - 1].
+__device__ __forceinline__ int subbucket_of(float y) {
+  return (int)fminf(y * (float)kSub, (float)(kSub * kBuckets - 1));
 }
 
 // Philox4x32-10 (Salmon et al., SC'11), word 0 of the output block.
@@ -241,28 +262,35 @@ __device__ __forceinline__ uint32_t wave_inscan_u32(uint32_t v) {
 
 struct SampleShared {
   union {
-    struct {
-      uint64_t a[kBuckets + 64];  // bucket masses: sums of a (units of 2^-31) and
-      uint64_t b[kBuckets + 64];  // of b (units of 2^-63); 64 per-lane spill slots
-      uint32_t cnt[kBuckets];     // element counts of the key passes
-    } h;
+    unsigned long long hf[kBuckets + 64];  // approximate bucket masses (units of 2^-32)
     struct {
       uint64_t key[kMaxCand];  // (~orderable key) << 32 | position: ascending = nucleus order
       uint64_t a[kMaxCand];
       uint64_t b[kMaxCand];
+      uint64_t sa[kMaxSub];  // exact sub-bucket masses of the window
+      uint64_t sb[kMaxSub];
+      uint32_t scnt[kMaxSub];
     } c;
+    struct {
+      uint64_t a[kCoarse + 64];  // exact group masses, 64 per-lane spill slots
+      uint64_t b[kCoarse + 64];
+      uint32_t cnt[256];  // element counts of the key passes
+    } h;
   } u;
   uint64_t seg_a[kMaxSeg];  // nucleus mass per segment
   uint64_t seg_b[kMaxSeg];
   uint32_t seg_t[kMaxSeg];  // elements tied at the threshold key per segment
+  uint64_t wkey[64];        // the crossing sub-bucket's elements
+  uint64_t wa[64];
+  uint64_t wb[64];
   double tab[64];
   U128 xred[kSWaves];
+  double dred[kSWaves];
   uint64_t kred[kSWaves];
   uint32_t ured[kSWaves];
   U128 above, claim_base;
-  uint32_t tie_base;
-  int32_t bstar, sel, ncand, cut_idx, cut_pos, claim_seg, tie_seg;
-  uint32_t T;
+  uint32_t tie_base, T;
+  int32_t bsel, lo, hi, ncand, cut_idx, cut_pos, claim_seg, tie_seg;
 };
 
 __device__ unsigned long long block_max_u64(unsigned long long v, SampleShared& sh) {
@@ -277,7 +305,7 @@ __device__ unsigned long long block_max_u64(unsigned long long v, SampleShared& 
   return r;
 }
 
-// Exclusive prefix sum over threads (thread order); *total = sum.
+// Exclusive prefix sums over threads (thread order); *total = sum.
 __device__ U128 block_exscan_u128(U128 v, SampleShared& sh, U128* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const U128 inc = wave_inscan_u128(v);
@@ -291,6 +319,27 @@ __device__ U128 block_exscan_u128(U128 v, SampleShared& sh, U128* total) {
   }
   *total = tot;
   return u128_add(base, u128_sub(inc, v));
+}
+
+__device__ double block_exscan_f64(double v, SampleShared& sh, double* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double inc = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double y =
+        __longlong_as_double((long long)shfl_up_u64((uint64_t)__double_as_longlong(inc), o));
+    if (lane >= o) inc += y;
+  }
+  __syncthreads();
+  if (lane == 63) sh.dred[wave] = inc;
+  __syncthreads();
+  double base = 0.0, tot = 0.0;
+  for (int w = 0; w < kSWaves; ++w) {
+    if (w < wave) base += sh.dred[w];
+    tot += sh.dred[w];
+  }
+  *total = tot;
+  return base + inc - v;
 }
 
 __device__ uint32_t block_exscan_u32(uint32_t v, SampleShared& sh, uint32_t* total) {
@@ -308,7 +357,14 @@ __device__ uint32_t block_exscan_u32(uint32_t v, SampleShared& sh, uint32_t* tot
   return base + inc - v;
 }
 
-// The lane's four positions p .. p+3 of a chunk; out-of-row ones are invalid.
+__device__ __forceinline__ U128 block_sum_u128(U128 v, SampleShared& sh) {
+  U128 tot;
+  block_exscan_u128(v, sh, &tot);
+  return tot;
+}
+
+// The lane's four positions p .. p+3 of a chunk; positions past the row are
+// invalid and not read.
 template <bool VEC>
 __device__ __forceinline__ void load4(const float* __restrict__ row, int n, int p, float (&x)[4],
                                       bool (&v)[4]) {
@@ -329,14 +385,28 @@ __device__ __forceinline__ void load4(const float* __restrict__ row, int n, int 
   }
 }
 
+// fn(q, p, x, v) on every chunk q of the row, chunks dealt to waves in turn,
+// two chunks loaded ahead per wave iteration.
+template <bool VEC, class F>
+__device__ __forceinline__ void for_chunks(const float* __restrict__ row, int n, int NC, F&& fn) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int q = wave; q < NC; q += 2 * kSWaves) {
+    const int q2 = q + kSWaves;
+    float x0[4], x1[4];
+    bool v0[4], v1[4];
+    load4<VEC>(row, n, q * kChunk + 4 * lane, x0, v0);
+    load4<VEC>(row, n, q2 * kChunk + 4 * lane, x1, v1);
+    fn(q, q * kChunk + 4 * lane, x0, v0);
+    if (q2 < NC) fn(q2, q2 * kChunk + 4 * lane, x1, v1);
+  }
+}
+
 // VEC: rows start 16-byte aligned (n % 4 == 0), positions load as float4.
 template <bool VEC>
-__global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ f, int n,
-                                                      const unsigned long long* __restrict__ best,
-                                                      int nblk, const int32_t* __restrict__ ids,
-                                                      int R, float temperature, float top_p,
-                                                      uint32_t seed_lo, uint32_t seed_hi,
-                                                      int32_t* __restrict__ tokens) {
+__global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_sample(
+    const float* __restrict__ f, int n, const unsigned long long* __restrict__ best, int nblk,
+    const int32_t* __restrict__ ids, int R, float temperature, float top_p, uint32_t seed_lo,
+    uint32_t seed_hi, int32_t* __restrict__ tokens) {
   __shared__ SampleShared sh;
   const int m = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -347,14 +417,11 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
   const int NC = (n + kChunk - 1) / kChunk;
 
   if (t < 64) sh.tab[t] = exp2((double)t * (1.0 / 64.0));
-  for (int s = t; s < kMaxSeg; s += kSThreads) {
-    sh.seg_a[s] = 0ull;
-    sh.seg_b[s] = 0ull;
-    sh.seg_t[s] = 0u;
-  }
+  sh.seg_a[t] = 0ull;
+  sh.seg_b[t] = 0ull;
+  sh.seg_t[t] = 0u;
   if (t == 0) {
-    sh.bstar = -1;
-    sh.sel = 0;
+    sh.bsel = -1;
     sh.ncand = 0;
     sh.cut_idx = -1;
     sh.cut_pos = n;
@@ -367,195 +434,338 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
   for (int i = t; i < nblk; i += kSThreads) kmax = max(kmax, best[(int64_t)m * kMaxBlocks + i]);
   kmax = block_max_u64(kmax, sh);  // its barriers also publish the table and the zeroed state
   const float vmax = from_orderable((uint32_t)(kmax >> 32));
-  const double dmax = (double)vmax;
   const double kk = 64.0 / (kLn2 * (double)temperature);
+  const double c0 = -(double)vmax * kk;
   const float kb = (float)kBuckets / (kYSpan * temperature);
   const double* tab = sh.tab;
-  auto fix = [&](float x) { return fix_of(weight31(x, dmax, kk, tab)); };
+  auto fix = [&](float x) { return fix_of(weight28(x, kk, c0, tab)); };
+  auto member = [&](float x, int pos, uint32_t T, int cut) {
+    const uint32_t k = orderable(x);
+    return k > T || (k == T && pos <= cut);
+  };
 
-  const bool all = !(top_p < 1.0f);
-  int bstar = kBuckets;  // buckets below bstar are wholly inside the nucleus
-  U128 above{0ull, 0ull}, need{0ull, 0ull};
-  if (!all) {
-    for (int b = t; b < kBuckets + 64; b += kSThreads) {
-      sh.u.h.a[b] = 0ull;
-      sh.u.h.b[b] = 0ull;
-    }
-    __syncthreads();
-    // 1. value-bucket mass histogram; the crowded last bucket goes to
-    // per-lane slots folded in afterwards
-    for (int q = wave; q < NC; q += kSWaves) {
-      const int p = q * kChunk + 4 * lane;
-      float x[4];
-      bool v[4];
-      load4<VEC>(row, n, p, x, v);
+  // Exact pass with the window [lo, hi]: segment masses of the buckets below
+  // lo, the window's elements into the list.  Returns the total mass Z.
+  auto collect = [&](int lo, int hi) -> U128 {
+    uint64_t za = 0ull, zb = 0ull;
+    for_chunks<VEC>(row, n, NC, [&](int q, int p, const float (&x)[4], const bool (&v)[4]) {
+      uint32_t ca = 0u, cb = 0u, ma = 0u, mb = 0u;  // four weights of at most 2^28 each
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const Fix w = fix(x[e]);
-        int b = bucket_of(x[e], vmax, kb);
-        if (!v[e] || b == kBuckets - 1) b = kBuckets + lane;
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.a[b]),
-                  (unsigned long long)(v[e] ? w.a : 0u));
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.b[b]),
-                  (unsigned long long)(v[e] ? w.b : 0u));
-      }
-    }
-    __syncthreads();
-    if (wave == 0) {
-      const uint64_t ta = wave_sum_u64(sh.u.h.a[kBuckets + lane]);
-      const uint64_t tb = wave_sum_u64(sh.u.h.b[kBuckets + lane]);
-      if (lane == 0) {
-        sh.u.h.a[kBuckets - 1] += ta;
-        sh.u.h.b[kBuckets - 1] += tb;
-      }
-    }
-    __syncthreads();
-    U128 s[kBPT];
-    U128 ls{0ull, 0ull};
-#pragma unroll
-    for (int i = 0; i < kBPT; ++i) {
-      const int b = kBPT * t + i;
-      s[i] = u128_join(sh.u.h.a[b], sh.u.h.b[b]);
-      ls = u128_add(ls, s[i]);
-    }
-    U128 Z;
-    U128 acc = block_exscan_u128(ls, sh, &Z);
-    need = u128_ceil((double)top_p * u128_to_f64(Z));
-    if (need.lo == 0ull && need.hi == 0ull) need.lo = 1ull;
-#pragma unroll
-    for (int i = 0; i < kBPT; ++i) {
-      const U128 nxt = u128_add(acc, s[i]);
-      if (u128_lt(acc, need) && !u128_lt(nxt, need)) {
-        sh.bstar = kBPT * t + i;
-        sh.above = acc;
-      }
-      acc = nxt;
-    }
-    __syncthreads();
-    if (sh.bstar >= 0) {
-      bstar = sh.bstar;
-      above = sh.above;
-    }
-  }
-
-  // 2. members of the buckets before b* into segment masses; collect b*
-  for (int q = wave; q < NC; q += kSWaves) {
-    const int p = q * kChunk + 4 * lane;
-    float x[4];
-    bool v[4];
-    load4<VEC>(row, n, p, x, v);
-    uint64_t A = 0ull, B = 0ull;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const Fix w = fix(x[e]);
-      const int b = bucket_of(x[e], vmax, kb);
-      const bool mem = v[e] && b < bstar;
-      A += mem ? w.a : 0u;
-      B += mem ? w.b : 0u;
-      const bool cand = v[e] && b == bstar;
-      const uint64_t bal = __ballot(cand);
-      if (bal) {
-        const int leader = __ffsll((unsigned long long)bal) - 1;
-        int base = 0;
-        if (lane == leader) base = atomicAdd(&sh.ncand, __popcll(bal));
-        base = __shfl(base, leader, 64);
-        if (cand) {
-          const int slot = base + __popcll(bal & ((1ull << lane) - 1ull));
-          if (slot < kMaxCand) {
-            sh.u.c.key[slot] = ((uint64_t)(~orderable(x[e])) << 32) | (uint32_t)(p + e);
-            sh.u.c.a[slot] = w.a;
-            sh.u.c.b[slot] = w.b;
-          }
-        }
-      }
-    }
-    A = wave_sum_u64(A);
-    B = wave_sum_u64(B);
-    if (lane == 0 && (A | B)) {
-      const int sg = q * kChunk / G;
-      atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
-      atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
-    }
-  }
-  __syncthreads();
-
-  if (bstar < kBuckets) {
-    const int nc = sh.ncand;
-    if (nc <= kMaxCand) {
-      // sort the cut bucket by (key desc, position asc), scan, cut
-      int P = 1;
-      while (P < nc) P <<= 1;
-      for (int i = nc + t; i < P; i += kSThreads) {
-        sh.u.c.key[i] = ~0ull;
-        sh.u.c.a[i] = 0ull;
-        sh.u.c.b[i] = 0ull;
-      }
-      __syncthreads();
-      for (int k = 2; k <= P; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-          if (t < P / 2) {
-            const int i = 2 * t - (t & (j - 1));
-            const int l = i + j;
-            const uint64_t ki = sh.u.c.key[i], kl = sh.u.c.key[l];
-            if ((ki > kl) == ((i & k) == 0)) {
-              sh.u.c.key[i] = kl;
-              sh.u.c.key[l] = ki;
-              const uint64_t ai = sh.u.c.a[i], bi = sh.u.c.b[i];
-              sh.u.c.a[i] = sh.u.c.a[l];
-              sh.u.c.b[i] = sh.u.c.b[l];
-              sh.u.c.a[l] = ai;
-              sh.u.c.b[l] = bi;
+        const int b = bucket_of(ypos(x[e], vmax, kb));
+        ca += v[e] ? w.a : 0u;
+        cb += v[e] ? w.b : 0u;
+        const bool mem = v[e] && b < lo;
+        ma += mem ? w.a : 0u;
+        mb += mem ? w.b : 0u;
+        const bool cand = v[e] && b >= lo && b <= hi;
+        const uint64_t bal = __ballot(cand);
+        if (bal) {
+          const int leader = __ffsll((unsigned long long)bal) - 1;
+          int base = 0;
+          if (lane == leader) base = atomicAdd(&sh.ncand, __popcll(bal));
+          base = __shfl(base, leader, 64);
+          if (cand) {
+            const int slot = base + __popcll(bal & ((1ull << lane) - 1ull));
+            if (slot < kMaxCand) {
+              sh.u.c.key[slot] = ((uint64_t)(~orderable(x[e])) << 32) | (uint32_t)(p + e);
+              sh.u.c.a[slot] = w.a;
+              sh.u.c.b[slot] = w.b;
             }
           }
-          __syncthreads();
         }
       }
-      const int i0 = 2 * t, i1 = 2 * t + 1;
-      const U128 e0 = i0 < nc ? u128_join(sh.u.c.a[i0], sh.u.c.b[i0]) : U128{0ull, 0ull};
-      const U128 e1 = i1 < nc ? u128_join(sh.u.c.a[i1], sh.u.c.b[i1]) : U128{0ull, 0ull};
-      U128 tot;
-      const U128 ex0 = u128_add(above, block_exscan_u128(u128_add(e0, e1), sh, &tot));
-      const U128 ex1 = u128_add(ex0, e0);
-      if (i0 < nc && u128_lt(ex0, need) && !u128_lt(ex1, need)) sh.cut_idx = i0;
-      if (i1 < nc && u128_lt(ex1, need) && !u128_lt(u128_add(ex1, e1), need)) sh.cut_idx = i1;
-      __syncthreads();
-      const int jc = sh.cut_idx;
-      for (int i = t; i <= jc; i += kSThreads) {
-        const int pos = (int)(uint32_t)sh.u.c.key[i];
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[pos / G]),
-                  (unsigned long long)sh.u.c.a[i]);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[pos / G]),
-                  (unsigned long long)sh.u.c.b[i]);
+      za += ca;
+      zb += cb;
+      const uint64_t A = wave_sum_u64(ma), B = wave_sum_u64(mb);
+      if (lane == 0 && (A | B)) {
+        const int sg = q * kChunk / G;
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
       }
-      if (t == 0 && jc >= 0) {
-        sh.T = ~(uint32_t)(sh.u.c.key[jc] >> 32);
-        sh.cut_pos = (int)(uint32_t)sh.u.c.key[jc];
+    });
+    return block_sum_u128(u128_join(za, zb), sh);  // barriers: segments and list complete
+  };
+
+  const bool all = !(top_p < 1.0f);
+  int lo = kBuckets, hi = kBuckets - 1;  // all: every bucket below lo, no window
+  if (!all) {
+    // 1. approximate histogram (fp32 weights in units of 2^-32) -> window
+    for (int b = t; b < kBuckets + 64; b += kSThreads) sh.u.hf[b] = 0ull;
+    __syncthreads();
+    const float c32 = 1.4426950408889634f / temperature;
+    for_chunks<VEC>(row, n, NC, [&](int, int, const float (&x)[4], const bool (&v)[4]) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float y = ypos(x[e], vmax, kb);
+        const float w = exp2f((x[e] - vmax) * c32);
+        int b = bucket_of(y);
+        if (!v[e] || b == kBuckets - 1) b = kBuckets + lane;
+        atomicAdd(&sh.u.hf[b], v[e] ? (unsigned long long)(uint32_t)(w * 4294967040.0f) : 0ull);
       }
+    });
+    __syncthreads();
+    if (wave == 0) {
+      const uint64_t tail = wave_sum_u64(sh.u.hf[kBuckets + lane]);
+      if (lane == 0) sh.u.hf[kBuckets - 1] += tail;
+    }
+    __syncthreads();
+    double d[kBPT];
+    double dl = 0.0;
+#pragma unroll
+    for (int i = 0; i < kBPT; ++i) {
+      d[i] = (double)sh.u.hf[kBPT * t + i];
+      dl += d[i];
+    }
+    double ztot;
+    double acc = block_exscan_f64(dl, sh, &ztot);
+    const double need_a = (double)top_p * ztot;
+    // error of the estimate: fp32 exponent and exp2 rounding, truncation
+    const double slack = 1e-5 * ztot + 2.0 * (double)n;
+#pragma unroll
+    for (int i = 0; i < kBPT; ++i) {
+      if (acc < need_a && acc + d[i] >= need_a) {
+        const int b = kBPT * t + i;
+        sh.lo = (acc >= need_a - slack && b > 0) ? b - 1 : b;
+        sh.hi = (acc + d[i] <= need_a + slack && b < kBuckets - 1) ? b + 1 : b;
+        sh.bsel = b;
+      }
+      acc += d[i];
+    }
+    __syncthreads();
+    if (sh.bsel >= 0) {
+      lo = sh.lo;
+      hi = sh.hi;
     } else {
-      // exact radix select on the keys of bucket b*
-      uint32_t Tk = 0u, kmask = 0u, nt = 0u;
-      U128 ab = above;
-      constexpr int kShift[3] = {21, 10, 0};
-      constexpr int kBits[3] = {11, 11, 10};
-      for (int pass = 0; pass < 3; ++pass) {
-        const int shift = kShift[pass], nb = 1 << kBits[pass];
-        __syncthreads();  // earlier readers of the histogram are done
-        for (int b = t; b < nb; b += kSThreads) {
-          sh.u.h.a[b] = 0ull;
-          sh.u.h.b[b] = 0ull;
-          sh.u.h.cnt[b] = 0u;
+      lo = kBuckets - 2;
+      hi = kBuckets - 1;
+    }
+    __syncthreads();
+  }
+
+  // 2. exact pass: Z, segment masses below the window, the window's list
+  const U128 Z = collect(lo, hi);
+  if (!all) {
+    U128 need = u128_ceil((double)top_p * u128_to_f64(Z));
+    if (need.lo == 0ull && need.hi == 0ull) need.lo = 1ull;
+    U128 above = block_sum_u128(u128_join(sh.seg_a[t], sh.seg_b[t]), sh);
+    int nc = sh.ncand;
+    U128 wmass{0ull, 0ull};
+    if (nc <= kMaxCand) {
+      U128 cl{0ull, 0ull};
+      for (int i = t; i < nc; i += kSThreads) cl = u128_add(cl, u128_join(sh.u.c.a[i], sh.u.c.b[i]));
+      wmass = block_sum_u128(cl, sh);
+    }
+    if (nc > kMaxCand || !u128_lt(above, need) || u128_lt(u128_add(above, wmass), need)) {
+      // the window missed the cut or overflowed the list: exact histogram
+      // over groups of 4 buckets, then the exact pass over that group
+      __syncthreads();
+      for (int b = t; b < kCoarse + 64; b += kSThreads) {
+        sh.u.h.a[b] = 0ull;
+        sh.u.h.b[b] = 0ull;
+      }
+      if (t == 0) {
+        sh.bsel = -1;
+        sh.ncand = 0;
+      }
+      sh.seg_a[t] = 0ull;
+      sh.seg_b[t] = 0ull;
+      __syncthreads();
+      for_chunks<VEC>(row, n, NC, [&](int, int, const float (&x)[4], const bool (&v)[4]) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const Fix w = fix(x[e]);
+          int b = bucket_of(ypos(x[e], vmax, kb)) >> 2;
+          if (!v[e] || b == kCoarse - 1) b = kCoarse + lane;
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.a[b]),
+                    (unsigned long long)(v[e] ? w.a : 0u));
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.b[b]),
+                    (unsigned long long)(v[e] ? w.b : 0u));
+        }
+      });
+      __syncthreads();
+      if (wave == 0) {
+        const uint64_t ta = wave_sum_u64(sh.u.h.a[kCoarse + lane]);
+        const uint64_t tb = wave_sum_u64(sh.u.h.b[kCoarse + lane]);
+        if (lane == 0) {
+          sh.u.h.a[kCoarse - 1] += ta;
+          sh.u.h.b[kCoarse - 1] += tb;
+        }
+      }
+      __syncthreads();
+      const U128 s0 = u128_join(sh.u.h.a[2 * t], sh.u.h.b[2 * t]);
+      const U128 s1 = u128_join(sh.u.h.a[2 * t + 1], sh.u.h.b[2 * t + 1]);
+      U128 tot;
+      const U128 x0 = block_exscan_u128(u128_add(s0, s1), sh, &tot);
+      const U128 x1 = u128_add(x0, s0);
+      if (u128_lt(x0, need) && !u128_lt(x1, need)) sh.bsel = 2 * t;
+      if (u128_lt(x1, need) && !u128_lt(u128_add(x1, s1), need)) sh.bsel = 2 * t + 1;
+      __syncthreads();
+      const int cg = max(sh.bsel, 0);
+      lo = 4 * cg;
+      hi = 4 * cg + 3;
+      __syncthreads();
+      collect(lo, hi);
+      above = block_sum_u128(u128_join(sh.seg_a[t], sh.seg_b[t]), sh);
+      nc = sh.ncand;
+    }
+
+    if (nc <= kMaxCand) {
+      // exact histogram of the list over sub-buckets of the window
+      const int nsub = kSub * (hi - lo + 1);
+      sh.u.c.sa[t] = 0ull;
+      sh.u.c.sb[t] = 0ull;
+      sh.u.c.scnt[t] = 0u;
+      if (t == 0) sh.bsel = -1;
+      __syncthreads();
+      auto sub_of = [&](uint64_t key) {
+        const float x = from_orderable(~(uint32_t)(key >> 32));
+        return min(max(subbucket_of(ypos(x, vmax, kb)) - kSub * lo, 0), nsub - 1);
+      };
+      for (int i = t; i < nc; i += kSThreads) {
+        const int s = sub_of(sh.u.c.key[i]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.c.sa[s]),
+                  (unsigned long long)sh.u.c.a[i]);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.c.sb[s]),
+                  (unsigned long long)sh.u.c.b[i]);
+        atomicAdd(&sh.u.c.scnt[s], 1u);
+      }
+      __syncthreads();
+      const U128 st = u128_join(sh.u.c.sa[t], sh.u.c.sb[t]);
+      U128 tot;
+      const U128 sx = u128_add(above, block_exscan_u128(st, sh, &tot));
+      if (t < nsub && u128_lt(sx, need) && !u128_lt(u128_add(sx, st), need)) {
+        sh.bsel = t;
+        sh.above = sx;
+      }
+      __syncthreads();
+      const int ss = max(sh.bsel, 0);
+      const U128 as = sh.above;
+      const uint32_t cs = sh.u.c.scnt[ss];
+      if (cs <= 64u) {
+        if (wave == 0) {
+          // gather sub-bucket ss, then rank it by (key desc, position asc)
+          int got = 0;
+          for (int base = 0; base < nc; base += 64) {
+            const int i = base + lane;
+            const bool in = i < nc && sub_of(sh.u.c.key[i]) == ss;
+            const uint64_t bal = __ballot(in);
+            if (in) {
+              const int slot = got + __popcll(bal & ((1ull << lane) - 1ull));
+              sh.wkey[slot] = sh.u.c.key[i];
+              sh.wa[slot] = sh.u.c.a[i];
+              sh.wb[slot] = sh.u.c.b[i];
+            }
+            got += __popcll(bal);
+          }
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          if (lane < got) {
+            const uint64_t kj = sh.wkey[lane];
+            uint64_t A = 0ull, B = 0ull;
+            for (int i = 0; i < got; ++i) {
+              const bool before = sh.wkey[i] < kj;
+              A += before ? sh.wa[i] : 0ull;
+              B += before ? sh.wb[i] : 0ull;
+            }
+            const U128 ex = u128_add(as, u128_join(A, B));
+            const U128 in = u128_add(ex, u128_join(sh.wa[lane], sh.wb[lane]));
+            if (u128_lt(ex, need) && !u128_lt(in, need)) {
+              sh.T = ~(uint32_t)(kj >> 32);
+              sh.cut_pos = (int)(uint32_t)kj;
+            }
+          }
         }
         __syncthreads();
-        for (int q = wave; q < NC; q += kSWaves) {
-          const int p = q * kChunk + 4 * lane;
-          float x[4];
-          bool v[4];
-          load4<VEC>(row, n, p, x, v);
+        // members of the window: sub-buckets before ss, and ss up to the cut
+        const uint64_t kc = ((uint64_t)(~sh.T) << 32) | (uint32_t)sh.cut_pos;
+        for (int i = t; i < nc; i += kSThreads) {
+          const uint64_t key = sh.u.c.key[i];
+          const int s = sub_of(key);
+          if (s < ss || (s == ss && key <= kc)) {
+            const int pos = (int)(uint32_t)key;
+            atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[pos / G]),
+                      (unsigned long long)sh.u.c.a[i]);
+            atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[pos / G]),
+                      (unsigned long long)sh.u.c.b[i]);
+          }
+        }
+      } else {
+        // a crowded sub-bucket: bitonic sort of the list, scan, cut
+        int P = 1;
+        while (P < nc) P <<= 1;
+        for (int i = nc + t; i < P; i += kSThreads) {
+          sh.u.c.key[i] = ~0ull;
+          sh.u.c.a[i] = 0ull;
+          sh.u.c.b[i] = 0ull;
+        }
+        __syncthreads();
+        for (int k = 2; k <= P; k <<= 1) {
+          for (int j = k >> 1; j > 0; j >>= 1) {
+            if (t < P / 2) {
+              const int i = 2 * t - (t & (j - 1));
+              const int l = i + j;
+              const uint64_t ki = sh.u.c.key[i], kl = sh.u.c.key[l];
+              if ((ki > kl) == ((i & k) == 0)) {
+                sh.u.c.key[i] = kl;
+                sh.u.c.key[l] = ki;
+                const uint64_t ai = sh.u.c.a[i], bi = sh.u.c.b[i];
+                sh.u.c.a[i] = sh.u.c.a[l];
+                sh.u.c.b[i] = sh.u.c.b[l];
+                sh.u.c.a[l] = ai;
+                sh.u.c.b[l] = bi;
+              }
+            }
+            __syncthreads();
+          }
+        }
+        const int i0 = 2 * t, i1 = 2 * t + 1;
+        const U128 e0 = i0 < nc ? u128_join(sh.u.c.a[i0], sh.u.c.b[i0]) : U128{0ull, 0ull};
+        const U128 e1 = i1 < nc ? u128_join(sh.u.c.a[i1], sh.u.c.b[i1]) : U128{0ull, 0ull};
+        U128 tot2;
+        const U128 ex0 = u128_add(above, block_exscan_u128(u128_add(e0, e1), sh, &tot2));
+        const U128 ex1 = u128_add(ex0, e0);
+        if (i0 < nc && u128_lt(ex0, need) && !u128_lt(ex1, need)) sh.cut_idx = i0;
+        if (i1 < nc && u128_lt(ex1, need) && !u128_lt(u128_add(ex1, e1), need)) sh.cut_idx = i1;
+        __syncthreads();
+        const int jc = sh.cut_idx;
+        for (int i = t; i <= jc; i += kSThreads) {
+          const int pos = (int)(uint32_t)sh.u.c.key[i];
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[pos / G]),
+                    (unsigned long long)sh.u.c.a[i]);
+          atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[pos / G]),
+                    (unsigned long long)sh.u.c.b[i]);
+        }
+        if (t == 0 && jc >= 0) {
+          sh.T = ~(uint32_t)(sh.u.c.key[jc] >> 32);
+          sh.cut_pos = (int)(uint32_t)sh.u.c.key[jc];
+        }
+      }
+    } else {
+      // exact radix select, 8 bits per pass, on the keys of the window
+      auto in_window = [&](float x) {
+        const int b = bucket_of(ypos(x, vmax, kb));
+        return b >= lo && b <= hi;
+      };
+      uint32_t Tk = 0u, kmask = 0u, nt = 0u;
+      U128 ab = above;
+      for (int shift = 24; shift >= 0; shift -= 8) {
+        __syncthreads();  // earlier readers of the histogram are done
+        if (t < 256) {
+          sh.u.h.a[t] = 0ull;
+          sh.u.h.b[t] = 0ull;
+          sh.u.h.cnt[t] = 0u;
+        }
+        if (t == 0) sh.bsel = -1;
+        __syncthreads();
+        for_chunks<VEC>(row, n, NC, [&](int, int, const float (&x)[4], const bool (&v)[4]) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const uint32_t key = orderable(x[e]);
-            if (v[e] && bucket_of(x[e], vmax, kb) == bstar && (key & kmask) == Tk) {
-              const int b = (int)((key >> shift) & (uint32_t)(nb - 1));
+            if (v[e] && in_window(x[e]) && (key & kmask) == Tk) {
+              const int b = (int)((key >> shift) & 255u);
               const Fix w = fix(x[e]);
               atomicAdd(reinterpret_cast<unsigned long long*>(&sh.u.h.a[b]),
                         (unsigned long long)w.a);
@@ -564,34 +774,23 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
               atomicAdd(&sh.u.h.cnt[b], 1u);
             }
           }
-        }
+        });
         __syncthreads();
-        // thread t owns key buckets nb-1-(kBPT t + i): descending keys
-        U128 ks[kBPT];
-        U128 kls{0ull, 0ull};
-#pragma unroll
-        for (int i = 0; i < kBPT; ++i) {
-          const int b = nb - 1 - (kBPT * t + i);
-          ks[i] = b >= 0 ? u128_join(sh.u.h.a[b], sh.u.h.b[b]) : U128{0ull, 0ull};
-          kls = u128_add(kls, ks[i]);
-        }
+        // thread t < 256 owns key bucket 255 - t: descending keys
+        const U128 ks =
+            t < 256 ? u128_join(sh.u.h.a[255 - t], sh.u.h.b[255 - t]) : U128{0ull, 0ull};
         U128 ktot;
-        U128 kacc = u128_add(ab, block_exscan_u128(kls, sh, &ktot));
-#pragma unroll
-        for (int i = 0; i < kBPT; ++i) {
-          const U128 nxt = u128_add(kacc, ks[i]);
-          if (u128_lt(kacc, need) && !u128_lt(nxt, need)) {
-            sh.sel = nb - 1 - (kBPT * t + i);
-            sh.above = kacc;
-          }
-          kacc = nxt;
+        const U128 kacc = u128_add(ab, block_exscan_u128(ks, sh, &ktot));
+        if (t < 256 && u128_lt(kacc, need) && !u128_lt(u128_add(kacc, ks), need)) {
+          sh.bsel = 255 - t;
+          sh.above = kacc;
         }
         __syncthreads();
-        const int sel = min(max(sh.sel, 0), nb - 1);
-        ab = sh.above;
+        const int sel = max(sh.bsel, 0);
+        ab = sh.bsel >= 0 ? sh.above : ab;
         nt = sh.u.h.cnt[sel];
         Tk |= (uint32_t)sel << shift;
-        kmask |= (uint32_t)(nb - 1) << shift;
+        kmask |= 255u << shift;
       }
       // the c-th element tied at Tk in id order completes the nucleus:
       // smallest c >= 1 with ab + c * E(Tk) >= need
@@ -602,35 +801,20 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
       while (c > 1u && !u128_lt(u128_add(ab, u128_mul32(WT, c - 1u)), need)) --c;
       while (c < nt && u128_lt(u128_add(ab, u128_mul32(WT, c)), need)) ++c;
       // ties per segment, then the segment and the lane holding the c-th
-      for (int q = wave; q < NC; q += kSWaves) {
-        const int p = q * kChunk + 4 * lane;
-        float x[4];
-        bool v[4];
-        load4<VEC>(row, n, p, x, v);
+      for_chunks<VEC>(row, n, NC, [&](int q, int, const float (&x)[4], const bool (&v)[4]) {
         uint32_t ties = 0u;
 #pragma unroll
         for (int e = 0; e < 4; ++e) ties += (v[e] && orderable(x[e]) == Tk) ? 1u : 0u;
         ties = (uint32_t)wave_sum_u64(ties);
         if (lane == 0 && ties) atomicAdd(&sh.seg_t[q * kChunk / G], ties);
-      }
+      });
       __syncthreads();
-      uint32_t tc[kSPT];
-      uint32_t tl = 0u;
-#pragma unroll
-      for (int i = 0; i < kSPT; ++i) {
-        const int sg = kSPT * t + i;
-        tc[i] = sg < NS ? sh.seg_t[sg] : 0u;
-        tl += tc[i];
-      }
+      const uint32_t tc = t < NS ? sh.seg_t[t] : 0u;
       uint32_t ttot;
-      uint32_t tb = block_exscan_u32(tl, sh, &ttot);
-#pragma unroll
-      for (int i = 0; i < kSPT; ++i) {
-        if (tb < c && c <= tb + tc[i]) {
-          sh.tie_seg = kSPT * t + i;
-          sh.tie_base = tb;
-        }
-        tb += tc[i];
+      const uint32_t tb = block_exscan_u32(tc, sh, &ttot);
+      if (tb < c && c <= tb + tc) {
+        sh.tie_seg = t;
+        sh.tie_base = tb;
       }
       __syncthreads();
       if (wave == 0 && sh.tie_seg >= 0) {
@@ -653,13 +837,11 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
           uint32_t seen = run + inc - lt;
           int hit = -1;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
+          for (int e = 0; e < 4; ++e)
             if (tie[e] && ++seen == c && hit < 0) hit = p + e;
-          }
           const uint64_t bal = __ballot(hit >= 0);
           if (bal) {
-            const int src = __ffsll((unsigned long long)bal) - 1;
-            const int pos = __shfl(hit, src, 64);
+            const int pos = __shfl(hit, __ffsll((unsigned long long)bal) - 1, 64);
             if (lane == 0) {
               sh.T = Tk;
               sh.cut_pos = pos;
@@ -670,19 +852,14 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
         }
       }
       __syncthreads();
-      // members of bucket b*
-      const uint32_t T = sh.T;
-      const int cut = sh.cut_pos;
-      for (int q = wave; q < NC; q += kSWaves) {
-        const int p = q * kChunk + 4 * lane;
-        float x[4];
-        bool v[4];
-        load4<VEC>(row, n, p, x, v);
+      // members of the window
+      const uint32_t Tw = sh.T;
+      const int cw = sh.cut_pos;
+      for_chunks<VEC>(row, n, NC, [&](int q, int p, const float (&x)[4], const bool (&v)[4]) {
         uint64_t A = 0ull, B = 0ull;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const uint32_t key = orderable(x[e]);
-          if (v[e] && bucket_of(x[e], vmax, kb) == bstar && (key > T || (key == T && p + e <= cut))) {
+          if (v[e] && in_window(x[e]) && member(x[e], p + e, Tw, cw)) {
             const Fix w = fix(x[e]);
             A += w.a;
             B += w.b;
@@ -695,7 +872,7 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
           atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
           atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
         }
-      }
+      });
     }
     __syncthreads();
   }
@@ -704,27 +881,15 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
   const int cut = sh.cut_pos;
 
   // 3. segment masses in id order, then the inverse CDF inside one segment
-  U128 sm[kSPT];
-  U128 sl{0ull, 0ull};
-#pragma unroll
-  for (int i = 0; i < kSPT; ++i) {
-    const int sg = kSPT * t + i;
-    sm[i] = sg < NS ? u128_join(sh.seg_a[sg], sh.seg_b[sg]) : U128{0ull, 0ull};
-    sl = u128_add(sl, sm[i]);
-  }
+  const U128 sm = t < NS ? u128_join(sh.seg_a[t], sh.seg_b[t]) : U128{0ull, 0ull};
   U128 mass;
-  U128 sb = block_exscan_u128(sl, sh, &mass);
+  const U128 sb = block_exscan_u128(sm, sh, &mass);
   const uint32_t s_idx = (uint32_t)(m / R), r_idx = (uint32_t)(m % R);
   const uint32_t u24 = philox_x0(r_idx, s_idx, 0u, 0u, seed_lo, seed_hi) >> 8;
   const U128 target = u128_mul32(mass, u24);
-#pragma unroll
-  for (int i = 0; i < kSPT; ++i) {
-    const U128 nxt = u128_add(sb, sm[i]);
-    if (!u128_lt(target, u128_shl24(sb)) && u128_lt(target, u128_shl24(nxt))) {
-      sh.claim_seg = kSPT * t + i;
-      sh.claim_base = sb;
-    }
-    sb = nxt;
+  if (!u128_lt(target, u128_shl24(sb)) && u128_lt(target, u128_shl24(u128_add(sb, sm)))) {
+    sh.claim_seg = t;
+    sh.claim_base = sb;
   }
   __syncthreads();
   if (wave == 0) {
@@ -742,8 +907,7 @@ __global__ __launch_bounds__(kSThreads) void k_sample(const float* __restrict__ 
         U128 l{0ull, 0ull};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const uint32_t key = orderable(x[e]);
-          if (v[e] && (key > T || (key == T && p + e <= cut))) {
+          if (v[e] && member(x[e], p + e, T, cut)) {
             const Fix w = fix(x[e]);
             l = u128_add(l, u128_join(w.a, w.b));
           }
