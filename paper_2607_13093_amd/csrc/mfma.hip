@@ -441,6 +441,138 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #endif
 }
 
+// Direct-to-LDS variant for fp8 E4M3 weights (K a multiple of 64).  The A
+// tile is staged as above; the B tile keeps its bytes: a weight row holds 64
+// codes per K step (64 bytes, four 16-byte chunks), and a wave instruction
+// fills 16 rows.  Chunks are XOR-swizzled with g(row) = (row >> 2) & 3, so
+// the 32 rows a fragment read touches spread over the LDS banks.  Each lane
+// reads its 8 codes of a fragment (ds_read_b64) and widens them to bf16
+// (exact) in registers right before the MFMA; the per-row scale is applied
+// in the epilogue.  All fragments of a step are read before the next step's
+// loads are issued (the compiler would otherwise make the reads wait for
+// those loads), and scheduling barriers keep the loads ahead of the MFMAs.
+__device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
+
+template <int BM, int BN, int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_mfma_dma8(const MfmaArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int TM = BM / 2, TN = BN / 2;
+  constexpr int FM = TM / 32, FN = TN / 32;
+  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 16 / 4;  // DMA instructions per wave per step
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);             // [2][BM][64] bf16
+  uint8_t* Bs = reinterpret_cast<uint8_t*>(As + 2 * BM * kBK);   // [2][BN][64] fp8
+  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + 2 * BN * kBK);
+  uint32_t* s_rmax = reinterpret_cast<uint32_t*>(s_ids + BN);
+  unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_rmax + BM + (BM & 1));
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  int mt, nt;
+  tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int M = a.M, K = a.K, n = a.n;
+  const int last_id = a.ids[min(n, n0 + BN) - 1];
+  for (int i = tid; i < BN; i += 256) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  for (int i = tid; i < BM; i += 256) {
+    s_rmax[i] = 0u;
+    s_rkey[i] = 0ull;
+  }
+  __syncthreads();
+
+  const uint8_t* pa[A_INS];
+  const uint8_t* pb[B_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    const int r = (wave * A_INS + i) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ swz8(r);
+    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int r = (wave * B_INS + i) * 16 + (lane >> 2);
+    const int lc = (lane & 3) ^ swz4(r);
+    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+  }
+  auto issue = [&](int k0, int stage) {
+    uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
+    uint8_t* bs = Bs + stage * BN * kBK;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
+                                       (lds_void_t*)(as + (wave * A_INS + i) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pb[i] + k0, (lds_void_t*)(bs + (wave * B_INS + i) * 1024),
+                                       16, 0, 0);
+  };
+
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  if (K > 0) {
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  int stage = 0;
+  for (int k0 = 0; k0 < K; k0 += kBK) {
+    const uint16_t* as = As + stage * BM * kBK;
+    const uint8_t* bs = Bs + stage * BN * kBK;
+    bf16x8_t af[kBK / 16][FM];
+    uint2 bq[kBK / 16][FN];
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int c = kk * 2 + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * TM + i * 32 + (lane & 31);
+        af[kk][i] = *reinterpret_cast<const bf16x8_t*>(as + row * kBK + ((c ^ swz8(row)) << 3));
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int row = wn * TN + j * 32 + (lane & 31);
+        bq[kk][j] = *reinterpret_cast<const uint2*>(bs + row * kBK + ((kk ^ swz4(row)) << 4) +
+                                                    8 * (lane >> 5));
+      }
+    }
+    // the other stage was last read in the previous step, finished by all
+    // waves before that step's closing barrier
+    if (k0 + kBK < K) issue(k0 + kBK, stage ^ 1);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      bf16x8_t bfr[FN];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        u32x4_t w;
+        w.x = e4m3x2_to_bf16x2_m<false>(bq[kk][j].x);
+        w.y = e4m3x2_to_bf16x2_m<true>(bq[kk][j].x);
+        w.z = e4m3x2_to_bf16x2_m<false>(bq[kk][j].y);
+        w.w = e4m3x2_to_bf16x2_m<true>(bq[kk][j].y);
+        bfr[j] = __builtin_bit_cast(bf16x8_t, w);
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk][i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's loads for the next stage have landed
+    __syncthreads();
+    stage ^= 1;
+  }
+  tile_epilogue<BM, BN, 1, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+                                reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
+#endif
+}
+
 template <int BM, int BN>
 constexpr size_t mfma_lds_bytes() {
   return (size_t)2 * (BM + BN) * kLDK * 2 + (size_t)BN * 4 + (size_t)(BM + 1) * 4 + 8 +
@@ -453,6 +585,12 @@ constexpr size_t mfma_dma_lds_bytes() {
          (size_t)BM * 8;
 }
 
+template <int BM, int BN>
+constexpr size_t mfma_dma8_lds_bytes() {
+  return (size_t)2 * (BM * 2 + BN) * kBK + (size_t)BN * 4 + (size_t)(BM + 1) * 4 + 8 +
+         (size_t)BM * 8;
+}
+
 template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   a.m_tiles = (a.M + BM - 1) / BM;
@@ -462,6 +600,17 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
     if (a.K % kBK == 0) {
       auto kd = k_mfma_dma<BM, BN, EPI>;
       constexpr size_t lds_d = mfma_dma_lds_bytes<BM, BN>();
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
+      return hipGetLastError();
+    }
+  }
+  if constexpr (WT == 1) {
+    if (a.K % kBK == 0) {
+      auto kd = k_mfma_dma8<BM, BN, EPI>;
+      constexpr size_t lds_d = mfma_dma8_lds_bytes<BM, BN>();
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
       if (e != hipSuccess) return e;

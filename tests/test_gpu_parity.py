@@ -191,6 +191,14 @@ def test_fp8_cloud_partial_dense():
     run_greedy_case(make_workload(cfg), tag="fp8 dense")
 
 
+def test_fp8_cloud_partial_dense_k_not_multiple_of_64():
+    # d_cloud = 1040: the fp8 codes are widened on their way into LDS instead
+    # of being copied there directly
+    cfg = Config("fp8_dense_k", 28, d=1072, d_end=32, vocab=5000, n_sub=2999, subset_kind="choice",
+                 sessions=13, rows_per_session=3, wtype="fp8")
+    run_greedy_case(make_workload(cfg), tag="fp8 dense, K % 64 = 16")
+
+
 # ---------------------------------------------------------------------------
 # edge cases of the interface
 # ---------------------------------------------------------------------------
