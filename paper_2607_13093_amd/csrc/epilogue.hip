@@ -62,7 +62,7 @@ hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int
   // float4 / char4 accesses need whole, aligned groups of four columns
   const int vec = (n % 4 == 0) && (reinterpret_cast<uintptr_t>(z) % 16 == 0) &&
                   (reinterpret_cast<uintptr_t>(q) % 4 == 0);
-  hipLaunchKernelGGL(k_quantize, dim3(M, chunks), dim3(256), 0, s, z, amax_part, nblk, n, vec,
+  launch_kernel(k_quantize, dim3(M, chunks), dim3(256), 0, s, z, amax_part, nblk, n, vec,
                      clip, q, scale);
   return hipGetLastError();
 }
@@ -128,7 +128,7 @@ hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_
                                int32_t* accept, hipStream_t s) {
   if (R > kMaxRowsPerSession || n < 1 || nblk > kMaxBlocks) return hipErrorInvalidValue;
   const int waves = R < kFinalWaves ? R : kFinalWaves;
-  hipLaunchKernelGGL(k_final_greedy, dim3(n_sessions), dim3(64 * waves), 0, s,
+  launch_kernel(k_final_greedy, dim3(n_sessions), dim3(64 * waves), 0, s,
                      reinterpret_cast<const unsigned long long*>(best_part), nblk, ids, n, R,
                      drafts, tokens, accept);
   return hipGetLastError();

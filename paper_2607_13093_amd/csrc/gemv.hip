@@ -351,7 +351,7 @@ static hipError_t launch_one(GemvArgs a, hipStream_t s) {
   a.rows_per_block = ipb * rpi;
   grid = (a.n + a.rows_per_block - 1) / a.rows_per_block;
   const size_t lds = hbytes + (size_t)a.rows_per_block * 4;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(kBS), lds, s, a);
+  launch_kernel(kern, dim3(grid), dim3(kBS), lds, s, a);
   return hipGetLastError();
 }
 

@@ -59,7 +59,7 @@ __device__ __forceinline__ unsigned long long shfl_xor_u64_m(unsigned long long 
 
 constexpr int kBK = 64;          // K elements per staged step
 constexpr int kLDK = kBK + 8;    // padded LDS row, bf16 elements (144 bytes)
-constexpr int kGM = 4;           // m-tiles grouped per n-tile in the tile order
+constexpr int kGM = 8;           // m-tiles grouped per n-tile in the tile order
 
 __device__ __forceinline__ void tile_of_block(int b, int m_tiles, int n_tiles, int& mt, int& nt) {
   const int total = m_tiles * n_tiles;
@@ -603,7 +603,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
+      launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
       return hipGetLastError();
     }
   }
@@ -614,7 +614,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
+      launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
       return hipGetLastError();
     }
   }
@@ -623,7 +623,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
+  launch_kernel(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 

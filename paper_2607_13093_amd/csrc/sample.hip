@@ -950,17 +950,17 @@ hipError_t launch_sample(const float* f, int M, int n, const unsigned long long*
   const uint32_t lo = (uint32_t)seed, hi = (uint32_t)(seed >> 32);
   const bool vec = n % 4 == 0 && (reinterpret_cast<uintptr_t>(f) & 15u) == 0;
   if (vec)
-    hipLaunchKernelGGL(k_sample<true>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
+    launch_kernel(k_sample<true>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
                        temperature, top_p, lo, hi, tokens);
   else
-    hipLaunchKernelGGL(k_sample<false>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
+    launch_kernel(k_sample<false>, dim3(M), dim3(kSThreads), 0, s, f, n, best, nblk, ids, R,
                        temperature, top_p, lo, hi, tokens);
   return hipGetLastError();
 }
 
 hipError_t launch_accept(const int32_t* tokens, const int32_t* drafts, int n_sessions, int R,
                          int32_t* accept, hipStream_t s) {
-  hipLaunchKernelGGL(k_accept, dim3((n_sessions + 255) / 256), dim3(256), 0, s, tokens, drafts,
+  launch_kernel(k_accept, dim3((n_sessions + 255) / 256), dim3(256), 0, s, tokens, drafts,
                      n_sessions, R, accept);
   return hipGetLastError();
 }

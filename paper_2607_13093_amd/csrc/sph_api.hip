@@ -48,10 +48,19 @@ int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 constexpr int64_t kMaxIds = 0x7FFFFFFF;
 
-// ---- kernel tracing: event pairs around launches -------------------------
+}  // namespace
+
+namespace sph {
+thread_local TraceEvents* t_trace_events = nullptr;
+}  // namespace sph
+
+namespace {
+
+// ---- kernel tracing: events attached to the dispatches of a region --------
 struct TraceSlot {
   const char* name;
   hipEvent_t start, stop;
+  bool used;
 };
 std::mutex g_trace_mu;
 std::vector<TraceSlot> g_trace;
@@ -68,29 +77,30 @@ void trace_free_locked() {
   g_tracing = false;
 }
 
-// Records the start event of a launch; returns the slot or -1.
-long trace_begin(const char* name, hipStream_t s) {
-  if (!g_tracing) return -1;
-  std::lock_guard<std::mutex> lk(g_trace_mu);
-  if (!g_tracing || g_trace_used >= g_trace.size()) return -1;
-  TraceSlot& t = g_trace[g_trace_used];
-  t.name = name;
-  if (hipEventRecord(t.start, s) != hipSuccess) return -1;
-  return (long)g_trace_used++;
-}
-
-void trace_end(long slot, hipStream_t s) {
-  if (slot < 0) return;
-  std::lock_guard<std::mutex> lk(g_trace_mu);
-  if ((size_t)slot < g_trace.size()) (void)hipEventRecord(g_trace[(size_t)slot].stop, s);
-}
-
-// Launch `body` (returning hipError_t) between two trace events.
+// Launch `body` (returning hipError_t); while tracing, its kernels record the
+// slot's events on their dispatches (see launch_kernel).
 template <class F>
 hipError_t traced(const char* name, hipStream_t s, F&& body) {
-  const long slot = trace_begin(name, s);
+  (void)s;
+  long slot = -1;
+  sph::TraceEvents ev{nullptr, nullptr, false};
+  if (g_tracing) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if (g_tracing && g_trace_used < g_trace.size()) {
+      slot = (long)g_trace_used++;
+      g_trace[(size_t)slot].name = name;
+      g_trace[(size_t)slot].used = false;
+      ev.start = g_trace[(size_t)slot].start;
+      ev.stop = g_trace[(size_t)slot].stop;
+    }
+  }
+  if (slot >= 0) sph::t_trace_events = &ev;
   const hipError_t e = body();
-  trace_end(slot, s);
+  sph::t_trace_events = nullptr;
+  if (slot >= 0) {
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if ((size_t)slot < g_trace.size()) g_trace[(size_t)slot].used = ev.launched;
+  }
   return e;
 }
 
@@ -424,7 +434,7 @@ int sph_trace_start(int capacity) {
   trace_free_locked();
   g_trace.reserve((size_t)capacity);
   for (int i = 0; i < capacity; ++i) {
-    TraceSlot t{nullptr, nullptr, nullptr};
+    TraceSlot t{nullptr, nullptr, nullptr, false};
     hipError_t e = hipEventCreate(&t.start);
     if (e == hipSuccess) {
       e = hipEventCreate(&t.stop);
@@ -445,7 +455,9 @@ int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out) {
   g_tracing = false;
   const size_t used = g_trace_used;
   int rc = SPH_OK;
+  int k = 0;  // regions that launched a kernel
   for (size_t i = 0; i < used; ++i) {
+    if (!g_trace[i].used) continue;
     hipError_t e = hipEventSynchronize(g_trace[i].stop);
     float ms = 0.0f;
     if (e == hipSuccess) e = hipEventElapsedTime(&ms, g_trace[i].start, g_trace[i].stop);
@@ -453,13 +465,14 @@ int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out) {
       rc = hip_fail(e, "sph_trace_stop: reading events");
       break;
     }
-    if (out && (int)i < max_records) {
-      std::memset(out[i].kernel, 0, SPH_TRACE_NAME_LEN);
-      std::strncpy(out[i].kernel, g_trace[i].name, SPH_TRACE_NAME_LEN - 1);
-      out[i].ms = ms;
+    if (out && k < max_records) {
+      std::memset(out[k].kernel, 0, SPH_TRACE_NAME_LEN);
+      std::strncpy(out[k].kernel, g_trace[i].name, SPH_TRACE_NAME_LEN - 1);
+      out[k].ms = ms;
     }
+    ++k;
   }
-  if (n_out) *n_out = (int)used;
+  if (n_out) *n_out = k;
   trace_free_locked();
   return rc == SPH_OK ? ok() : rc;
 }

@@ -1,11 +1,35 @@
 // Internal declarations shared by the host layer and the kernel files.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
 namespace sph {
+
+// While a trace region is open on this thread (sph_trace_start), launches
+// carry the region's events on the dispatch itself: the start event on the
+// first kernel, the stop event on every kernel (the last one wins), so the
+// recorded interval is kernel execution only.
+struct TraceEvents {
+  hipEvent_t start, stop;
+  bool launched;
+};
+extern thread_local TraceEvents* t_trace_events;
+
+template <class K, class... Args>
+inline void launch_kernel(K kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t s,
+                          Args... args) {
+  TraceEvents* te = t_trace_events;
+  if (te) {
+    hipExtLaunchKernelGGL(kernel, grid, block, lds, s, te->launched ? nullptr : te->start,
+                          te->stop, 0u, args...);
+    te->launched = true;
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+  }
+}
 
 // Per-block / per-tile partial results are stored [M][kMaxBlocks]; no
 // projection launch produces more column partials than this.
