@@ -119,6 +119,7 @@ RAGGED = [
     # dense (MFMA) path: more than 8 rows
     (3, 3, 520, 40, 3000, 1001),    # 9 rows, ragged m- and n-tiles
     (8, 5, 1032, 0, 4000, 2500),    # 40 rows, d_end = 0
+    (17, 17, 1096, 72, 9000, 4097), # 289 rows: three 128-row m-tiles, ragged n
     (13, 10, 2056, 8, 9000, 8193),  # 130 rows: two m-tiles, last n-tile of one column
 ]
 
