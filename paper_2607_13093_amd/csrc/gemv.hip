@@ -38,6 +38,13 @@ namespace sph {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+// Global-memory views of weight rows (loads through them are global, not flat).
+typedef __attribute__((address_space(1))) const uint8_t gbyte;
+typedef __attribute__((address_space(1))) const u32x4_t gu32x4;
+// Fourth word of a raw buffer descriptor (32-bit data format) and the
+// non-temporal cache policy of a buffer load.
+constexpr int kBufferWord3 = 0x00020000;
+constexpr int kNonTemporal = 2;
 
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
@@ -61,11 +68,18 @@ __device__ __forceinline__ unsigned long long argmax_key(float v, int pos) {
 constexpr int pow2ceil(int x) { return x <= 1 ? 1 : 2 * pow2ceil((x + 1) / 2); }
 constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
 
+// P floats held as one vector value: the butterfly's selects between its
+// elements then stay selects between registers.
+template <int P>
+struct FVec {
+  typedef float type __attribute__((ext_vector_type(P)));
+};
+
 // Transposing butterfly over the LPR lanes of a group.  On return, if
 // P <= LPR, lane c of the group holds the total of value c >> (log2 LPR -
 // log2 P) in v[0]; otherwise it holds values c*P/LPR .. (c+1)*P/LPR - 1.
 template <int P, int LPR>
-__device__ __forceinline__ void xreduce(float (&v)[P], int lane) {
+__device__ __forceinline__ void xreduce(typename FVec<P>::type& v, int lane) {
   int cnt = P;
 #pragma unroll
   for (int o = LPR / 2; o >= 1; o >>= 1) {
@@ -85,23 +99,31 @@ __device__ __forceinline__ void xreduce(float (&v)[P], int lane) {
   }
 }
 
-constexpr int kVR = 1;    // vocabulary rows per lane group in flight
 constexpr int kBS = 512;  // threads per block
 
 template <int LPR>
 struct GemvShape {
-  static constexpr int GPW = 64 / LPR;                   // lane groups per wave
-  static constexpr int RPI = (kBS / 64) * GPW * kVR;     // rows per block iteration
+  static constexpr int GPW = 64 / LPR;             // lane groups (rows) per wave
+  static constexpr int RPI = (kBS / 64) * GPW;     // rows per block iteration
 };
 
+// Minimum waves per SIMD the register allocation aims for: 6 where that
+// holds without spilling (checked per instantiation: a reload inside the
+// main loop would make the wave wait for all of its weight loads), else 4.
 template <int MR, int LPR, int UNR, int WT, int EPI>
-__global__ __launch_bounds__(kBS) __attribute__((amdgpu_waves_per_eu(4, 8))) void k_gemv(const GemvArgs a) {
-  constexpr int VR = kVR;
+constexpr int gemv_waves() {
+  if (UNR == 4) return MR <= 4 ? 6 : 4;
+  if (MR <= 2) return 6;
+  return (LPR == 64 && WT == 0 && EPI == kEpiCloud && MR <= 4) ? 6 : 4;
+}
+
+template <int MR, int LPR, int UNR, int WT, int EPI>
+__global__ __launch_bounds__(kBS) __attribute__((amdgpu_waves_per_eu(gemv_waves<MR, LPR, UNR, WT, EPI>(), 8)))
+void k_gemv(const GemvArgs a) {
   constexpr int GPW = GemvShape<LPR>::GPW, RPI = GemvShape<LPR>::RPI;
   constexpr int EPC = WT == 0 ? 8 : 16;  // weight elements per 16-byte chunk
   constexpr int HW = EPC / 2;            // h words (bf16 pairs) per chunk
-  constexpr int NV = VR * MR;
-  constexpr int P = pow2ceil(NV);
+  constexpr int P = pow2ceil(MR);
   constexpr int PER = P > LPR ? P / LPR : 1;
 
   extern __shared__ __align__(16) uint8_t smem[];
@@ -115,6 +137,110 @@ __global__ __launch_bounds__(kBS) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   const int n = a.n;
   const int r0 = blockIdx.x * a.rows_per_block;
   const int r1 = min(n, r0 + a.rows_per_block);
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int cl = lane % LPR;
+  const int grp = wave * GPW + lane / LPR;
+  const int nchunk = Kp / EPC;
+
+  // Item stream: item t = (iteration t / passes, pass t % passes); in
+  // iteration it the group owns position r0 + it * RPI + grp.
+  const int passes = nchunk > 0 ? (nchunk + LPR * UNR - 1) / (LPR * UNR) : 1;
+  const int iters = (r1 - r0 + RPI - 1) / RPI;
+  const int T = (r1 > r0 && nchunk > 0) ? iters * passes : 0;
+  // Position of the group in iteration it, clamped to the block's last
+  // position (whose row is then read again but not reported).
+  auto pos_of = [&](int it) { return min(r0 + it * RPI + grp, r1 - 1); };
+
+  // After the reduction, reduced value i of this lane is h row own_m[i].
+  int own_m[PER];
+  bool own[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    if constexpr (P > LPR) {
+      own_m[i] = cl * PER + i;
+      own[i] = own_m[i] < MR;
+    } else {
+      constexpr int sh = ilog2(LPR) - ilog2(P);
+      own_m[i] = cl >> sh;
+      own[i] = (cl & ((1 << sh) - 1)) == 0 && own_m[i] < MR;
+    }
+  }
+
+  // Weight-row access.  With LPR == 64 a wave owns one row: it is read
+  // through a buffer descriptor in scalar registers whose size is the row's
+  // nchunk chunks, so chunks past the row read as zero with no memory access
+  // and chunk u of a pass is an immediate offset.  Smaller groups put
+  // several rows in a wave: 64-bit row addresses and per-lane chunk offsets
+  // clamped to the row's last chunk (their products are skipped).
+  uint32_t coff[LPR == 64 ? 1 : UNR];
+  auto set_coff = [&](int p) {
+    if constexpr (LPR == 64) {
+      coff[0] = (uint32_t)(cl + p * UNR * LPR) * 16u;
+    } else {
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) coff[u] = (uint32_t)min(cl + (p * UNR + u) * LPR, nchunk - 1) * 16u;
+    }
+  };
+  auto row_of = [&](int id) {
+    const uint64_t x = reinterpret_cast<uint64_t>(a.w) + (uint64_t)((int64_t)id * a.ldw_bytes);
+    if constexpr (LPR == 64) {
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+      const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+      void* base = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+      return __builtin_amdgcn_make_buffer_rsrc(base, 0, nchunk * 16, kBufferWord3);
+    } else {
+      return reinterpret_cast<const gbyte*>(x);
+    }
+  };
+  auto load_chunk = [&](auto row, int u) {
+    if constexpr (LPR == 64)
+      return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(
+                                             row, (int)coff[0], u * LPR * 16, kNonTemporal));
+    else
+      return __builtin_nontemporal_load(reinterpret_cast<const gu32x4*>(row + coff[u]));
+  };
+
+  // Epilogue operands of the values a lane owns in iteration it: the fp8
+  // row scale and the bias (cloud), or the payload code (fuse).  Every lane
+  // loads them, from index 0 where it has none, so the loads are
+  // unconditional and go out with the item's first weight chunk: no load in
+  // an epilogue makes the wave wait for the next item's weight loads.
+  struct Epi {
+    float e0[PER], e1[PER];
+  };
+  auto load_epi = [&](int it, int id, Epi& e) {
+    const int j = r0 + it * RPI + grp;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if constexpr (EPI == kEpiCloud) {
+        e.e0[i] = WT == 1 ? a.wscale[id] : 1.0f;
+        const float* bp = a.bias ? a.bias : a.wscale;  // any valid float array when unused
+        const float b = (a.bias || WT == 1) ? bp[(a.bias ? id : 0)] : 0.0f;
+        e.e1[i] = a.bias ? b : 0.0f;
+      } else {
+        const bool ok = own[i] && j < r1;
+        const int q = (int)a.q[ok ? (int64_t)own_m[i] * n + j : 0];
+        e.e0[i] = ok ? (float)q : 0.0f;
+        e.e1[i] = 0.0f;
+      }
+    }
+  };
+
+  // The first item's weight loads go out before h is staged, so the staging
+  // overlaps them.
+  u32x4_t cur[UNR];
+  Epi ecur;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) ecur.e0[i] = ecur.e1[i] = 0.0f;
+  if (T > 0) {
+    set_coff(0);
+    const int id = a.ids[pos_of(0)];
+    const auto row = row_of(id);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) cur[u] = load_chunk(row, u);
+    load_epi(0, id, ecur);
+  }
 
   if (tid < MR) {
     s_amax[tid] = 0u;
@@ -138,26 +264,12 @@ __global__ __launch_bounds__(kBS) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
   for (int j = r0 + tid; j < r1; j += kBS) s_ids[j - r0] = a.ids[j];
   __syncthreads();
 
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int cl = lane % LPR;
-  const int grp = wave * GPW + lane / LPR;
-  const int nchunk = Kp / EPC;
-
-  // Which reduced values this lane ends up holding (fixed for the whole
-  // kernel): value i is (row v = own_idx / MR of the group, h row m = own_idx % MR).
-  int own_idx[PER];
-  bool own[PER];
+  float qsc[PER];  // fuse: the payload row scale of each owned value
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    if constexpr (P > LPR) {
-      own_idx[i] = cl * PER + i;
-      own[i] = own_idx[i] < NV;
-    } else {
-      constexpr int sh = ilog2(LPR) - ilog2(P);
-      own_idx[i] = cl >> sh;
-      own[i] = (cl & ((1 << sh) - 1)) == 0 && own_idx[i] < NV;
-    }
+  for (int i = 0; i < PER; ++i) qsc[i] = 0.0f;
+  if constexpr (EPI == kEpiFuse) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) qsc[i] = a.qscale[own[i] ? own_m[i] : 0];
   }
   float run_amax[PER];
   unsigned long long run_key[PER];
@@ -166,127 +278,106 @@ __global__ __launch_bounds__(kBS) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
     run_amax[i] = 0.0f;
     run_key[i] = 0ull;
   }
-
-  // Flat item stream: item t = (iteration t / passes, pass t % passes).
-  const int passes = nchunk > 0 ? (nchunk + LPR * UNR - 1) / (LPR * UNR) : 1;
-  const int iters = (r1 - r0 + RPI - 1) / RPI;
-  const int T = r1 > r0 ? iters * passes : 0;
-
-  u32x4_t cur[UNR][VR];
-  int qcur[PER];
+  float acc[MR];
 #pragma unroll
-  for (int i = 0; i < PER; ++i) qcur[i] = 0;
+  for (int m = 0; m < MR; ++m) acc[m] = 0.0f;
 
-  auto load_item = [&](int t, u32x4_t (&buf)[UNR][VR], int (&qb)[PER]) {
-    const int it = t / passes, pass = t - it * passes;
-    const int jb = r0 + it * RPI + grp * VR;
+  // Products of chunk u of the current item; hp0 is this lane's first h
+  // element of the item's pass in row 0 of hs.
+  auto products = [&](int u, const uint16_t* hp0) {
 #pragma unroll
-    for (int v = 0; v < VR; ++v) {
-      const int j = jb + v;
-      const bool ok = j < r1;
-      const uint8_t* row = a.w + (int64_t)(ok ? s_ids[j - r0] : 0) * a.ldw_bytes;
+    for (int m = 0; m < MR; ++m) {
+      const uint32_t* hp = reinterpret_cast<const uint32_t*>(hp0 + m * Kp + u * LPR * EPC);
+      uint32_t hw[HW];
 #pragma unroll
-      for (int u = 0; u < UNR; ++u) {
-        const int c = cl + (pass * UNR + u) * LPR;
-        if (ok && c < nchunk)
-          buf[u][v] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(row + (int64_t)c * 16));
-        else
-          buf[u][v] = u32x4_t{0u, 0u, 0u, 0u};
+      for (int e = 0; e < HW; e += 4) {
+        const u32x4_t x = *reinterpret_cast<const u32x4_t*>(hp + e);
+        hw[e] = x.x; hw[e + 1] = x.y; hw[e + 2] = x.z; hw[e + 3] = x.w;
       }
-    }
-    if constexpr (EPI == kEpiFuse) {
-      if (pass == 0) {
+      float s = acc[m];
+      if constexpr (WT == 0) {
+        s = dot2_bf16(cur[u].x, hw[0], s);
+        s = dot2_bf16(cur[u].y, hw[1], s);
+        s = dot2_bf16(cur[u].z, hw[2], s);
+        s = dot2_bf16(cur[u].w, hw[3], s);
+      } else {
+        const uint32_t w4[4] = {cur[u].x, cur[u].y, cur[u].z, cur[u].w};
 #pragma unroll
-        for (int i = 0; i < PER; ++i) {
-          const int j = jb + own_idx[i] / MR;
-          qb[i] = (own[i] && j < r1) ? (int)a.q[(int64_t)(own_idx[i] % MR) * n + j] : 0;
+        for (int e = 0; e < 4; ++e) {
+          s = dot2_bf16(e4m3x2_to_bf16x2<false>(w4[e]), hw[2 * e], s);
+          s = dot2_bf16(e4m3x2_to_bf16x2<true>(w4[e]), hw[2 * e + 1], s);
         }
       }
+      acc[m] = s;
     }
   };
-
-  float acc[VR][MR];
+  // Reduction and epilogue of iteration it (after its last pass).
+  auto finish = [&](int it, const Epi& e) {
+    typename FVec<P>::type vals;
 #pragma unroll
-  for (int v = 0; v < VR; ++v)
+    for (int i = 0; i < P; ++i) vals[i] = i < MR ? acc[i] : 0.0f;
+    xreduce<P, LPR>(vals, lane);
+    const int j = r0 + it * RPI + grp;
 #pragma unroll
-    for (int m = 0; m < MR; ++m) acc[v][m] = 0.0f;
+    for (int i = 0; i < PER; ++i) {
+      const int m = own_m[i];
+      if (!own[i] || j >= r1) continue;
+      const float dot = vals[i];
+      if constexpr (EPI == kEpiCloud) {
+        const float z = dot * e.e0[i] + e.e1[i];
+        a.z[(int64_t)m * n + j] = z;
+        const float y = fminf(fmaxf(z, -a.clip), a.clip);
+        run_amax[i] = fmaxf(run_amax[i], fabsf(y));
+      } else {
+        const float f = __builtin_fmaf(e.e0[i], qsc[i], dot);
+        if (a.f) a.f[(int64_t)m * n + j] = f;
+        const unsigned long long key = argmax_key(f, j);
+        run_key[i] = key > run_key[i] ? key : run_key[i];
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[m] = 0.0f;
+  };
 
-  for (int t = 0; t < T; ++t) {
-    const int it = t / passes, pass = t - it * passes;
-    load_item(t, cur, qcur);
-
+  // Items 0 .. T-2: chunk u is consumed and its registers are refilled at
+  // once with chunk u of the next item, so about UNR loads per lane stay in
+  // flight through the products and the epilogue.  The last item, which
+  // loads nothing, is peeled off so that the loop's loads are unconditional
+  // and the compiler's wait counts stay exact.
+  int it = 0, pass = 0;
+  for (int t = 0; t + 1 < T; ++t) {
+    const int npass = pass + 1 == passes ? 0 : pass + 1;
+    const int nit = npass == 0 ? it + 1 : it;
+    const int nid = s_ids[pos_of(nit) - r0];
+    const auto nrow = row_of(nid);
+    const uint16_t* hp0 = hs + (cl + pass * UNR * LPR) * EPC;
+    const int c0 = cl + pass * UNR * LPR;
+    if (passes > 1) set_coff(npass);
+    Epi enext = ecur;
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
-      const int c = cl + (pass * UNR + u) * LPR;
-      if (c < nchunk) {
-#pragma unroll
-        for (int m = 0; m < MR; ++m) {
-          const uint32_t* hp = reinterpret_cast<const uint32_t*>(hs + m * Kp + c * EPC);
-          uint32_t hw[HW];
-#pragma unroll
-          for (int e = 0; e < HW; e += 4) {
-            const u32x4_t x = *reinterpret_cast<const u32x4_t*>(hp + e);
-            hw[e] = x.x; hw[e + 1] = x.y; hw[e + 2] = x.z; hw[e + 3] = x.w;
-          }
-#pragma unroll
-          for (int v = 0; v < VR; ++v) {
-            float s = acc[v][m];
-            if constexpr (WT == 0) {
-              s = dot2_bf16(cur[u][v].x, hw[0], s);
-              s = dot2_bf16(cur[u][v].y, hw[1], s);
-              s = dot2_bf16(cur[u][v].z, hw[2], s);
-              s = dot2_bf16(cur[u][v].w, hw[3], s);
-            } else {
-              const uint32_t w4[4] = {cur[u][v].x, cur[u][v].y, cur[u][v].z, cur[u][v].w};
-#pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                s = dot2_bf16(e4m3x2_to_bf16x2<false>(w4[e]), hw[2 * e], s);
-                s = dot2_bf16(e4m3x2_to_bf16x2<true>(w4[e]), hw[2 * e + 1], s);
-              }
-            }
-            acc[v][m] = s;
-          }
-        }
-      }
+      if (c0 + u * LPR < nchunk) products(u, hp0);
+      cur[u] = load_chunk(nrow, u);
+      if (u == 0 && npass == 0) load_epi(nit, nid, enext);
     }
-
-    if (pass == passes - 1) {
-      float vals[P];
+    if (pass == passes - 1) finish(it, ecur);
+    ecur = enext;
+    it = nit;
+    pass = npass;
+  }
+  if (T > 0) {
+    const uint16_t* hp0 = hs + (cl + pass * UNR * LPR) * EPC;
+    const int c0 = cl + pass * UNR * LPR;
 #pragma unroll
-      for (int i = 0; i < P; ++i) vals[i] = i < NV ? acc[i / MR][i % MR] : 0.0f;
-      xreduce<P, LPR>(vals, lane);
-      const int jb = r0 + it * RPI + grp * VR;
-#pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int m = own_idx[i] % MR;
-        const int j = jb + own_idx[i] / MR;
-        if (!own[i] || j >= r1) continue;
-        const float dot = vals[i];
-        if constexpr (EPI == kEpiCloud) {
-          float z = dot;
-          if constexpr (WT == 1) z = z * a.wscale[s_ids[j - r0]];
-          if (a.bias) z = z + a.bias[s_ids[j - r0]];
-          a.z[(int64_t)m * n + j] = z;
-          const float y = fminf(fmaxf(z, -a.clip), a.clip);
-          run_amax[i] = fmaxf(run_amax[i], fabsf(y));
-        } else {
-          const float f = __builtin_fmaf((float)qcur[i], a.qscale[m], dot);
-          if (a.f) a.f[(int64_t)m * n + j] = f;
-          const unsigned long long key = argmax_key(f, j);
-          run_key[i] = key > run_key[i] ? key : run_key[i];
-        }
-      }
-#pragma unroll
-      for (int v = 0; v < VR; ++v)
-#pragma unroll
-        for (int m = 0; m < MR; ++m) acc[v][m] = 0.0f;
-    }
+    for (int u = 0; u < UNR; ++u)
+      if (c0 + u * LPR < nchunk) products(u, hp0);
+    finish(it, ecur);
   }
 
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     if (!own[i]) continue;
-    const int m = own_idx[i] % MR;
+    const int m = own_m[i];
     if constexpr (EPI == kEpiCloud)
       atomicMax(&s_amax[m], __float_as_uint(run_amax[i]));
     else
@@ -317,7 +408,7 @@ int gemv_lpr(int K, int wtype) {
   return lpr;
 }
 
-int gemv_rows_per_iter(int lpr) { return 4 * (64 / lpr) * kVR; }
+int gemv_rows_per_iter(int lpr) { return (kBS / 64) * (64 / lpr); }
 
 // Chunks per lane per pass.
 static int gemv_unr(int K, int wtype, int lpr) {
