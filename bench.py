@@ -66,6 +66,54 @@ def algorithmic_bytes(cfg, n):
     return n * per_id + cfg.M * cfg.d_cloud * 2
 
 
+def attainable_peaks(dev):
+    """Attainable peaks measured in this job (best of 5 each):
+    - read_gbs: the library's streaming-read probe over 1 GiB (16-byte
+      non-temporal loads, as the skinny projection reads weight rows);
+    - mfma_bf16_tflops: the library's MFMA probe (32x32x16 bf16 loop on random
+      operands that change every iteration);
+    - copy_gbs: a 1 GiB device copy (bytes read + written), vendor kernel;
+    - gemm_bf16_tflops: an 8192^3 bf16 GEMM on N(0,1) data, vendor library."""
+    import torch
+
+    import paper_2607_13093_amd as sph
+
+    def best_ms(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(b))
+        return best
+
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    read_gbs = nbytes / (best_ms(lambda: sph.probe_read(src, sink)) * 1e-3) / 1e9
+    copy_gbs = 2 * nbytes / (best_ms(lambda: dst.copy_(src)) * 1e-3) / 1e9
+    del src, dst
+    iters = 20000
+    flops = sph.probe_mfma(iters, sink)
+    mfma_tflops = flops / (best_ms(lambda: sph.probe_mfma(iters, sink)) * 1e-3) / 1e12
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    n = 8192
+    a = torch.randn((n, n), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    b = torch.randn((n, n), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    gemm_tflops = 2.0 * n ** 3 / (best_ms(lambda: torch.matmul(a, b)) * 1e-3) / 1e12
+    del a, b
+    torch.cuda.empty_cache()
+    return {"read_gbs": read_gbs, "mfma_bf16_tflops": mfma_tflops, "copy_gbs": copy_gbs,
+            "gemm_bf16_tflops": gemm_tflops}
+
+
 def source_digest():
     h = hashlib.sha256()
     for name in ("gemv.hip", "sph_internal.h"):
@@ -237,6 +285,11 @@ def main():
                 "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": k_ms,
                 "kernel_source_sha256_16": digest}
 
+    att = attainable_peaks(dev)
+    att_peak = att["read_gbs"] if roof["bound"] == "hbm" else att["mfma_bf16_tflops"]
+    roof["attainable_peak"] = att_peak
+    roof["frac_attainable"] = roof["achieved"] / att_peak
+
     out = {
         "metric": "split-head rows*vocab/s",
         "value": M * n / (ms_step * 1e-3),
@@ -259,6 +312,7 @@ def main():
             "payload_bytes_per_row": n + 4,
         },
         "roofline": roof,
+        "attainable": att,
         "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
         "ms_per_step_traced": ms_step_traced,
     }

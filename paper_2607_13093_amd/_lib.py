@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(HERE, "libsph.so")
 c_i64 = ctypes.c_int64
 c_vp = ctypes.c_void_p
 
-# name -> (restype, argtypes); mirrors include/sph.h
+# name -> (restype, argtypes); mirrors include/sph.h and include/sph_probe.h
 SIGNATURES = {
     "sph_abi_version": (ctypes.c_int, []),
     "sph_last_error": (ctypes.c_char_p, []),
@@ -41,6 +41,9 @@ SIGNATURES = {
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
     "sph_trace_start": (ctypes.c_int, [ctypes.c_int]),
     "sph_trace_stop": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
+    # include/sph_probe.h
+    "sph_probe_read": (ctypes.c_int, [c_vp, c_i64, c_vp, c_vp]),
+    "sph_probe_mfma": (ctypes.c_int, [c_i64, c_vp, c_vp, ctypes.POINTER(ctypes.c_double)]),
 }
 
 

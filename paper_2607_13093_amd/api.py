@@ -179,3 +179,23 @@ def trace_collect(capacity: int):
     n = ctypes.c_int(0)
     check(lib.sph_trace_stop(recs, int(capacity), n))
     return [(recs[i].kernel.decode(), float(recs[i].ms)) for i in range(min(n.value, capacity))]
+
+
+def probe_read(buf: torch.Tensor, sink: torch.Tensor) -> None:
+    """Enqueue one streaming read of all of `buf` (measurement helper of
+    include/sph_probe.h); time it with events on the current stream."""
+    _require_gpu("buf", buf)
+    _require_gpu("sink", sink)
+    check(_lib.load().sph_probe_read(buf.data_ptr(), buf.numel() * buf.element_size(),
+                                     sink.data_ptr(), _stream_handle(buf.device)))
+
+
+def probe_mfma(iters: int, sink: torch.Tensor) -> float:
+    """Enqueue one bf16 MFMA loop of `iters` iterations (measurement helper of
+    include/sph_probe.h) and return its floating-point operation count."""
+    import ctypes
+    _require_gpu("sink", sink)
+    flops = ctypes.c_double(0.0)
+    check(_lib.load().sph_probe_mfma(int(iters), sink.data_ptr(), _stream_handle(sink.device),
+                                     ctypes.byref(flops)))
+    return flops.value

@@ -41,6 +41,12 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // Global-memory views of weight rows (loads through them are global, not flat).
 typedef __attribute__((address_space(1))) const uint8_t gbyte;
 typedef __attribute__((address_space(1))) const u32x4_t gu32x4;
+// Constant-space view: a load through it at a wave-uniform index is a scalar
+// load (no vector registers, not counted with the vector-memory loads).
+typedef __attribute__((address_space(4))) const float cfloat;
+__device__ __forceinline__ float uniform_load(const float* p, int i) {
+  return reinterpret_cast<const cfloat*>(reinterpret_cast<uintptr_t>(p))[i];
+}
 // Fourth word of a raw buffer descriptor (32-bit data format) and the
 // non-temporal cache policy of a buffer load.
 constexpr int kBufferWord3 = 0x00020000;
@@ -114,7 +120,7 @@ template <int MR, int LPR, int UNR, int WT, int EPI>
 constexpr int gemv_waves() {
   if (UNR == 4) return MR <= 4 ? 6 : 4;
   if (MR <= 2) return 6;
-  return (LPR == 64 && WT == 0 && EPI == kEpiCloud && MR <= 4) ? 6 : 4;
+  return (LPR == 64 && WT == 0 && EPI == kEpiCloud && MR <= 5) ? 6 : 4;
 }
 
 template <int MR, int LPR, int UNR, int WT, int EPI>
@@ -209,8 +215,12 @@ void k_gemv(const GemvArgs a) {
   struct Epi {
     float e0[PER], e1[PER];
   };
+  // With LPR == 64 the cloud operands are wave-uniform and are read with
+  // scalar loads in the epilogue instead.
+  constexpr bool kScalarEpi = EPI == kEpiCloud && LPR == 64;
   auto load_epi = [&](int it, int id, Epi& e) {
     const int j = r0 + it * RPI + grp;
+    if constexpr (kScalarEpi) return;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       if constexpr (EPI == kEpiCloud) {
@@ -323,7 +333,15 @@ void k_gemv(const GemvArgs a) {
       const int m = own_m[i];
       if (!own[i] || j >= r1) continue;
       const float dot = vals[i];
-      if constexpr (EPI == kEpiCloud) {
+      if constexpr (kScalarEpi) {
+        const int id = __builtin_amdgcn_readfirstlane(s_ids[j - r0]);
+        const float sc = WT == 1 ? uniform_load(a.wscale, id) : 1.0f;
+        const float b = a.bias ? uniform_load(a.bias, id) : 0.0f;
+        const float z = dot * sc + b;
+        a.z[(int64_t)m * n + j] = z;
+        const float y = fminf(fmaxf(z, -a.clip), a.clip);
+        run_amax[i] = fmaxf(run_amax[i], fabsf(y));
+      } else if constexpr (EPI == kEpiCloud) {
         const float z = dot * e.e0[i] + e.e1[i];
         a.z[(int64_t)m * n + j] = z;
         const float y = fminf(fmaxf(z, -a.clip), a.clip);

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "sph.h"
+#include "sph_probe.h"
 #include "sph_internal.h"
 
 struct sph_subset_s {
@@ -475,6 +476,27 @@ int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out) {
   if (n_out) *n_out = k;
   trace_free_locked();
   return rc == SPH_OK ? ok() : rc;
+}
+
+
+int sph_probe_read(const void* buf, int64_t bytes, float* sink, void* stream) {
+  if (!buf || !sink) return fail(SPH_E_INVALID_ARG, "sph_probe_read: buf or sink is NULL");
+  if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0 || bytes <= 0 || bytes % 16 != 0)
+    return fail(SPH_E_INVALID_ARG, "sph_probe_read: buf must be 16-byte aligned and bytes a positive "
+                                   "multiple of 16 (got %lld)", (long long)bytes);
+  const hipError_t e = sph::launch_probe_read(buf, bytes, sink, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "read probe launch");
+  return ok();
+}
+
+int sph_probe_mfma(int64_t iters, float* sink, void* stream, double* flops_out) {
+  if (!sink || !flops_out) return fail(SPH_E_INVALID_ARG, "sph_probe_mfma: sink or flops_out is NULL");
+  if (iters < 1 || iters > (int64_t(1) << 30))
+    return fail(SPH_E_INVALID_ARG, "sph_probe_mfma: iters %lld not in [1, 2^30]", (long long)iters);
+  const hipError_t e = sph::launch_probe_mfma((int)iters, sink, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(e, "MFMA probe launch");
+  *flops_out = sph::probe_mfma_flops(iters);
+  return ok();
 }
 
 }  // extern "C"

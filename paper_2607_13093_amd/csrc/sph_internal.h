@@ -119,4 +119,9 @@ hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_
                                int n_sessions, int R, const int32_t* drafts,
                                int32_t* tokens, int32_t* accept, hipStream_t s);
 
+// Measurement kernels (probe.hip).
+hipError_t launch_probe_read(const void* buf, int64_t bytes, float* sink, hipStream_t s);
+hipError_t launch_probe_mfma(int iters, float* sink, hipStream_t s);
+double probe_mfma_flops(int64_t iters);
+
 }  // namespace sph

@@ -1,7 +1,8 @@
-"""The C-ABI library: it loads, exports what include/sph.h declares, and its
+"""The C-ABI library: it loads, exports what include/*.h declare, and its
 host-side validation rejects bad arguments before touching any device."""
 
 import ctypes
+import glob
 import os
 import re
 
@@ -14,9 +15,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared_functions():
-    text = open(os.path.join(ROOT, "include", "sph.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(sph_[a-z_]+)\s*\(", text)))
+    names = set()
+    for path in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))):
+        text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
+        names |= set(re.findall(r"\b(sph_[a-z_]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
@@ -29,7 +32,7 @@ def test_every_declared_symbol_is_exported(lib):
     assert len(names) >= 10
     for name in names:
         assert hasattr(lib, name), name
-    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with sph.h"
+    assert set(names) == set(_lib.SIGNATURES), "binding signatures out of sync with include/*.h"
 
 
 def test_abi_version(lib):
@@ -141,3 +144,29 @@ def test_error_string_is_thread_local(lib):
     t.join()
     assert seen["msg"] == b""
     assert b"M=-1" in lib.sph_last_error()
+
+
+@pytest.mark.parametrize("buf,nbytes,sink,msg", [
+    (0, 1024, 64, "NULL"),
+    (16, 1024, 0, "NULL"),
+    (24, 1024, 64, "16-byte aligned"),
+    (16, 1000, 64, "multiple of 16"),
+    (16, 0, 64, "multiple of 16"),
+])
+def test_probe_read_validation(lib, buf, nbytes, sink, msg):
+    # rejected on the host: no pointer is dereferenced, nothing is launched
+    assert lib.sph_probe_read(buf, nbytes, sink, None) == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+
+
+@pytest.mark.parametrize("iters,sink,with_out,msg", [
+    (0, 64, True, "iters"),
+    ((1 << 30) + 1, 64, True, "iters"),
+    (10, 0, True, "NULL"),
+    (10, 64, False, "NULL"),
+])
+def test_probe_mfma_validation(lib, iters, sink, with_out, msg):
+    flops = ctypes.c_double(0.0)
+    out = ctypes.byref(flops) if with_out else None
+    assert lib.sph_probe_mfma(iters, sink, None, out) == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
