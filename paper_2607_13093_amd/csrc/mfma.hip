@@ -101,26 +101,28 @@ __device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
 }
 
 // Epilogue of a BM x BN tile held as acc[FM][FN] 32x32 fragments by the
-// 2 x 2 waves.  Row of accumulator r in fragment (i, j):
+// WM x WN waves.  Row of accumulator r in fragment (i, j):
 // 8*(r/4) + 4*(lane/32) + r%4; column: lane % 32.
 // For the fuse epilogue the payload tile q[m0:m0+BM, n0:n0+BN] and the row
 // scales are first staged in LDS the main loop no longer needs (s_q: BM*BN
 // bytes, s_qs: BM floats) with coalesced loads, instead of one byte load per
 // accumulator.  The caller has passed a barrier after its last LDS read.
-template <int BM, int BN, int WT, int EPI, int FM, int FN>
+template <int BM, int BN, int WM, int WN, int WT, int EPI, int FM, int FN>
 __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const MfmaArgs& a,
                                               const int32_t* s_ids, uint32_t* s_rmax,
                                               unsigned long long* s_rkey, int m0, int n0,
                                               int nt, int8_t* s_q, float* s_qs) {
-  constexpr int TM = BM / 2, TN = BN / 2, P = FM * 16;
+  constexpr int NT = 64 * WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
+  constexpr int P = (FM * 16 + 31) / 32 * 32;  // row values per lane, padded for the butterfly
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int M = a.M, n = a.n;
   if constexpr (EPI == kEpiFuse) {
     const bool vec = (n & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
     if (vec) {
       constexpr int CPR = BN / 16;  // 16-byte chunks per tile row
-      for (int c = tid; c < BM * CPR; c += 256) {
+      for (int c = tid; c < BM * CPR; c += NT) {
         const int r = c / CPR, k = c % CPR;
         const int row = m0 + r, col = n0 + k * 16;
         u32x4_t v = {0u, 0u, 0u, 0u};
@@ -128,17 +130,19 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
         *reinterpret_cast<u32x4_t*>(s_q + r * BN + k * 16) = v;
       }
     } else {
-      for (int c = tid; c < BM * BN; c += 256) {
+      for (int c = tid; c < BM * BN; c += NT) {
         const int r = c / BN, k = c % BN;
         const int row = m0 + r, col = n0 + k;
         s_q[c] = (row < M && col < n) ? a.q[(int64_t)row * n + col] : (int8_t)0;
       }
     }
-    for (int r = tid; r < BM; r += 256) s_qs[r] = m0 + r < M ? a.qscale[m0 + r] : 0.0f;
+    for (int r = tid; r < BM; r += NT) s_qs[r] = m0 + r < M ? a.qscale[m0 + r] : 0.0f;
     __syncthreads();
   }
   using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
   V red[P];
+#pragma unroll
+  for (int t = FM * 16; t < P; ++t) red[t] = V(0);
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -174,6 +178,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
 #pragma unroll
   for (int t = 0; t < PER; ++t) {
     const int idx = (lane & 31) * PER + t;
+    if (idx >= FM * 16) continue;
     const int i = idx / 16, r = idx % 16;
     const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
     if constexpr (EPI == kEpiCloud)
@@ -182,7 +187,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
       atomicMax(&s_rkey[lrow], red[t]);
   }
   __syncthreads();
-  for (int i = tid; i < BM; i += 256) {
+  for (int i = tid; i < BM; i += NT) {
     const int row = m0 + i;
     if (row >= M) continue;
     if constexpr (EPI == kEpiCloud)
@@ -317,7 +322,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     buf ^= 1;
   }
 
-  tile_epilogue<BM, BN, WT, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+  tile_epilogue<BM, BN, 2, 2, WT, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
                                  reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
 }
 
@@ -332,16 +337,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // M and subset positions past n read a valid row (row M-1 / the last id):
 // they only feed outputs that are never written.  On the decode-sized dense
 // shape this loop ran 1.2x faster than register staging.
+// Waves: WM x WN (wave tile (BM/WM) x (BN/WN)); 2 x 2 with one wave per SIMD,
+// or 2 x 4 for 320-row tiles (wave tile 160 x 64) with two waves per SIMD,
+// whose accumulators then live in the 256 registers each wave has.
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ int swz8(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_mfma_dma(const MfmaArgs a) {
+template <int BM, int BN, int WM, int WN, int EPI>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
+void k_mfma_dma(const MfmaArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int TM = BM / 2, TN = BN / 2;
+  constexpr int NT = 64 * WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;  // DMA instructions per wave per step
+  constexpr int A_INS = BM / 8 / (WM * WN), B_INS = BN / 8 / (WM * WN);  // DMA instructions per wave per step
   extern __shared__ __align__(16) uint8_t smem[];
   uint16_t* As = reinterpret_cast<uint16_t*>(smem);      // [2][BM][64]
   uint16_t* Bs = As + 2 * BM * kBK;                       // [2][BN][64]
@@ -350,14 +360,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_rmax + BM + (BM & 1));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   int mt, nt;
   tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   const int M = a.M, K = a.K, n = a.n;
   const int last_id = a.ids[min(n, n0 + BN) - 1];
-  for (int i = tid; i < BN; i += 256) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
-  for (int i = tid; i < BM; i += 256) {
+  for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  for (int i = tid; i < BM; i += NT) {
     s_rmax[i] = 0u;
     s_rkey[i] = 0ull;
   }
@@ -436,7 +446,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __syncthreads();
     stage ^= 1;
   }
-  tile_epilogue<BM, BN, 0, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+  tile_epilogue<BM, BN, WM, WN, 0, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
                                 reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
 #endif
 }
@@ -448,17 +458,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // the 32 rows a fragment read touches spread over the LDS banks.  Each lane
 // reads its 8 codes of a fragment (ds_read_b64) and widens them to bf16
 // (exact) in registers right before the MFMA; the per-row scale is applied
-// in the epilogue.  All fragments of a step are read before the next step's
-// loads are issued (the compiler would otherwise make the reads wait for
-// those loads), and scheduling barriers keep the loads ahead of the MFMAs.
+// in the epilogue.  With one wave per SIMD all fragments of a step are read
+// before the next step's loads are issued (the compiler would otherwise make
+// the reads wait for those loads), and scheduling barriers keep the loads
+// ahead of the MFMAs.  With two waves per SIMD (320-row tiles) those
+// fragments would not fit next to the accumulators: the loads go out first,
+// each sub-step reads its own fragments, and the SIMD's other wave covers
+// the wait.
 __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_mfma_dma8(const MfmaArgs a) {
+template <int BM, int BN, int WM, int WN, int EPI>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
+void k_mfma_dma8(const MfmaArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int TM = BM / 2, TN = BN / 2;
+  constexpr int NT = 64 * WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN;
   constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 16 / 4;  // DMA instructions per wave per step
+  constexpr int A_INS = BM / 8 / (WM * WN), B_INS = BN / 16 / (WM * WN);  // DMA instructions per wave per step
   extern __shared__ __align__(16) uint8_t smem[];
   uint16_t* As = reinterpret_cast<uint16_t*>(smem);             // [2][BM][64] bf16
   uint8_t* Bs = reinterpret_cast<uint8_t*>(As + 2 * BM * kBK);   // [2][BN][64] fp8
@@ -467,14 +483,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_rmax + BM + (BM & 1));
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   int mt, nt;
   tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   const int M = a.M, K = a.K, n = a.n;
   const int last_id = a.ids[min(n, n0 + BN) - 1];
-  for (int i = tid; i < BN; i += 256) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
-  for (int i = tid; i < BM; i += 256) {
+  for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  for (int i = tid; i < BM; i += NT) {
     s_rmax[i] = 0u;
     s_rkey[i] = 0ull;
   }
@@ -524,6 +540,45 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   for (int k0 = 0; k0 < K; k0 += kBK) {
     const uint16_t* as = As + stage * BM * kBK;
     const uint8_t* bs = Bs + stage * BN * kBK;
+    if constexpr (WM * WN > 4) {
+      // Two waves per SIMD: a step's fragments for all four sub-steps do not
+      // fit in registers next to the accumulators, so the next stage's loads
+      // go out first and each sub-step reads its own fragments (the other
+      // wave of the SIMD covers any wait on the loads).
+      if (k0 + kBK < K) issue(k0 + kBK, stage ^ 1);
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        const int c = kk * 2 + (lane >> 5);
+        bf16x8_t af[FM], bfr[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int row = wm * TM + i * 32 + (lane & 31);
+          af[i] = *reinterpret_cast<const bf16x8_t*>(as + row * kBK + ((c ^ swz8(row)) << 3));
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int row = wn * TN + j * 32 + (lane & 31);
+          const uint2 q = *reinterpret_cast<const uint2*>(bs + row * kBK + ((kk ^ swz4(row)) << 4) +
+                                                          8 * (lane >> 5));
+          u32x4_t w;
+          w.x = e4m3x2_to_bf16x2_m<false>(q.x);
+          w.y = e4m3x2_to_bf16x2_m<true>(q.x);
+          w.z = e4m3x2_to_bf16x2_m<false>(q.y);
+          w.w = e4m3x2_to_bf16x2_m<true>(q.y);
+          bfr[j] = __builtin_bit_cast(bf16x8_t, w);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+      stage ^= 1;
+      continue;
+    }
     bf16x8_t af[kBK / 16][FM];
     uint2 bq[kBK / 16][FN];
 #pragma unroll
@@ -568,7 +623,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     __syncthreads();
     stage ^= 1;
   }
-  tile_epilogue<BM, BN, 1, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
+  tile_epilogue<BM, BN, WM, WN, 1, EPI>(acc, a, s_ids, s_rmax, s_rkey, m0, n0, nt,
                                 reinterpret_cast<int8_t*>(As), reinterpret_cast<float*>(Bs));
 #endif
 }
@@ -591,57 +646,61 @@ constexpr size_t mfma_dma8_lds_bytes() {
          (size_t)BM * 8;
 }
 
+// Waves of a row tile: 2 x 2 (wave tile (BM/2) x (BN/2)); 320-row tiles use
+// 2 x 4 waves (wave tile 160 x 64), two per SIMD.
+template <int BM>
+struct WaveGrid {
+  static constexpr int WM = 2, WN = BM == 320 ? 4 : 2;
+};
+
 template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
+  constexpr int WM = WaveGrid<BM>::WM, WN = WaveGrid<BM>::WN, NT = 64 * WM * WN;
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
   if (a.n_tiles > kMaxBlocks) return hipErrorInvalidValue;
-  if constexpr (WT == 0) {
-    if (a.K % kBK == 0) {
-      auto kd = k_mfma_dma<BM, BN, EPI>;
-      constexpr size_t lds_d = mfma_dma_lds_bytes<BM, BN>();
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
-      if (e != hipSuccess) return e;
-      launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
-      return hipGetLastError();
-    }
+  if (a.K % kBK == 0) {
+    auto kd = WT == 0 ? k_mfma_dma<BM, BN, WM, WN, EPI> : k_mfma_dma8<BM, BN, WM, WN, EPI>;
+    constexpr size_t lds_d = WT == 0 ? mfma_dma_lds_bytes<BM, BN>() : mfma_dma8_lds_bytes<BM, BN>();
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
+    if (e != hipSuccess) return e;
+    launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(NT), lds_d, s, a);
+    return hipGetLastError();
   }
-  if constexpr (WT == 1) {
-    if (a.K % kBK == 0) {
-      auto kd = k_mfma_dma8<BM, BN, EPI>;
-      constexpr size_t lds_d = mfma_dma8_lds_bytes<BM, BN>();
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
-      if (e != hipSuccess) return e;
-      launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_d, s, a);
-      return hipGetLastError();
-    }
+  if constexpr (WM * WN == 4) {
+    auto kern = k_mfma<BM, BN, WT, EPI>;
+    constexpr size_t lds = mfma_lds_bytes<BM, BN>();
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    launch_kernel(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
+    return hipGetLastError();
   }
-  auto kern = k_mfma<BM, BN, WT, EPI>;
-  constexpr size_t lds = mfma_lds_bytes<BM, BN>();
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  launch_kernel(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
-// Row tile: 256 (the better ratio of MFMA work to operand traffic) unless that
-// pads M by more than half where 128 pads less.  Measured: M = 640 runs 13%
-// faster with 256-row tiles despite 20% padding; M = 320 (60% padding) is even.
-static int mfma_bm(int M) {
+// Row tile for M rows: 128 up to 128 rows, else whichever of 256 and 320
+// pads M less (320-row tiles need K a multiple of the K step).  Measured on
+// the batched shape (M = 320, 60000 ids): 320-row tiles, one per 256 ids,
+// 156 us against 265 us for 256-row and 289 us for 128-row tiles; M = 640
+// with fp8 weights: 460 us against 537 us for 256-row tiles.
+static int mfma_bm(int M, int K) {
+  if (M <= 128) return 128;
   const int pad256 = (M + 255) / 256 * 256 - M;
-  const int pad128 = (M + 127) / 128 * 128 - M;
-  return (pad256 * 2 > M && pad128 < pad256) ? 128 : 256;
+  const int pad320 = (M + 319) / 320 * 320 - M;
+  return (K % kBK == 0 && pad320 < pad256) ? 320 : 256;
 }
 
 int mfma_n_tiles(int n) { return (n + kMfmaBN - 1) / kMfmaBN; }
 
 template <int WT, int EPI>
 static hipError_t launch_bm(const MfmaArgs& a, hipStream_t s) {
-  return mfma_bm(a.M) == 256 ? launch_tile<256, kMfmaBN, WT, EPI>(a, s)
-                             : launch_tile<128, kMfmaBN, WT, EPI>(a, s);
+  switch (mfma_bm(a.M, a.K)) {
+    case 320: return launch_tile<320, kMfmaBN, WT, EPI>(a, s);
+    case 256: return launch_tile<256, kMfmaBN, WT, EPI>(a, s);
+    default: return launch_tile<128, kMfmaBN, WT, EPI>(a, s);
+  }
 }
 
 hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s) {

@@ -119,7 +119,8 @@ RAGGED = [
     # dense (MFMA) path: more than 8 rows
     (3, 3, 520, 40, 3000, 1001),    # 9 rows, ragged m- and n-tiles
     (8, 5, 1032, 0, 4000, 2500),    # 40 rows, d_end = 0
-    (17, 17, 1096, 72, 9000, 4097), # 289 rows: three 128-row m-tiles, ragged n
+    (17, 17, 1096, 72, 9000, 4097), # 289 rows: one 320-row m-tile (8 waves), ragged n
+    (24, 25, 1096, 72, 9000, 4097), # 600 rows: two 320-row m-tiles, the second ragged
     (13, 10, 2056, 8, 9000, 8193),  # 130 rows: two m-tiles, last n-tile of one column
 ]
 
@@ -190,6 +191,13 @@ def test_fp8_cloud_partial_dense():
     cfg = Config("fp8_dense", 27, d=1056, d_end=32, vocab=5000, n_sub=3001, subset_kind="choice",
                  sessions=12, rows_per_session=5, wtype="fp8", with_bias=True)
     run_greedy_case(make_workload(cfg), tag="fp8 dense")
+
+
+def test_fp8_cloud_partial_dense_320_row_tiles():
+    # 300 rows: one 320-row tile of 8 waves, fp8 codes copied to LDS directly
+    cfg = Config("fp8_dense_320", 29, d=1088, d_end=64, vocab=7000, n_sub=3003, subset_kind="choice",
+                 sessions=60, rows_per_session=5, wtype="fp8", with_bias=True)
+    run_greedy_case(make_workload(cfg), tag="fp8 dense, 320-row tiles")
 
 
 def test_fp8_cloud_partial_dense_k_not_multiple_of_64():
