@@ -171,10 +171,11 @@ int sph_fuse_verify(const int8_t* q, const float* scale,
                     void* workspace, size_t ws_bytes, void* stream);
 
 /*
- * Kernel tracing.  While a trace is active, every kernel the library
- * launches is bracketed by two HIP events recorded on the launch stream, so
- * the durations are those of the kernels as they ran in the caller's
- * workload.  Tracing is process-wide and costs two event records per launch.
+ * Kernel tracing.  While a trace is active, each call records one duration
+ * per kernel it launches: start and stop HIP events are attached to the
+ * kernel dispatches themselves (hipExtLaunchKernelGGL), so a duration is
+ * the kernel's execution on the launch stream as it ran in the caller's
+ * workload, with no launch gap included.  Tracing is process-wide.
  */
 #define SPH_TRACE_NAME_LEN 32
 typedef struct {
