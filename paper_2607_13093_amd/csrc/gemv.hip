@@ -81,28 +81,76 @@ struct FVec {
   typedef float type __attribute__((ext_vector_type(P)));
 };
 
+// Lane exchanges of the butterfly below, all VALU (no LDS crossbar):
+//  * v_permlane32_swap / v_permlane16_swap exchange the upper half of one
+//    register's 64- / 32-lane groups with the lower half of another's; the sum
+//    of the two results is, in the lower half of each group, x[l] + x[l ^ o]
+//    and, in the upper half, y[l] + y[l ^ o] (o = 32 / 16) - one transposing
+//    butterfly step for the pair (x, y) in one swap and one add;
+//  * DPP row_ror:8 and quad permutations read lane l ^ 8, l ^ 2, l ^ 1;
+//  * DPP row_half_mirror pairs lanes l and 7 - l of an 8-lane group.
+// (Lane mappings checked on the device.)
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppRor8 = 0x128, kDppHalfMirror = 0x141, kDppXor2 = 0x4E, kDppXor1 = 0xB1;
+
+template <int O>
+__device__ __forceinline__ float lane_xor(float v) {
+  if constexpr (O == 8) return dpp<kDppRor8>(v);
+  else if constexpr (O == 2) return dpp<kDppXor2>(v);
+  else if constexpr (O == 1) return dpp<kDppXor1>(v);
+  else return __shfl_xor(v, O, 64);
+}
+
+// One step of the transposing butterfly over the lanes of a group, at lane
+// distance O with CNT values per lane still to be reduced, then the rest.
+template <int O, int CNT, int P>
+__device__ __forceinline__ void xstep(typename FVec<P>::type& v, int lane) {
+  if constexpr (O >= 1) {
+    if constexpr (CNT > 1) {
+      constexpr int H = CNT / 2;
+      const bool upper = (lane & O) != 0;
+#pragma unroll
+      for (int i = 0; i < H; ++i) {
+        if constexpr (O == 32 || O == 16) {
+          const auto r = O == 32
+              ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]), __float_as_uint(v[i + H]), false, false)
+              : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]), __float_as_uint(v[i + H]), false, false);
+          v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+        } else {
+          const float t0 = v[i] + lane_xor<O>(v[i]);
+          const float t1 = v[i + H] + lane_xor<O>(v[i + H]);
+          v[i] = upper ? t1 : t0;
+        }
+      }
+      xstep<O / 2, H, P>(v, lane);
+    } else if constexpr (O == 4) {
+      // plain sum over the 8 lanes of a group: mirror pairs, then quads
+      float t = v[0] + dpp<kDppHalfMirror>(v[0]);
+      t += dpp<kDppXor2>(t);
+      v[0] = t + dpp<kDppXor1>(t);
+    } else {
+      if constexpr (O == 32 || O == 16) {
+        const uint32_t u = __float_as_uint(v[0]);
+        const auto r = O == 32 ? __builtin_amdgcn_permlane32_swap(u, u, false, false)
+                               : __builtin_amdgcn_permlane16_swap(u, u, false, false);
+        v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+      } else {
+        v[0] += lane_xor<O>(v[0]);
+      }
+      xstep<O / 2, 1, P>(v, lane);
+    }
+  }
+}
+
 // Transposing butterfly over the LPR lanes of a group.  On return, if
 // P <= LPR, lane c of the group holds the total of value c >> (log2 LPR -
 // log2 P) in v[0]; otherwise it holds values c*P/LPR .. (c+1)*P/LPR - 1.
 template <int P, int LPR>
 __device__ __forceinline__ void xreduce(typename FVec<P>::type& v, int lane) {
-  int cnt = P;
-#pragma unroll
-  for (int o = LPR / 2; o >= 1; o >>= 1) {
-    if (cnt > 1) {
-      const int half = cnt / 2;
-      const bool upper = (lane & o) != 0;
-#pragma unroll
-      for (int i = 0; i < half; ++i) {
-        const float send = upper ? v[i] : v[i + half];
-        const float keep = upper ? v[i + half] : v[i];
-        v[i] = keep + __shfl_xor(send, o, 64);
-      }
-      cnt = half;
-    } else {
-      v[0] += __shfl_xor(v[0], o, 64);
-    }
-  }
+  xstep<LPR / 2, P, P>(v, lane);
 }
 
 constexpr int kBS = 512;  // threads per block
