@@ -51,12 +51,6 @@ __device__ __forceinline__ unsigned long long argmax_key_m(float v, int pos) {
   return ((unsigned long long)u << 32) | (unsigned long long)(0xFFFFFFFFu - (uint32_t)pos);
 }
 
-__device__ __forceinline__ unsigned long long shfl_xor_u64_m(unsigned long long x, int o) {
-  const uint32_t lo = __shfl_xor((uint32_t)x, o, 64);
-  const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), o, 64);
-  return ((unsigned long long)hi << 32) | lo;
-}
-
 constexpr int kBK = 64;          // K elements per staged step
 constexpr int kLDK = kBK + 8;    // padded LDS row, bf16 elements (144 bytes)
 constexpr int kGM = 8;           // m-tiles grouped per n-tile in the tile order
@@ -76,28 +70,77 @@ __device__ __forceinline__ void tile_of_block(int b, int m_tiles, int n_tiles, i
 }
 
 
+// Lane exchanges of the butterfly below, all VALU except the 4-lane step:
+// v_permlane16_swap exchanges the upper 16 lanes of each 32-lane half of one
+// register with the lower 16 of another, so the larger of its two results is,
+// in lanes l & 16 == 0, max(x[l], x[l ^ 16]) and otherwise max(y[l], y[l ^ 16]);
+// DPP row_ror:8 and quad permutations read lane l ^ 8, l ^ 2 and l ^ 1.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <int O>
+__device__ __forceinline__ uint32_t lane_xor_u32(uint32_t v) {
+  if constexpr (O == 8) return dpp_u32<0x128>(v);       // row_ror:8
+  else if constexpr (O == 2) return dpp_u32<0x4E>(v);   // quad_perm 2,3,0,1
+  else if constexpr (O == 1) return dpp_u32<0xB1>(v);   // quad_perm 1,0,3,2
+  else return (uint32_t)__shfl_xor((int)v, O, 64);
+}
+template <class T>
+__device__ __forceinline__ T vmax(T a, T b) { return a > b ? a : b; }
+
+// Values are float or 64-bit keys, moved as 32-bit words.
+template <class T, int O>
+__device__ __forceinline__ T xor_lane(T v) {
+  if constexpr (sizeof(T) == 8) {
+    const uint32_t lo = lane_xor_u32<O>((uint32_t)v), hi = lane_xor_u32<O>((uint32_t)(v >> 32));
+    return ((T)hi << 32) | lo;
+  } else {
+    return __uint_as_float(lane_xor_u32<O>(__float_as_uint(v)));
+  }
+}
+template <class T>
+__device__ __forceinline__ void swap16(T& x, T& y) {
+  if constexpr (sizeof(T) == 8) {
+    const auto lo = __builtin_amdgcn_permlane16_swap((uint32_t)x, (uint32_t)y, false, false);
+    const auto hi = __builtin_amdgcn_permlane16_swap((uint32_t)(x >> 32), (uint32_t)(y >> 32), false, false);
+    x = ((T)hi[0] << 32) | lo[0];
+    y = ((T)hi[1] << 32) | lo[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+    x = __uint_as_float(r[0]);
+    y = __uint_as_float(r[1]);
+  }
+}
+
+template <int O, int CNT, int P, class T>
+__device__ __forceinline__ void half_wave_max_step(T (&v)[P], int lane) {
+  if constexpr (O >= 1) {
+    constexpr int H = CNT / 2;
+    const bool upper = (lane & O) != 0;
+#pragma unroll
+    for (int i = 0; i < H; ++i) {
+      if constexpr (O == 16) {
+        T x = v[i], y = v[i + H];
+        swap16(x, y);
+        v[i] = vmax(x, y);
+      } else {
+        const T t0 = vmax(v[i], xor_lane<T, O>(v[i]));
+        const T t1 = vmax(v[i + H], xor_lane<T, O>(v[i + H]));
+        v[i] = upper ? t1 : t0;
+      }
+    }
+    half_wave_max_step<O / 2, H, P>(v, lane);
+  }
+}
+
 // Transposing butterfly inside each 32-lane half of a wave: on entry lane l
 // holds P values; after log2(32) exchanges lane (l & 31) holds the max over
 // the half's 32 lanes of values (l & 31) * P/32 .. + P/32 - 1.
 template <int P, class T>
 __device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
   static_assert(P >= 32 && P % 32 == 0, "values per lane");
-  int cnt = P;
-#pragma unroll
-  for (int o = 16; o >= 1; o >>= 1) {
-    const int half = cnt / 2;
-    const bool upper = (lane & o) != 0;
-#pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const T send = upper ? v[i] : v[i + half];
-      const T keep = upper ? v[i + half] : v[i];
-      T got;
-      if constexpr (sizeof(T) == 8) got = shfl_xor_u64_m(send, o);
-      else got = __shfl_xor(send, o, 64);
-      v[i] = keep > got ? keep : got;
-    }
-    cnt = half;
-  }
+  half_wave_max_step<16, P, P>(v, lane);
 }
 
 // Epilogue of a BM x BN tile held as acc[FM][FN] 32x32 fragments by the
@@ -122,12 +165,20 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
     const bool vec = (n & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
     if (vec) {
       constexpr int CPR = BN / 16;  // 16-byte chunks per tile row
-      for (int c = tid; c < BM * CPR; c += NT) {
-        const int r = c / CPR, k = c % CPR;
+      constexpr int PT = BM * CPR / NT;  // chunks per thread, all loaded before any is stored
+      static_assert(PT * NT == BM * CPR, "payload tile / threads");
+      u32x4_t v[PT];
+#pragma unroll
+      for (int t = 0; t < PT; ++t) {
+        const int c = tid + t * NT, r = c / CPR, k = c % CPR;
         const int row = m0 + r, col = n0 + k * 16;
-        u32x4_t v = {0u, 0u, 0u, 0u};
-        if (row < M && col < n) v = *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)row * n + col);
-        *reinterpret_cast<u32x4_t*>(s_q + r * BN + k * 16) = v;
+        v[t] = (row < M && col < n) ? *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)row * n + col)
+                                    : u32x4_t{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int t = 0; t < PT; ++t) {
+        const int c = tid + t * NT, r = c / CPR, k = c % CPR;
+        *reinterpret_cast<u32x4_t*>(s_q + r * BN + k * 16) = v[t];
       }
     } else {
       for (int c = tid; c < BM * BN; c += NT) {
@@ -646,19 +697,25 @@ constexpr size_t mfma_dma8_lds_bytes() {
          (size_t)BM * 8;
 }
 
-// Waves of a row tile: 256- and 320-row tiles use 2 x 4 waves (wave tiles
-// 128 x 64 and 160 x 64, two waves per SIMD, so one wave's MFMAs run while
-// the other waits at a barrier or on LDS); 128-row tiles use 2 x 2.  On the
-// dense 2048-row shapes 2 x 4 waves ran the cloud projection 9% and the
-// endpoint projection 28% faster than 2 x 2 (wave tile 128 x 128).
-template <int BM>
+// Waves of a row tile.  256- and 320-row tiles use 8 waves, two per SIMD, so
+// one wave's MFMAs run while the other waits at a barrier or on LDS: 2 x 4
+// (wave tiles 128 x 64 / 160 x 64) for the cloud projection, whose long K
+// loop ran 6% faster so than with 4 x 2; 4 x 2 (wave tile 64 x 128) for the
+// endpoint projection, whose short K loop leaves its epilogue dominant: 32
+// rows per lane instead of 64 halve the argmax butterfly.  128-row tiles use
+// 2 x 2.  On the dense 2048-row shapes 8 waves ran the cloud projection 9%
+// and the endpoint projection 28% faster than 4 (wave tile 128 x 128).
+template <int BM, int EPI>
 struct WaveGrid {
-  static constexpr int WM = 2, WN = BM >= 256 ? 4 : 2;
+  static constexpr bool kEight = BM >= 256;
+  static constexpr bool kTall = kEight && !(BM == 256 && EPI == kEpiFuse);
+  static constexpr int WM = kEight ? (kTall ? 2 : 4) : 2;
+  static constexpr int WN = kEight ? (kTall ? 4 : 2) : 2;
 };
 
 template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
-  constexpr int WM = WaveGrid<BM>::WM, WN = WaveGrid<BM>::WN, NT = 64 * WM * WN;
+  constexpr int WM = WaveGrid<BM, EPI>::WM, WN = WaveGrid<BM, EPI>::WN, NT = 64 * WM * WN;
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
   if (a.n_tiles > kMaxBlocks) return hipErrorInvalidValue;
