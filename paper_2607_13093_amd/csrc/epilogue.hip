@@ -27,8 +27,18 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ z,
   const int m = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ float s_red[4];
+  // all of a thread's partial maxima are loaded at once (no load waits on
+  // the previous one)
+  constexpr int PT = kMaxBlocks / 256;
+  float part[PT];
+#pragma unroll
+  for (int t = 0; t < PT; ++t) {
+    const int i = tid + 256 * t;
+    part[t] = i < nblk ? amax_part[(int64_t)m * kMaxBlocks + i] : 0.0f;
+  }
   float a = 0.0f;
-  for (int i = tid; i < nblk; i += 256) a = fmaxf(a, amax_part[(int64_t)m * kMaxBlocks + i]);
+#pragma unroll
+  for (int t = 0; t < PT; ++t) a = fmaxf(a, part[t]);
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) a = fmaxf(a, __shfl_xor(a, o, 64));
   if (lane == 0) s_red[wave] = a;
@@ -41,13 +51,23 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ z,
   const int j0 = blockIdx.y * kQuantChunk;
   const int j1 = min(n, j0 + kQuantChunk);
   if (vec) {
-    for (int j = j0 + tid * 4; j < j1; j += 1024) {
-      const float4 v = *reinterpret_cast<const float4*>(z + row + j);
+    // the chunk's z values of this thread are loaded before any is stored
+    constexpr int VT = kQuantChunk / 1024;
+    float4 v[VT];
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const int j = j0 + tid * 4 + 1024 * t;
+      v[t] = j < j1 ? *reinterpret_cast<const float4*>(z + row + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int t = 0; t < VT; ++t) {
+      const int j = j0 + tid * 4 + 1024 * t;
+      if (j >= j1) continue;
       char4 o;
-      o.x = quantize_one(v.x, clip, s);
-      o.y = quantize_one(v.y, clip, s);
-      o.z = quantize_one(v.z, clip, s);
-      o.w = quantize_one(v.w, clip, s);
+      o.x = quantize_one(v[t].x, clip, s);
+      o.y = quantize_one(v[t].y, clip, s);
+      o.z = quantize_one(v[t].z, clip, s);
+      o.w = quantize_one(v[t].w, clip, s);
       *reinterpret_cast<char4*>(q + row + j) = o;
     }
   } else {
@@ -89,6 +109,10 @@ __global__ __launch_bounds__(64 * kFinalWaves) void k_final_greedy(
   const int s = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   __shared__ int32_t s_tok[kMaxRowsPerSession];
+  __shared__ int32_t s_draft[kMaxRowsPerSession];
+  // the session's drafts are staged while the keys are read, so the prefix
+  // match below reads LDS only
+  for (int r = tid; r < R - 1; r += blockDim.x) s_draft[r] = drafts[(int64_t)s * (R - 1) + r];
   for (int r = wave; r < R; r += kFinalWaves) {
     const int64_t m = (int64_t)s * R + r;
     unsigned long long x[PER_LANE];
@@ -118,7 +142,7 @@ __global__ __launch_bounds__(64 * kFinalWaves) void k_final_greedy(
   if (tid == 0) {
     const int kd = R - 1;
     int a = 0;
-    while (a < kd && s_tok[a] == drafts[(int64_t)s * kd + a]) ++a;
+    while (a < kd && s_tok[a] == s_draft[a]) ++a;
     accept[s] = a;
   }
 }

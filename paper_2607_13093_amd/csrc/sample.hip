@@ -937,7 +937,22 @@ __global__ void k_accept(const int32_t* __restrict__ tokens, const int32_t* __re
   if (s >= n_sessions) return;
   const int kd = R - 1;
   int a = 0;
-  while (a < kd && tokens[(int64_t)s * R + a] == drafts[(int64_t)s * kd + a]) ++a;
+  bool run = true;
+  // tokens and drafts are loaded eight at a time, before any comparison
+  for (int b = 0; b < kd && run; b += 8) {
+    int32_t t[8], d[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const bool ok = b + u < kd;
+      t[u] = ok ? tokens[(int64_t)s * R + b + u] : 0;
+      d[u] = ok ? drafts[(int64_t)s * kd + b + u] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (run && b + u < kd && t[u] == d[u]) ++a;
+      else run = false;
+    }
+  }
   accept[s] = a;
 }
 
