@@ -234,9 +234,34 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t x, int o) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+// Sum over the wave, in every lane, without the LDS crossbar: the 32- and
+// 16-lane steps swap register halves with v_permlane32_swap /
+// v_permlane16_swap (both results summed), then DPP rotations by 8, 4, 2
+// and 1 lanes inside each 16-lane row finish the sum.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  return ((uint64_t)dpp_u32<CTRL>((uint32_t)(v >> 32)) << 32) | dpp_u32<CTRL>((uint32_t)v);
+}
+template <bool W32>
+__device__ __forceinline__ uint64_t swap_sum_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const auto l = W32 ? __builtin_amdgcn_permlane32_swap(lo, lo, false, false)
+                     : __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+  const auto h = W32 ? __builtin_amdgcn_permlane32_swap(hi, hi, false, false)
+                     : __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+  return (((uint64_t)h[0] << 32) | l[0]) + (((uint64_t)h[1] << 32) | l[1]);
+}
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += shfl_xor_u64(v, o);
+  v = swap_sum_u64<true>(v);
+  v = swap_sum_u64<false>(v);
+  v += dpp_u64<0x128>(v);  // row_ror:8
+  v += dpp_u64<0x124>(v);  // row_ror:4
+  v += dpp_u64<0x122>(v);  // row_ror:2
+  v += dpp_u64<0x121>(v);  // row_ror:1
   return v;
 }
 
