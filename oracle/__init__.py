@@ -19,8 +19,13 @@ from .split_head import (  # noqa: F401
     full_head_logits,
     cloud_partial_logits,
     clip_quantize,
+    clip_quantize_fmt,
+    pack_codes,
+    unpack_codes,
+    payload_bytes,
     endpoint_partial_logits,
     fuse_masked,
+    fuse_masked_fmt,
     round_sum_to_f32,
     greedy_select,
     philox4x32_10,

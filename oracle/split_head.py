@@ -16,7 +16,9 @@ the design notes of the repository):
 * clipping is a symmetric clamp of the cloud partial logits to [-c, c];
 * the b-bit quantiser Q_b of eq. 18 is per-row symmetric int8 with a dynamic
   scale s = amax/127, codes in [-127, 127], round-half-to-even, computed with
-  correctly rounded fp32 division;
+  correctly rounded fp32 division; the configurable variant takes b in {4, 8}
+  (codes in [-(2^(b-1) - 1), 2^(b-1) - 1], 4-bit codes packed two per byte)
+  and one scale per row or per block of subset positions;
 * dequantisation and fusion are one fp32 rounding of q*s + z_end;
 * greedy ties go to the lowest vocabulary id;
 * sampling uses top-p nucleus selection on top of eq. 15, with the draw made
@@ -166,6 +168,88 @@ def clip_quantize(z, clip_c):
     return {"y": y, "amax": amax, "scale": scale, "t": t, "q": q}
 
 
+def clip_quantize_fmt(z, clip_c, bits=8, block=0):
+    """Clip and quantise with a configurable bit width b and scale granularity.
+
+    Eq. 18 quantises tensor elements to a configurable bit width b, and the
+    payload estimate of eq. 21 is |V_l| * b/8 bytes plus metadata.  Reading
+    for b in {4, 8}: symmetric codes in [-qmax, qmax], qmax = 2^(b-1) - 1,
+    with one dynamic scale per row (block = 0, the reading of clip_quantize)
+    or per row and block of `block` consecutive subset positions (the last
+    block of a row may be shorter):
+        y = clamp(z, -c, c)                           (fp32)
+        a[m, k] = max |y[m, j]| over block k          (exact)
+        s[m, k] = fp32(a / qmax), 0 if a = 0          (correctly rounded)
+        t = fp32(y / s[m, k(j)])                      (correctly rounded)
+        q = clamp(rint_half_even(t), -qmax, qmax), 0 where s = 0
+    Returns dict(y, amax [M, nb], scale [M, nb], t, q (int8 codes [M, n])).
+    Pinned by: b = 8 with one scale per row reproduces clip_quantize;
+    |q*s - y| <= s/2; every block's element of largest |y| gets +-qmax; a
+    hand-worked 4-bit example with two blocks.
+    """
+    if bits not in (4, 8):
+        raise ValueError("bits must be 4 or 8")
+    z = np.asarray(z, dtype=np.float32)
+    c = np.float32(clip_c)
+    y = np.minimum(np.maximum(z, -c), c)
+    M, n = y.shape
+    qmax = np.float32(2 ** (bits - 1) - 1)
+    width = n if block == 0 else block
+    nb = 1 if block == 0 else max(1, -(-n // block))
+    amax = np.zeros((M, nb), dtype=np.float32)
+    for k in range(nb):
+        seg = y[:, k * width:(k + 1) * width]
+        if seg.shape[1]:
+            amax[:, k] = np.abs(seg).max(axis=1)
+    scale = (amax / qmax).astype(np.float32)
+    col_scale = np.repeat(scale, width, axis=1)[:, :n] if n else np.zeros((M, 0), np.float32)
+    pos = col_scale > 0
+    t = np.zeros_like(y)
+    np.divide(y, col_scale, out=t, where=pos)
+    q = np.clip(np.rint(t), -qmax, qmax).astype(np.int8)
+    q[~pos] = 0
+    return {"y": y, "amax": amax, "scale": scale, "t": t, "q": q}
+
+
+def pack_codes(q, bits):
+    """Payload bytes of b-bit codes, row by row: b = 8 stores each code as a
+    byte (two's complement); b = 4 stores code 2i in the low and code 2i+1 in
+    the high nibble of byte i (two's complement nibbles; an odd row ends with
+    a zero high nibble).  Returns uint8 [M, ceil(n * b / 8)].
+    Pinned by: a hand-written byte pattern and the unpack round trip."""
+    q = np.asarray(q, dtype=np.int8)
+    if bits == 8:
+        return q.view(np.uint8).copy()
+    if bits != 4:
+        raise ValueError("bits must be 4 or 8")
+    M, n = q.shape
+    nib = (q.astype(np.int16) & 0xF).astype(np.uint8)
+    if n % 2:
+        nib = np.concatenate([nib, np.zeros((M, 1), np.uint8)], axis=1)
+    return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+
+
+def unpack_codes(p, n, bits):
+    """Inverse of pack_codes: int8 codes [M, n]."""
+    p = np.asarray(p, dtype=np.uint8)
+    if bits == 8:
+        return p[:, :n].view(np.int8).copy()
+    lo = (p & 0xF).astype(np.int16)
+    hi = (p >> 4).astype(np.int16)
+    nib = np.empty((p.shape[0], 2 * p.shape[1]), np.int16)
+    nib[:, 0::2] = lo
+    nib[:, 1::2] = hi
+    nib = np.where(nib >= 8, nib - 16, nib)
+    return nib[:, :n].astype(np.int8)
+
+
+def payload_bytes(n, bits, block):
+    """Payload of one row (eq. 21 without transport overheads): the packed
+    codes plus one fp32 scale per block (one per row for block = 0)."""
+    nb = 1 if block == 0 else max(1, -(-n // block))
+    return -(-n * bits // 8) + 4 * nb
+
+
 # ---------------------------------------------------------------------------
 # eq. 11 restricted to S: the endpoint partial
 # ---------------------------------------------------------------------------
@@ -240,6 +324,17 @@ def fuse_masked(q, scale, z_end) -> np.ndarray:
     q = np.asarray(q, dtype=np.int8).astype(np.float64)
     s = np.asarray(scale, dtype=np.float32).astype(np.float64)[:, None]
     return round_sum_to_f32(q * s, np.asarray(z_end, dtype=np.float32).astype(np.float64))
+
+
+def fuse_masked_fmt(q, scale, z_end, block=0) -> np.ndarray:
+    """fuse_masked with per-(row, block) scales: f[m, j] = fp32(q[m, j] *
+    s[m, k(j)] + z_end[m, j]), k(j) = j // block (k = 0 for block = 0).
+    Pinned by: with one scale per row it equals fuse_masked."""
+    q = np.asarray(q, dtype=np.int8).astype(np.float64)
+    s = np.asarray(scale, dtype=np.float32).astype(np.float64)
+    n = q.shape[1]
+    cols = np.zeros(n, dtype=np.int64) if block == 0 else np.arange(n) // block
+    return round_sum_to_f32(q * s[:, cols], np.asarray(z_end, dtype=np.float32).astype(np.float64))
 
 
 # ---------------------------------------------------------------------------

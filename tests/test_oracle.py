@@ -239,6 +239,69 @@ def test_clip_and_zero_rows():
 
 
 # ---------------------------------------------------------------------------
+# configurable payload format: b in {4, 8}, one scale per row or per block
+# (eq. 18 with a configurable bit width; eq. 21's payload size)
+# ---------------------------------------------------------------------------
+
+def test_format_b8_per_row_is_the_int8_reading():
+    rng = np.random.default_rng(12)
+    z = (rng.standard_normal((7, 1001)) * 6).astype(np.float32)
+    a, b = oracle.clip_quantize(z, 30.0), oracle.clip_quantize_fmt(z, 30.0, bits=8, block=0)
+    np.testing.assert_array_equal(a["q"], b["q"])
+    np.testing.assert_array_equal(a["scale"], b["scale"][:, 0])
+
+
+@pytest.mark.parametrize("bits,block", [(4, 0), (4, 256), (8, 256), (4, 1024), (8, 4096)])
+def test_format_invariants(bits, block):
+    rng = np.random.default_rng(13)
+    n = 3001                                        # ragged last block, odd for the 4-bit packing
+    z = (rng.standard_normal((9, n)) * rng.uniform(0.1, 20, (9, 1))).astype(np.float32)
+    out = oracle.clip_quantize_fmt(z, 30.0, bits=bits, block=block)
+    y, s, q = out["y"], out["scale"], out["q"].astype(np.int32)
+    qmax = 2 ** (bits - 1) - 1
+    width = n if block == 0 else block
+    cols = np.arange(n) // width
+    sc = s[:, cols].astype(np.float64)
+    assert np.all(np.abs(q) <= qmax)
+    assert np.all(np.abs(q * sc - y) <= sc * (0.5 + 2 ** -20))
+    for k in range(s.shape[1]):
+        seg = np.abs(y[:, k * width:(k + 1) * width])
+        at = np.argmax(seg, axis=1) + k * width
+        assert np.all(np.abs(q[np.arange(9), at]) == qmax)
+        # a block's scale never exceeds the row's
+        assert np.all(s[:, k] <= np.abs(y).max(axis=1) / qmax * (1 + 2 ** -22))
+    np.testing.assert_array_equal(oracle.unpack_codes(oracle.pack_codes(out["q"], bits), n, bits), out["q"])
+    assert oracle.pack_codes(out["q"], bits).shape[1] == -(-n * bits // 8)
+    assert oracle.payload_bytes(n, bits, block) == -(-n * bits // 8) + 4 * s.shape[1]
+
+
+def test_format_4bit_worked_example():
+    # two blocks of 4 positions, codes in [-7, 7]
+    z = np.array([[0.7, -1.4, 0.35, 0.0, 2.0, 3.5, -0.25, 7.0, 1.0]], dtype=np.float32)
+    out = oracle.clip_quantize_fmt(z, 30.0, bits=4, block=4)
+    # block 0: amax 1.4, s = fp32(1.4/7) = 0.2: t = 3.5, -7, 1.75, 0 -> 4 (half to even), -7, 2, 0
+    # block 1: amax 7,   s = 1:               t = 2, 3.5, -0.25, 7 -> 2, 4, 0, 7
+    # block 2: amax 1,   s = fp32(1/7):       t = 7                -> 7
+    np.testing.assert_array_equal(out["scale"][0], np.float32([np.float32(1.4) / np.float32(7),
+                                                               1.0, np.float32(1.0) / np.float32(7)]))
+    np.testing.assert_array_equal(out["q"][0], [4, -7, 2, 0, 2, 4, 0, 7, 7])
+    # nibbles (two's complement): 4|-7 -> 0x94, 2|0 -> 0x02, 2|4 -> 0x42, 0|7 -> 0x70, 7|pad -> 0x07
+    np.testing.assert_array_equal(oracle.pack_codes(out["q"], 4)[0], [0x94, 0x02, 0x42, 0x70, 0x07])
+    np.testing.assert_array_equal(oracle.pack_codes([[1, -1, 7, -7]], 4)[0], [0xF1, 0x97])
+
+
+def test_format_fuse_per_row_equals_fuse_masked_and_uses_block_scales():
+    rng = np.random.default_rng(14)
+    q = rng.integers(-7, 8, (3, 600)).astype(np.int8)
+    s = rng.uniform(0.01, 1, (3, 3)).astype(np.float32)
+    ze = rng.standard_normal((3, 600)).astype(np.float32)
+    np.testing.assert_array_equal(oracle.fuse_masked_fmt(q, s[:, :1], ze, 0), oracle.fuse_masked(q, s[:, 0], ze))
+    f = oracle.fuse_masked_fmt(q, s, ze, 256)
+    j = 513                                         # third block
+    assert f[1, j] == np.float32(float(q[1, j]) * float(s[1, 2]) + float(ze[1, j]))
+
+
+# ---------------------------------------------------------------------------
 # fusion rounding
 # ---------------------------------------------------------------------------
 
