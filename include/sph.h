@@ -171,6 +171,50 @@ int sph_fuse_verify(const int8_t* q, const float* scale,
                     void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Configurable payload format (eq. 18 quantises to a configurable bit width
+ * b; eq. 21 puts the payload at about |V_l| * b/8 bytes plus metadata).
+ *
+ *   bits   8: codes in [-127, 127], one byte each (the format above);
+ *          4: codes in [-7, 7], two per byte: code 2i in the low and code
+ *             2i+1 in the high nibble of byte i, two's complement nibbles;
+ *             an odd n_sub ends with a zero high nibble.
+ *   block  0: one scale per row (the format above);
+ *          256, 512, 1024, 2048 or 4096: one scale per row and block of that
+ *             many consecutive subset positions (the last block may be
+ *             shorter): a[m, k] = max |y[m, j]| over block k and
+ *             scale[m, k] = fp32(a[m, k] / qmax), qmax = 2^(bits-1) - 1.
+ *   Codes are clamp(rint_half_even(fp32(y / scale)), -qmax, qmax) as above.
+ * A payload of M rows is M * sph_payload_code_bytes(n_sub, bits) code bytes
+ * (rows contiguous) and fp32 scales [M, sph_payload_scale_count(n_sub, block)].
+ */
+
+/* ceil(n_sub * bits / 8), or -1 for an invalid bits or n_sub. */
+int64_t sph_payload_code_bytes(int64_t n_sub, int bits);
+
+/* 1 for block 0, else ceil(n_sub / block) (at least 1); -1 if invalid. */
+int64_t sph_payload_scale_count(int64_t n_sub, int64_t block);
+
+/* sph_cloud_partial with the payload in format (bits, block): q_out holds the
+ * packed codes, scale_out the scales as described above.  (8, 0) is
+ * sph_cloud_partial.  Same workspace. */
+int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                          const void* w_cloud, int64_t ldw, int wtype, const float* w_row_scale,
+                          const float* bias, sph_subset subset, float clip_c, int bits,
+                          int64_t block, void* q_out, float* scale_out, float* z_out,
+                          void* workspace, size_t ws_bytes, void* stream);
+
+/* sph_fuse_verify reading a payload in format (bits, block):
+ *   f[m, j] = fmaf(code[m, j], scale[m, k(j)], z_end[m, j]),  k(j) = j / block
+ * (k = 0 for block 0).  (8, 0) is sph_fuse_verify.  Same workspace. */
+int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t block,
+                        const void* h_end, int64_t ldh, int64_t d_end, const void* w_end,
+                        int64_t ldw, sph_subset subset, int64_t n_sessions,
+                        int64_t rows_per_session, const int32_t* drafts, int mode,
+                        float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                        int32_t* accept_len_out, float* fused_out, void* workspace,
+                        size_t ws_bytes, void* stream);
+
+/*
  * Kernel tracing.  While a trace is active, each call records one duration
  * per kernel it launches: start and stop HIP events are attached to the
  * kernel dispatches themselves (hipExtLaunchKernelGGL), so a duration is

@@ -14,6 +14,8 @@ from .api import (  # noqa: F401
     cloud_partial_workspace,
     fuse_verify,
     fuse_verify_workspace,
+    payload_code_bytes,
+    payload_scale_count,
     probe_mfma,
     probe_read,
     trace_collect,

@@ -39,6 +39,23 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_uint64,  # mode, temperature, top_p, seed
         c_vp, c_vp, c_vp,                   # tokens_out, accept_len_out, fused_out
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_payload_code_bytes": (c_i64, [c_i64, ctypes.c_int]),
+    "sph_payload_scale_count": (c_i64, [c_i64, c_i64]),
+    "sph_cloud_partial_fmt": (ctypes.c_int, [
+        c_vp, c_i64, c_i64, c_i64,          # h_cloud, ldh, M, d_cloud
+        c_vp, c_i64, ctypes.c_int, c_vp,    # w_cloud, ldw, wtype, w_row_scale
+        c_vp, c_vp, ctypes.c_float,         # bias, subset, clip_c
+        ctypes.c_int, c_i64,                # bits, block
+        c_vp, c_vp, c_vp,                   # q_out, scale_out, z_out
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_fuse_verify_fmt": (ctypes.c_int, [
+        c_vp, c_vp, ctypes.c_int, c_i64,    # q, scale, bits, block
+        c_vp, c_i64, c_i64,                 # h_end, ldh, d_end
+        c_vp, c_i64, c_vp,                  # w_end, ldw, subset
+        c_i64, c_i64, c_vp,                 # n_sessions, rows_per_session, drafts
+        ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_uint64,  # mode, temperature, top_p, seed
+        c_vp, c_vp, c_vp,                   # tokens_out, accept_len_out, fused_out
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
     "sph_trace_start": (ctypes.c_int, [ctypes.c_int]),
     "sph_trace_stop": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
     # include/sph_probe.h

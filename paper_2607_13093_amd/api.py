@@ -91,14 +91,28 @@ def fuse_verify_workspace(M: int, subset: Subset, mode: int = GREEDY) -> int:
     return int(_lib.load().sph_fuse_verify_workspace(int(M), subset.handle, int(mode)))
 
 
+def payload_code_bytes(n: int, bits: int = 8) -> int:
+    """Bytes of one payload row's codes (include/sph.h)."""
+    return int(_lib.load().sph_payload_code_bytes(int(n), int(bits)))
+
+
+def payload_scale_count(n: int, block: int = 0) -> int:
+    """Scales of one payload row (include/sph.h)."""
+    return int(_lib.load().sph_payload_scale_count(int(n), int(block)))
+
+
 def cloud_partial(h_cloud: torch.Tensor, w_cloud: torch.Tensor, subset: Subset, clip_c: float,
                   w_row_scale: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
-                  want_z: bool = False, workspace: Optional[torch.Tensor] = None, out=None):
-    """Cloud half: returns (q int8 [M, n], scale fp32 [M], z fp32 [M, n] or None).
+                  want_z: bool = False, workspace: Optional[torch.Tensor] = None, out=None,
+                  bits: int = 8, block: int = 0):
+    """Cloud half: returns (q, scale, z fp32 [M, n] or None).
 
     h_cloud: bf16 [M, d_cloud] view (rows may be strided, e.g. h[:, d_end:]).
     w_cloud: bf16 [V, d_cloud] or fp8 E4M3 (torch.float8_e4m3fn / uint8) with
     w_row_scale fp32 [V].
+    Payload format (bits, block): q is int8 [M, n] for 8-bit codes, uint8
+    [M, ceil(n/2)] (two codes per byte) for 4-bit codes; scale is fp32 [M]
+    for one scale per row (block 0), else [M, ceil(n / block)].
     """
     lib = _lib.load()
     _require_gpu("h_cloud", h_cloud)
@@ -113,18 +127,22 @@ def cloud_partial(h_cloud: torch.Tensor, w_cloud: torch.Tensor, subset: Subset, 
     M, d_cloud = h_cloud.shape
     dev = h_cloud.device
     if out is None:
-        q = torch.empty((M, subset.n), dtype=torch.int8, device=dev)
-        scale = torch.empty((M,), dtype=torch.float32, device=dev)
+        nb = payload_scale_count(subset.n, block)
+        if bits == 8:
+            q = torch.empty((M, subset.n), dtype=torch.int8, device=dev)
+        else:
+            q = torch.empty((M, max(payload_code_bytes(subset.n, bits), 0)), dtype=torch.uint8, device=dev)
+        scale = torch.empty((M,) if block == 0 else (M, max(nb, 0)), dtype=torch.float32, device=dev)
         z = torch.empty((M, subset.n), dtype=torch.float32, device=dev) if want_z else None
     else:
         q, scale, z = out
     need = cloud_partial_workspace(M, subset)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    check(lib.sph_cloud_partial(
+    check(lib.sph_cloud_partial_fmt(
         h_cloud.data_ptr(), h_cloud.stride(0) if M > 0 else d_cloud, M, d_cloud,
         w_cloud.data_ptr(), w_cloud.stride(0), wtype, _ptr(w_row_scale),
-        _ptr(bias), subset.handle, float(clip_c),
+        _ptr(bias), subset.handle, float(clip_c), int(bits), int(block),
         q.data_ptr(), scale.data_ptr(), _ptr(z),
         workspace.data_ptr(), workspace.numel(), _stream_handle(dev)))
     return q, scale, z
@@ -134,8 +152,10 @@ def fuse_verify(q: torch.Tensor, scale: torch.Tensor, h_end: Optional[torch.Tens
                 w_end: Optional[torch.Tensor], subset: Subset, n_sessions: int,
                 rows_per_session: int, drafts: Optional[torch.Tensor], mode: int = GREEDY,
                 temperature: float = 1.0, top_p: float = 1.0, seed: int = 0,
-                want_fused: bool = False, workspace: Optional[torch.Tensor] = None, out=None):
-    """Endpoint half: returns (tokens int32 [M], accept_len int32 [S], fused fp32 or None)."""
+                want_fused: bool = False, workspace: Optional[torch.Tensor] = None, out=None,
+                bits: int = 8, block: int = 0):
+    """Endpoint half: returns (tokens int32 [M], accept_len int32 [S], fused fp32 or None).
+    (q, scale) is a payload of cloud_partial in format (bits, block)."""
     lib = _lib.load()
     dev = q.device
     M = int(n_sessions) * int(rows_per_session)
@@ -157,8 +177,8 @@ def fuse_verify(q: torch.Tensor, scale: torch.Tensor, h_end: Optional[torch.Tens
     need = fuse_verify_workspace(M, subset, mode)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    check(lib.sph_fuse_verify(
-        q.data_ptr(), scale.data_ptr(), hp, ldh, d_end, wp, ldw, subset.handle,
+    check(lib.sph_fuse_verify_fmt(
+        q.data_ptr(), scale.data_ptr(), int(bits), int(block), hp, ldh, d_end, wp, ldw, subset.handle,
         int(n_sessions), int(rows_per_session), _ptr(drafts),
         int(mode), float(temperature), float(top_p), int(seed) & 0xFFFFFFFFFFFFFFFF,
         tokens.data_ptr(), accept.data_ptr(), _ptr(fused),

@@ -167,7 +167,7 @@ struct GemvShape {
 template <int MR, int LPR, int UNR, int WT, int EPI>
 constexpr int gemv_waves() {
   if (UNR == 4) return MR <= 4 ? 6 : 4;
-  if (MR <= 2) return 6;
+  if (MR <= (EPI == kEpiFuse ? 1 : 2)) return 6;
   return (LPR == 64 && WT == 0 && EPI == kEpiCloud && MR <= 5) ? 6 : 4;
 }
 
@@ -256,7 +256,9 @@ void k_gemv(const GemvArgs a) {
   };
 
   // Epilogue operands of the values a lane owns in iteration it: the fp8
-  // row scale and the bias (cloud), or the payload code (fuse).  Every lane
+  // row scale and the bias (cloud), or the payload code and its scale
+  // (fuse; 8-bit codes are bytes, 4-bit codes nibbles, one scale per row or
+  // per row and block of 2^qshift positions).  Every lane
   // loads them, from index 0 where it has none, so the loads are
   // unconditional and go out with the item's first weight chunk: no load in
   // an epilogue makes the wave wait for the next item's weight loads.
@@ -278,9 +280,17 @@ void k_gemv(const GemvArgs a) {
         e.e1[i] = a.bias ? b : 0.0f;
       } else {
         const bool ok = own[i] && j < r1;
-        const int q = (int)a.q[ok ? (int64_t)own_m[i] * n + j : 0];
-        e.e0[i] = ok ? (float)q : 0.0f;
-        e.e1[i] = 0.0f;
+        const int64_t rq = (int64_t)own_m[i] * a.qstride;
+        const uint8_t byte = a.q[ok ? rq + (a.qbits == 8 ? j : (j >> 1)) : 0];
+        int code;
+        if (a.qbits == 8) {
+          code = (int)(int8_t)byte;
+        } else {
+          const int nib = (j & 1) ? (byte >> 4) : (byte & 15);
+          code = nib >= 8 ? nib - 16 : nib;
+        }
+        e.e0[i] = ok ? (float)code : 0.0f;
+        e.e1[i] = a.qscale[ok ? (int64_t)own_m[i] * a.qnb + (a.qshift < 0 ? 0 : (j >> a.qshift)) : 0];
       }
     }
   };
@@ -322,13 +332,6 @@ void k_gemv(const GemvArgs a) {
   for (int j = r0 + tid; j < r1; j += kBS) s_ids[j - r0] = a.ids[j];
   __syncthreads();
 
-  float qsc[PER];  // fuse: the payload row scale of each owned value
-#pragma unroll
-  for (int i = 0; i < PER; ++i) qsc[i] = 0.0f;
-  if constexpr (EPI == kEpiFuse) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) qsc[i] = a.qscale[own[i] ? own_m[i] : 0];
-  }
   float run_amax[PER];
   unsigned long long run_key[PER];
 #pragma unroll
@@ -395,7 +398,7 @@ void k_gemv(const GemvArgs a) {
         const float y = fminf(fmaxf(z, -a.clip), a.clip);
         run_amax[i] = fmaxf(run_amax[i], fabsf(y));
       } else {
-        const float f = __builtin_fmaf(e.e0[i], qsc[i], dot);
+        const float f = __builtin_fmaf(e.e0[i], e.e1[i], dot);
         if (a.f) a.f[(int64_t)m * n + j] = f;
         const unsigned long long key = argmax_key(f, j);
         run_key[i] = key > run_key[i] ? key : run_key[i];

@@ -162,32 +162,44 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
   const int wm = wave / WN, wn = wave % WN;
   const int M = a.M, n = a.n;
   if constexpr (EPI == kEpiFuse) {
-    const bool vec = (n & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
+    // the payload tile: BN codes of a row are BN * qbits / 8 bytes starting
+    // at byte n0 * qbits / 8 of the row
+    const int qb = a.qbits;
+    const int TB = BN * qb / 8;  // tile bytes per row
+    const int64_t c0 = (int64_t)n0 * qb / 8;
+    const int64_t rowbytes = ((int64_t)n * qb + 7) / 8;
+    const bool vec = (a.qstride & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
     if (vec) {
-      constexpr int CPR = BN / 16;  // 16-byte chunks per tile row
-      constexpr int PT = BM * CPR / NT;  // chunks per thread, all loaded before any is stored
-      static_assert(PT * NT == BM * CPR, "payload tile / threads");
+      // all of a thread's 16-byte chunks are loaded before any is stored
+      constexpr int PT = BM * (BN / 16) / NT;  // chunks per thread at 8 bits
+      static_assert(PT * NT == BM * (BN / 16), "payload tile / threads");
+      const int CPR = TB / 16;  // 16-byte chunks per tile row
       u32x4_t v[PT];
 #pragma unroll
       for (int t = 0; t < PT; ++t) {
         const int c = tid + t * NT, r = c / CPR, k = c % CPR;
-        const int row = m0 + r, col = n0 + k * 16;
-        v[t] = (row < M && col < n) ? *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)row * n + col)
-                                    : u32x4_t{0u, 0u, 0u, 0u};
+        const int row = m0 + r;
+        const int64_t col = c0 + k * 16;
+        v[t] = (r < BM && row < M && col < rowbytes)
+                   ? *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)row * a.qstride + col)
+                   : u32x4_t{0u, 0u, 0u, 0u};
       }
 #pragma unroll
       for (int t = 0; t < PT; ++t) {
         const int c = tid + t * NT, r = c / CPR, k = c % CPR;
-        *reinterpret_cast<u32x4_t*>(s_q + r * BN + k * 16) = v[t];
+        if (r < BM) *reinterpret_cast<u32x4_t*>(s_q + r * TB + k * 16) = v[t];
       }
     } else {
-      for (int c = tid; c < BM * BN; c += NT) {
-        const int r = c / BN, k = c % BN;
-        const int row = m0 + r, col = n0 + k;
-        s_q[c] = (row < M && col < n) ? a.q[(int64_t)row * n + col] : (int8_t)0;
+      for (int c = tid; c < BM * TB; c += NT) {
+        const int r = c / TB, k = c % TB;
+        const int row = m0 + r;
+        const int64_t col = c0 + k;
+        s_q[c] = (row < M && col < rowbytes) ? (int8_t)a.q[(int64_t)row * a.qstride + col] : (int8_t)0;
       }
     }
-    for (int r = tid; r < BM; r += NT) s_qs[r] = m0 + r < M ? a.qscale[m0 + r] : 0.0f;
+    // a tile lies in one block of positions (blocks are multiples of BN)
+    const int kb = a.qshift < 0 ? 0 : (n0 >> a.qshift);
+    for (int r = tid; r < BM; r += NT) s_qs[r] = m0 + r < M ? a.qscale[(int64_t)(m0 + r) * a.qnb + kb] : 0.0f;
     __syncthreads();
   }
   using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
@@ -214,7 +226,15 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
             __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
             best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
           } else {
-            const float f = __builtin_fmaf((float)s_q[lrow * BN + lcol], s_qs[lrow], dot);
+            int code;
+            if (a.qbits == 8) {
+              code = s_q[lrow * BN + lcol];
+            } else {
+              const int byte = (uint8_t)s_q[lrow * (BN / 2) + (lcol >> 1)];
+              const int nib = (lcol & 1) ? (byte >> 4) : (byte & 15);
+              code = nib >= 8 ? nib - 16 : nib;
+            }
+            const float f = __builtin_fmaf((float)code, s_qs[lrow], dot);
             if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
             const unsigned long long key = argmax_key_m(f, col);
             best = key > best ? key : best;

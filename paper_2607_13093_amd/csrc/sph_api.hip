@@ -105,6 +105,15 @@ hipError_t traced(const char* name, hipStream_t s, F&& body) {
   return e;
 }
 
+// log2(block) for a payload block of 256 ... 4096 positions (a power of two),
+// -1 for block 0 (one scale per row), -2 for anything else.
+int block_shift(int64_t block) {
+  if (block == 0) return -1;
+  for (int sh = 8; sh <= 12; ++sh)
+    if (block == (int64_t(1) << sh)) return sh;
+  return -2;
+}
+
 int make_plan(const int32_t* host_ids, int64_t n, int64_t vocab, hipStream_t stream,
               sph_subset* out) {
   int dev = 0;
@@ -207,12 +216,37 @@ size_t sph_fuse_verify_workspace(int64_t M, sph_subset subset, int mode) {
   return fuse_ws(M, subset->n, mode);
 }
 
+int64_t sph_payload_code_bytes(int64_t n_sub, int bits) {
+  if (n_sub < 0 || (bits != 8 && bits != 4)) return -1;
+  return (n_sub * bits + 7) / 8;
+}
+
+int64_t sph_payload_scale_count(int64_t n_sub, int64_t block) {
+  if (n_sub < 0 || block_shift(block) == -2) return -1;
+  return block == 0 ? 1 : std::max<int64_t>(1, (n_sub + block - 1) / block);
+}
+
 int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
                       const void* w_cloud, int64_t ldw, int wtype, const float* w_row_scale,
                       const float* bias, sph_subset subset, float clip_c, int8_t* q_out,
                       float* scale_out, float* z_out, void* workspace, size_t ws_bytes,
                       void* stream) {
+  return sph_cloud_partial_fmt(h_cloud, ldh, M, d_cloud, w_cloud, ldw, wtype, w_row_scale, bias,
+                               subset, clip_c, 8, 0, q_out, scale_out, z_out, workspace, ws_bytes,
+                               stream);
+}
+
+int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                          const void* w_cloud, int64_t ldw, int wtype, const float* w_row_scale,
+                          const float* bias, sph_subset subset, float clip_c, int bits,
+                          int64_t block, void* q_out, float* scale_out, float* z_out,
+                          void* workspace, size_t ws_bytes, void* stream) {
   const char* fn = "sph_cloud_partial";
+  if (bits != 8 && bits != 4) return fail(SPH_E_INVALID_ARG, "%s: bits=%d not 4 or 8", fn, bits);
+  const int qshift = block_shift(block);
+  if (qshift == -2)
+    return fail(SPH_E_INVALID_ARG, "%s: block=%lld not 0 or a power of two in [256, 4096]", fn,
+                (long long)block);
   if (M < 0 || M > (1 << 24)) return fail(SPH_E_INVALID_ARG, "%s: M=%lld out of range", fn, (long long)M);
   if (d_cloud < 0 || d_cloud > (1 << 20))
     return fail(SPH_E_INVALID_ARG, "%s: d_cloud=%lld out of range", fn, (long long)d_cloud);
@@ -300,8 +334,11 @@ int sph_cloud_partial(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_clo
       if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
     }
   }
+  const int64_t qstride = sph_payload_code_bytes(n, bits);
+  const int qnb = (int)sph_payload_scale_count(n, block);
   hipError_t e = traced("cloud_quantize", s, [&] {
-    return sph::launch_quantize(z, amax, nblk, (int)M, (int)n, clip_c, q_out, scale_out, s);
+    return sph::launch_quantize(z, amax, nblk, (int)M, (int)n, clip_c, bits, qshift,
+                                static_cast<uint8_t*>(q_out), qstride, scale_out, qnb, s);
   });
   if (e != hipSuccess) return hip_fail(e, "quantiser launch");
   return ok();
@@ -313,7 +350,24 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
                     float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
                     int32_t* accept_len_out, float* fused_out, void* workspace, size_t ws_bytes,
                     void* stream) {
+  return sph_fuse_verify_fmt(q, scale, 8, 0, h_end, ldh, d_end, w_end, ldw, subset, n_sessions,
+                             rows_per_session, drafts, mode, temperature, top_p, seed, tokens_out,
+                             accept_len_out, fused_out, workspace, ws_bytes, stream);
+}
+
+int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t block,
+                        const void* h_end, int64_t ldh, int64_t d_end, const void* w_end,
+                        int64_t ldw, sph_subset subset, int64_t n_sessions,
+                        int64_t rows_per_session, const int32_t* drafts, int mode,
+                        float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                        int32_t* accept_len_out, float* fused_out, void* workspace,
+                        size_t ws_bytes, void* stream) {
   const char* fn = "sph_fuse_verify";
+  if (bits != 8 && bits != 4) return fail(SPH_E_INVALID_ARG, "%s: bits=%d not 4 or 8", fn, bits);
+  const int qshift = block_shift(block);
+  if (qshift == -2)
+    return fail(SPH_E_INVALID_ARG, "%s: block=%lld not 0 or a power of two in [256, 4096]", fn,
+                (long long)block);
   if (n_sessions < 0 || rows_per_session < 1 || rows_per_session > 1024)
     return fail(SPH_E_INVALID_ARG, "%s: n_sessions=%lld / rows_per_session=%lld out of range", fn,
                 (long long)n_sessions, (long long)rows_per_session);
@@ -351,6 +405,8 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
   if (n > (int64_t)sph::kMaxBlocks * sph::kGemvMaxIdsPerBlock)
     return fail(SPH_E_UNSUPPORTED, "%s: subset of %lld ids is too large", fn, (long long)n);
   const int64_t Kp = round_up(d_end, 8);
+  const int64_t qstride = sph_payload_code_bytes(n, bits);
+  const int qnb = (int)sph_payload_scale_count(n, block);
 
   hipStream_t s = (hipStream_t)stream;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -371,8 +427,12 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
     a.ldw_bytes = ldw * 2;
     a.ids = subset->d_ids;
     a.n = (int)n;
-    a.q = q;
+    a.q = static_cast<const uint8_t*>(q);
+    a.qstride = qstride;
     a.qscale = scale;
+    a.qbits = bits;
+    a.qshift = qshift;
+    a.qnb = qnb;
     a.f = fused;
     a.best_part = best;
     hipError_t e = traced("fuse_mfma", s, [&] { return sph::launch_mfma(sph::kEpiFuse, 0, a, s); });
@@ -397,8 +457,12 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
       a.ids = subset->d_ids;
       a.n = (int)n;
       a.nblk = nblk;
-      a.q = q + m0 * n;
-      a.qscale = scale + m0;
+      a.q = static_cast<const uint8_t*>(q) + m0 * qstride;
+      a.qstride = qstride;
+      a.qscale = scale + m0 * qnb;
+      a.qbits = bits;
+      a.qshift = qshift;
+      a.qnb = qnb;
       a.f = fused ? fused + m0 * n : nullptr;
       a.best_part = best + m0 * sph::kMaxBlocks;
       hipError_t e = traced("fuse_gemv", s, [&] { return sph::launch_gemv(sph::kEpiFuse, 0, rows, a, s); });

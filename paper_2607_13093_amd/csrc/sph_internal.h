@@ -61,9 +61,12 @@ struct GemvArgs {
   float clip;
   float* z;               // fp32 [rows, n]
   float* amax_part;       // fp32 [rows, kMaxBlocks]
-  // fuse epilogue
-  const int8_t* q;        // int8 [rows, n]
-  const float* qscale;    // fp32 [rows]
+  // fuse epilogue: the payload in format (qbits, block of 2^qshift positions
+  // or one per row when qshift < 0)
+  const uint8_t* q;       // codes, rows of qstride bytes
+  int64_t qstride;
+  const float* qscale;    // fp32 [rows, qnb]
+  int qbits, qshift, qnb;
   float* f;               // fp32 [rows, n] or null
   uint64_t* best_part;    // argmax keys [rows, kMaxBlocks]
 };
@@ -85,9 +88,12 @@ struct MfmaArgs {
   float clip;
   float* z;               // fp32 [M, n]
   float* amax_part;       // fp32 [M, kMaxBlocks], slot = n-tile
-  // fuse epilogue
-  const int8_t* q;        // int8 [M, n]
-  const float* qscale;    // fp32 [M]
+  // fuse epilogue: the payload in format (qbits, block of 2^qshift >= 256
+  // positions or one per row when qshift < 0)
+  const uint8_t* q;       // codes, rows of qstride bytes
+  int64_t qstride;
+  const float* qscale;    // fp32 [M, qnb]
+  int qbits, qshift, qnb;
   float* f;               // fp32 [M, n] or null
   uint64_t* best_part;    // argmax keys [M, kMaxBlocks], slot = n-tile
 };
@@ -104,8 +110,13 @@ int gemv_lpr(int K, int wtype);
 hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s);
 int mfma_n_tiles(int n);
 
+// Clip + quantise z [M, n] to b-bit codes (bits 8 or 4; 4-bit codes two per
+// byte, low nibble first) with one scale per row (qshift < 0: from the
+// projection's per-block maxima amax_part) or per row and block of 2^qshift
+// positions (8 <= qshift <= 12).  q rows are qstride bytes, scale rows qnb.
 hipError_t launch_quantize(const float* z, const float* amax_part, int nblk, int M, int n,
-                           float clip, int8_t* q, float* scale, hipStream_t s);
+                           float clip, int bits, int qshift, uint8_t* q, int64_t qstride,
+                           float* scale, int qnb, hipStream_t s);
 
 // best/nblk: the endpoint projection's per-tile argmax keys of each row
 // (row stride kMaxBlocks), whose maximum gives the row's largest logit.

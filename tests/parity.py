@@ -67,14 +67,15 @@ class DeviceWorkload:
         else:
             self.subset = sph.Subset(wl.subset, vocab=cfg.vocab)
 
-    def cloud(self, rows=None, want_z=True):
+    def cloud(self, rows=None, want_z=True, bits=8, block=0):
         de = self.cfg.d_end
         h = self.h if rows is None else self.h[rows[0]:rows[1]]
         q, s, z = sph.cloud_partial(h[:, de:], self.w_cloud, self.subset, self.cfg.clip_c,
-                                    w_row_scale=self.w_scale, bias=self.bias, want_z=want_z)
+                                    w_row_scale=self.w_scale, bias=self.bias, want_z=want_z,
+                                    bits=bits, block=block)
         return q, s, z
 
-    def fuse(self, q, s, drafts, want_fused=True, n_sessions=None, h=None):
+    def fuse(self, q, s, drafts, want_fused=True, n_sessions=None, h=None, bits=8, block=0):
         cfg = self.cfg
         de = cfg.d_end
         h = self.h if h is None else h
@@ -83,7 +84,8 @@ class DeviceWorkload:
         mode = sph.GREEDY if cfg.mode == "greedy" else sph.SAMPLE
         return sph.fuse_verify(q, s, h[:, :de], self.w_end, self.subset, S,
                                cfg.rows_per_session, d, mode=mode, temperature=cfg.temperature,
-                               top_p=cfg.top_p, seed=cfg.philox_seed, want_fused=want_fused)
+                               top_p=cfg.top_p, seed=cfg.philox_seed, want_fused=want_fused,
+                               bits=bits, block=block)
 
 
 def host(t):
@@ -133,6 +135,50 @@ def stage_c(q_gpu, s_gpu, orc):
     return {"code_mismatch": int(mism.sum()), "code_exempt": int(exempt.sum()), "codes": int(dq.size)}
 
 
+def stage_b_fmt(z_gpu, payload_gpu, s_gpu, clip_c, bits, block):
+    """Stage B for a payload format: the oracle's quantiser of the GPU's own
+    partials, packed, must equal the GPU's payload byte for byte (padding
+    nibble included) and its scales bit for bit.  Returns the GPU codes."""
+    ref = oracle.clip_quantize_fmt(z_gpu, clip_c, bits, block)
+    M, n = z_gpu.shape
+    np.testing.assert_array_equal(ref["scale"].view(np.uint32), s_gpu.reshape(M, -1).view(np.uint32),
+                                  err_msg="stage B: scales differ from the quantiser applied to the GPU partials")
+    np.testing.assert_array_equal(oracle.pack_codes(ref["q"], bits), payload_gpu,
+                                  err_msg="stage B: payload bytes differ from the packed oracle codes")
+    return oracle.unpack_codes(payload_gpu, n, bits)
+
+
+def stage_c_fmt(q_gpu, s_gpu, orc_fmt, absdot, block):
+    """Stage C for a payload format (q_gpu: unpacked codes).  A block's
+    maximum moves by at most the largest tolerance of its elements, so its
+    scale by that much over qmax."""
+    tol = tol_of(absdot)
+    y, t = orc_fmt["y"], orc_fmt["t"].astype(np.float64)
+    a, s = orc_fmt["amax"].astype(np.float64), orc_fmt["scale"].astype(np.float64)
+    M, n = y.shape
+    nb = a.shape[1]
+    width = n if block == 0 else block
+    tol_a = np.zeros((M, nb))
+    for k in range(nb):
+        seg = tol[:, k * width:(k + 1) * width]
+        if seg.shape[1]:
+            tol_a[:, k] = seg.max(axis=1)
+    cols = block_cols(n, block)
+    dq = np.abs(q_gpu.astype(np.int32) - orc_fmt["q"].astype(np.int32))
+    assert dq.max(initial=0) <= 1, "stage C: a code differs by more than one step"
+    with np.errstate(divide="ignore", invalid="ignore"):
+        rel = tol_a / a
+        bound = (tol + np.abs(y) * rel[:, cols]) / s[:, cols]
+        dist = np.abs(t - np.floor(t) - 0.5)
+        exempt = (dist <= bound) | (a[:, cols] == 0)
+        ds = np.abs(s_gpu.reshape(M, nb).astype(np.float64) - s)
+        ok_s = (ds <= s * rel + s * ULP) | (a == 0)
+    assert ok_s.all(), "stage C: scale outside the propagated tolerance"
+    mism = dq > 0
+    assert not (mism & ~exempt).any(), f"stage C: {int((mism & ~exempt).sum())} non-exempt code mismatches"
+    return {"code_mismatch": int(mism.sum()), "code_exempt": int(exempt.sum()), "codes": int(dq.size)}
+
+
 def exempt_rows(f_ref, bound):
     """Rows whose argmax may legitimately move: some competitor j lies within
     bound[j*] + bound[j] of the reference maximum f_ref[j*]."""
@@ -158,12 +204,24 @@ def check_tokens_and_accept(tok_gpu, acc_gpu, ref_tok, ref_acc, exempt, subset, 
     return {"token_mismatch": int((tok_gpu != ref_tok).sum()), "token_exempt_rows": int(exempt.sum())}
 
 
-def stage_d_greedy(q_gpu, s_gpu, f_gpu, tok_gpu, acc_gpu, wl, drafts, rows=None):
+def block_cols(n, block):
+    """Scale index of every subset position: 0 for one scale per row."""
+    return np.zeros(n, np.int64) if block == 0 else np.arange(n) // block
+
+
+def _fuse(q, s, z_e, block):
+    if s.ndim == 1:
+        return oracle.fuse_masked(q, s, z_e)
+    return oracle.fuse_masked_fmt(q, s, z_e, block)
+
+
+def stage_d_greedy(q_gpu, s_gpu, f_gpu, tok_gpu, acc_gpu, wl, drafts, rows=None, block=0):
+    """q_gpu: int8 codes [M, n]; s_gpu: scales [M] (one per row) or [M, nb]."""
     cfg = wl.cfg
     h = wl.h_bits if rows is None else wl.h_bits[rows[0]:rows[1]]
     S = h.shape[0] // cfg.rows_per_session
     z_e, absdot = oracle.endpoint_partial_logits(h, cfg.d_end, wl.subset, wl.w_end_bits, with_abs=True)
-    f_ref = oracle.fuse_masked(q_gpu, s_gpu, z_e)
+    f_ref = _fuse(q_gpu, s_gpu, z_e, block)
     bound = tol_of(absdot) + ULP * np.abs(f_ref.astype(np.float64))
     if f_gpu is not None:
         df = np.abs(f_gpu.astype(np.float64) - f_ref.astype(np.float64))
@@ -175,17 +233,21 @@ def stage_d_greedy(q_gpu, s_gpu, f_gpu, tok_gpu, acc_gpu, wl, drafts, rows=None)
                                    cfg.rows_per_session)
 
 
-def stage_e_greedy(q_gpu, s_gpu, tok_gpu, acc_gpu, orc_cloud, wl, drafts, rows=None):
+def stage_e_greedy(q_gpu, s_gpu, tok_gpu, acc_gpu, orc_cloud, wl, drafts, rows=None, block=0):
     cfg = wl.cfg
     h = wl.h_bits if rows is None else wl.h_bits[rows[0]:rows[1]]
     S = h.shape[0] // cfg.rows_per_session
     z_e, absdot = oracle.endpoint_partial_logits(h, cfg.d_end, wl.subset, wl.w_end_bits, with_abs=True)
-    f_ref = oracle.fuse_masked(orc_cloud["q"], orc_cloud["scale"], z_e)
+    f_ref = _fuse(orc_cloud["q"], orc_cloud["scale"], z_e, block)
     ref_tok, _, _ = oracle.greedy_select(f_ref, wl.subset)
     ref_acc = oracle.accept_lengths(ref_tok, drafts, S, cfg.rows_per_session)
-    s_ref = orc_cloud["scale"].astype(np.float64)[:, None]
+    # scales per subset position
+    cols = block_cols(q_gpu.shape[1], block)
+    s_o = orc_cloud["scale"].astype(np.float64).reshape(q_gpu.shape[0], -1)
+    s_g = s_gpu.astype(np.float64).reshape(q_gpu.shape[0], -1)
+    s_ref = s_o[:, cols]
     dq = np.abs(q_gpu.astype(np.float64) - orc_cloud["q"].astype(np.float64))
-    ds = np.abs(s_gpu.astype(np.float64) - orc_cloud["scale"].astype(np.float64))[:, None]
+    ds = np.abs(s_g - s_o)[:, cols]
     bound = (dq * s_ref + np.abs(q_gpu.astype(np.float64)) * ds + tol_of(absdot)
              + ULP * np.abs(f_ref.astype(np.float64)))
     ex = exempt_rows(f_ref, bound)

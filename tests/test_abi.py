@@ -131,6 +131,49 @@ def test_fuse_verify_validation(lib, kw, msg):
     assert msg in lib.sph_last_error().decode()
 
 
+@pytest.mark.parametrize("bits,block,msg", [
+    (2, 0, "bits=2"),
+    (16, 0, "bits=16"),
+    (8, 128, "block=128"),
+    (4, 300, "block=300"),
+    (4, 8192, "block=8192"),
+    (8, -256, "block=-256"),
+])
+def test_payload_format_validation(lib, bits, block, msg):
+    # both halves reject a payload format they do not implement, before any
+    # other argument is looked at
+    rc = lib.sph_cloud_partial_fmt(1, 64, 3, 64, 16, 64, _lib.SPH_W_BF16, None, None, None, 30.0,
+                                   bits, block, 1, 1, None, 1, 0, None)
+    assert rc == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+    rc = lib.sph_fuse_verify_fmt(1, 1, bits, block, 1, 64, 64, 16, 64, None, 2, 3, 1,
+                                 _lib.SPH_GREEDY, 1.0, 1.0, 0, 1, 1, None, 1, 0, None)
+    assert rc == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+
+
+@pytest.mark.parametrize("n,bits,block,code_bytes,scales", [
+    (0, 8, 0, 0, 1),
+    (1, 4, 256, 1, 1),
+    (5, 4, 0, 3, 1),
+    (49153, 8, 0, 49153, 1),
+    (49153, 4, 1024, 24577, 49),
+    (4096, 4, 4096, 2048, 1),
+    (4097, 8, 4096, 4097, 2),
+])
+def test_payload_sizes(lib, n, bits, block, code_bytes, scales):
+    # eq. 21: ceil(n * b / 8) code bytes plus the scales of the row
+    assert lib.sph_payload_code_bytes(n, bits) == code_bytes
+    assert lib.sph_payload_scale_count(n, block) == scales
+
+
+def test_payload_sizes_reject(lib):
+    assert lib.sph_payload_code_bytes(5, 3) == -1
+    assert lib.sph_payload_code_bytes(-1, 8) == -1
+    assert lib.sph_payload_scale_count(5, 300) == -1
+    assert lib.sph_payload_scale_count(-5, 0) == -1
+
+
 def test_error_string_is_thread_local(lib):
     import threading
     assert _cloud(lib, M=-1) == _lib.SPH_E_INVALID_ARG
