@@ -6,7 +6,8 @@ partial, dequantise + fuse + mask, greedy select, accepted draft prefix).
 
 Default workload: single-session decode, d=4096, d_end=256, V=128256, a
 49152-id language subset (one block of 32768 ids plus 16384 scattered ids),
-1 session x 5 rows (k=4 drafts), bf16 h/W, clip 30, int8 payload.
+1 session x 5 rows (k=4 drafts), bf16 h/W, clip 30, int8 payload with one
+scale per row (--bits / --block choose another payload format).
 
 Prints ONE JSON line.  `value` is rows*vocab/s = M*|S| / (seconds per step)
 with every input resident in HBM before the timed region; three copies of
@@ -39,6 +40,10 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default="decode")
+    p.add_argument("--bits", type=int, default=8, choices=(4, 8),
+                   help="payload code width b (eq. 18)")
+    p.add_argument("--block", type=int, default=0,
+                   help="payload scale block: 0 = one scale per row, else 256..4096 positions")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the oracle's CPU baseline run (0 to skip)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -211,8 +216,13 @@ def main():
     mode = sph.GREEDY if cfg.mode == "greedy" else sph.SAMPLE
     M, de = cfg.M, cfg.d_end
     h_c, h_e = h[:, de:], h[:, :de]
-    q = torch.empty((M, n), dtype=torch.int8, device=dev)
-    s = torch.empty((M,), dtype=torch.float32, device=dev)
+    bits, block = args.bits, args.block
+    code_bytes = sph.payload_code_bytes(n, bits)
+    nb = sph.payload_scale_count(n, block)
+    if code_bytes < 0 or nb < 0:
+        raise SystemExit(f"unsupported payload format bits={bits} block={block}")
+    q = torch.empty((M, code_bytes), dtype=torch.int8 if bits == 8 else torch.uint8, device=dev)
+    s = torch.empty((M,) if block == 0 else (M, nb), dtype=torch.float32, device=dev)
     tok = torch.empty((M,), dtype=torch.int32, device=dev)
     acc = torch.empty((cfg.sessions,), dtype=torch.int32, device=dev)
     ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
@@ -222,11 +232,11 @@ def main():
     def step(i):
         c = i % N_COPIES
         sph.cloud_partial(h_c, wc[c], sub, cfg.clip_c, w_row_scale=wsc, workspace=ws_c,
-                          out=(q, s, None))
+                          out=(q, s, None), bits=bits, block=block)
         sph.fuse_verify(q, s, h_e, we[c], sub, cfg.sessions, cfg.rows_per_session,
                         drafts if cfg.k else None, mode=mode, temperature=cfg.temperature,
                         top_p=cfg.top_p, seed=cfg.philox_seed, workspace=ws_f,
-                        out=(tok, acc, None))
+                        out=(tok, acc, None), bits=bits, block=block)
 
     # drafts: a fair coin between the GPU's own token for the row and a random subset id
     step(0)
@@ -309,7 +319,9 @@ def main():
                         f"{cfg.mode} clip={cfg.clip_c}",
             "rows": M,
             "subset": n,
-            "payload_bytes_per_row": n + 4,
+            "payload": f"b={bits} " + ("one scale per row" if block == 0 else
+                                       f"one scale per {block} positions"),
+            "payload_bytes_per_row": code_bytes + 4 * nb,
         },
         "roofline": roof,
         "attainable": att,
