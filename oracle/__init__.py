@@ -24,6 +24,8 @@ from .split_head import (  # noqa: F401
     unpack_codes,
     payload_bytes,
     endpoint_partial_logits,
+    hidden_quantize,
+    endpoint_partial_logits_hq,
     fuse_masked,
     fuse_masked_fmt,
     round_sum_to_f32,

@@ -285,6 +285,72 @@ def endpoint_partial_logits(h_bits, d_end, subset, w_end_bits, rows=None, with_a
 
 
 # ---------------------------------------------------------------------------
+# Section 5.3: the returned hidden state is quantised before it leaves the
+# cloud; eq. 11 then runs on the dequantised values
+# ---------------------------------------------------------------------------
+
+
+def hidden_quantize(h_bits):
+    """Per-row int8 quantisation of returned hidden states.
+
+    Section 5.3 quantises (and encrypts) every tensor the cloud returns, the
+    hidden state included, with the Q_b of eq. 18.  Reading (b = 8, the
+    logit rule of clip_quantize without a clip, since the hidden state has
+    no natural range):
+        x = bf16 value (exact in fp32)
+        a = max_i |x[m, i]|                    (exact)
+        s = fp32(a / 127), 0 if a = 0          (correctly rounded)
+        t = fp32(x / s)                        (correctly rounded)
+        q = clamp(rint_half_even(t), -127, 127), 0 where s = 0
+    Returns (q int8 [M, d], s fp32 [M]).
+    Pinned by: a row whose maximum is 127 (s = 1, q = rint(x), ties to
+    even), |q*s - x| <= s/2, +-127 at every row maximum, a zero row, and
+    agreement with clip_quantize for a clip above every |x|.
+    """
+    x = decode_bf16(np.asarray(h_bits)).astype(np.float32)
+    M = x.shape[0]
+    if x.shape[1] == 0:
+        return np.zeros(x.shape, np.int8), np.zeros(M, np.float32)
+    amax = np.abs(x).max(axis=1)
+    scale = (amax / np.float32(127.0)).astype(np.float32)
+    pos = scale > 0
+    t = np.zeros_like(x)
+    np.divide(x, scale[:, None], out=t, where=pos[:, None])
+    q = np.clip(np.rint(t), -127, 127).astype(np.int8)
+    q[~pos] = 0
+    return q, scale
+
+
+def endpoint_partial_logits_hq(hq, h_scale, d_end, subset, w_end_bits, with_abs=False,
+                               chunk=8192):
+    """z_end[m, j] = fp32( sum_{i < D_end} (q[m, i] * s_m) * W_end[S_j, i] ).
+
+    Eq. 11 on the endpoint's dequantised hidden state (the codes of
+    hidden_quantize and their row scale; only the first D_end columns enter
+    the sum).  q * s is exact in fp64; fp64 accumulation, one rounding.
+    Returns (z_end fp32 [M, n], absdot = sum |q s| |W| or None).
+    Pinned by: equality with endpoint_partial_logits when every q * s is a
+    bf16 value (rows with s = 1 and s = 2^-3), and a hand-worked example.
+    """
+    q = np.asarray(hq, dtype=np.int8)[:, :d_end].astype(np.float64)
+    s = np.asarray(h_scale, dtype=np.float32).astype(np.float64)
+    H = q * s[:, None]
+    subset = np.asarray(subset, dtype=np.int64)
+    n = subset.size
+    z = np.zeros((H.shape[0], n), dtype=np.float32)
+    absdot = np.zeros((H.shape[0], n), dtype=np.float64) if with_abs else None
+    if d_end == 0:
+        return z, absdot
+    for j0 in range(0, n, chunk):
+        ids = subset[j0:j0 + chunk]
+        W = decode_bf16(np.asarray(w_end_bits)[ids])
+        z[:, j0:j0 + len(ids)] = _to_f32(H @ W.T)
+        if with_abs:
+            absdot[:, j0:j0 + len(ids)] = np.abs(H) @ np.abs(W).T
+    return z, absdot
+
+
+# ---------------------------------------------------------------------------
 # eq. 13-14: dequantise, fuse, mask
 # ---------------------------------------------------------------------------
 

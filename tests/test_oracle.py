@@ -224,6 +224,82 @@ def test_quantizer_rounds_half_to_even():
     np.testing.assert_array_equal(out["q"][0], [127, 2, 4, -2, -4, 0, 2, 126])
 
 
+# ---------------------------------------------------------------------------
+# hidden-state quantisation (Section 5.3 with eq. 18) and eq. 11 on it
+# ---------------------------------------------------------------------------
+
+def _bf(x):
+    return f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
+
+
+def test_hidden_quantize_unit_scale_row():
+    # a row whose largest |x| is 127 has s = 1, so the codes are rint(x)
+    # (ties to even); a second row of zeros has s = 0 and zero codes
+    h = _bf([[127, -1.5, 2.5, 0.25, -127, 3.5, -0.5, 126.5],
+             [0, 0, 0, 0, 0, 0, 0, 0]])
+    q, s = oracle.hidden_quantize(h)
+    assert s[0] == 1.0 and s[1] == 0.0
+    np.testing.assert_array_equal(q[0], [127, -2, 2, 0, -127, 4, 0, 126])
+    assert not q[1].any()
+
+
+def test_hidden_quantize_invariants():
+    rng = np.random.default_rng(12)
+    x = (rng.standard_normal((12, 700)) * rng.uniform(0.01, 50, (12, 1))).astype(np.float32)
+    x[3, 17] = 900.0    # an outlier sets its row's scale
+    h = _bf(x)
+    xv = oracle.decode_bf16(h)
+    q, s = oracle.hidden_quantize(h)
+    qi = q.astype(np.int32)
+    assert np.all(np.abs(qi) <= 127)
+    # t = fp32(x / s) is within ulp(t)/2 <= 2^-18 of x / s for |t| < 128,
+    # so |q - x/s| <= 1/2 + 2^-18
+    err = np.abs(qi * s[:, None].astype(np.float64) - xv)
+    assert np.all(err <= s[:, None].astype(np.float64) * (0.5 + 2 ** -18))
+    at = np.argmax(np.abs(xv), axis=1)
+    assert np.all(np.abs(qi[np.arange(12), at]) == 127)
+    assert np.all(np.sign(qi) * np.sign(xv) >= 0)
+    assert s[3] == np.float32(np.float32(900.0) / np.float32(127.0))
+    # with a clip above every |x| the logit quantiser gives the same codes and scales
+    ref = oracle.clip_quantize(xv.astype(np.float32), 1e30)
+    np.testing.assert_array_equal(ref["q"], q)
+    np.testing.assert_array_equal(ref["scale"], s)
+
+
+def test_endpoint_partial_hq_hand_example():
+    # codes [2, -3] with s = 0.5 are the values [1, -1.5]; ids 0 and 1 of
+    # W_end are [1, 1] and [2, -1]: z = [1 - 1.5, 2 + 1.5]; a third code
+    # column lies beyond d_end and must not enter the sum
+    hq = np.array([[2, -3, 99]], dtype=np.int8)
+    w = _bf([[1, 1], [2, -1], [5, 5]])
+    z, a = oracle.endpoint_partial_logits_hq(hq, np.array([0.5], np.float32), 2, [0, 1], w,
+                                             with_abs=True)
+    np.testing.assert_array_equal(z, [[-0.5, 3.5]])
+    np.testing.assert_array_equal(a, [[2.5, 3.5]])
+
+
+def test_endpoint_partial_hq_equals_bf16_partial_when_exact():
+    # rows whose dequantised values are bf16 numbers: integers with maximum
+    # 127 (s = 1) and integers / 8 with maximum 127 / 8 (s = 2^-3); the
+    # endpoint partial on the codes must equal eq. 11 on those values, row
+    # by row (two scales in one call)
+    rng = np.random.default_rng(13)
+    d, d_end = 96, 64
+    ints = rng.integers(-127, 128, size=(2, d)).astype(np.float32)
+    ints[:, 5] = 127
+    x = ints.copy()
+    x[1] /= 8
+    h = _bf(x)
+    q, s = oracle.hidden_quantize(h)
+    assert s[0] == 1.0 and s[1] == 0.125
+    np.testing.assert_array_equal(q.astype(np.float32), ints)
+    w = _bf(rng.standard_normal((300, d_end)).astype(np.float32) / 8)
+    S = np.sort(rng.choice(300, 77, replace=False))
+    z_hq, _ = oracle.endpoint_partial_logits_hq(q, s, d_end, S, w)
+    z_ref, _ = oracle.endpoint_partial_logits(h, d_end, S, w)
+    np.testing.assert_array_equal(z_hq, z_ref)
+
+
 def test_clip_and_zero_rows():
     cfg = Config("t", 0, d=512, d_end=64, vocab=8192, n_sub=4096, subset_kind="perm",
                  sessions=1, rows_per_session=3)
@@ -299,6 +375,11 @@ def test_format_fuse_per_row_equals_fuse_masked_and_uses_block_scales():
     f = oracle.fuse_masked_fmt(q, s, ze, 256)
     j = 513                                         # third block
     assert f[1, j] == np.float32(float(q[1, j]) * float(s[1, 2]) + float(ze[1, j]))
+    # hand example: unit codes, zero partials, blocks of 2 with scales 1, 2, 4
+    # (the last block holds one position)
+    f = oracle.fuse_masked_fmt(np.ones((1, 5), np.int8), np.float32([[1, 2, 4]]),
+                               np.zeros((1, 5), np.float32), 2)
+    np.testing.assert_array_equal(f[0], [1, 1, 2, 2, 4])
 
 
 # ---------------------------------------------------------------------------
