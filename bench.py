@@ -44,6 +44,9 @@ def parse():
                    help="payload code width b (eq. 18)")
     p.add_argument("--block", type=int, default=0,
                    help="payload scale block: 0 = one scale per row, else 256..4096 positions")
+    p.add_argument("--hidden-int8", action="store_true",
+                   help="the cloud also quantises the whole hidden row to int8 codes and the "
+                        "endpoint projects from them (sph_hidden_quantize + sph_fuse_verify_hq)")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the oracle's CPU baseline run (0 to skip)")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -227,12 +230,24 @@ def main():
     acc = torch.empty((cfg.sessions,), dtype=torch.int32, device=dev)
     ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
     ws_f = torch.empty(max(1, sph.fuse_verify_workspace(M, sub, mode)), dtype=torch.uint8, device=dev)
+    hq = torch.empty((M, cfg.d), dtype=torch.int8, device=dev)
+    hs = torch.empty((M,), dtype=torch.float32, device=dev)
+    if args.hidden_int8:
+        ws_f = torch.empty(max(1, sph.fuse_verify_hq_workspace(M, de, sub, mode)), dtype=torch.uint8,
+                           device=dev)
     drafts = torch.zeros((cfg.sessions, max(cfg.k, 1)), dtype=torch.int32, device=dev)
 
     def step(i):
         c = i % N_COPIES
         sph.cloud_partial(h_c, wc[c], sub, cfg.clip_c, w_row_scale=wsc, workspace=ws_c,
                           out=(q, s, None), bits=bits, block=block)
+        if args.hidden_int8:
+            sph.hidden_quantize(h, out=(hq, hs))
+            sph.fuse_verify_hq(q, s, hq, hs, de, we[c], sub, cfg.sessions, cfg.rows_per_session,
+                               drafts if cfg.k else None, mode=mode, temperature=cfg.temperature,
+                               top_p=cfg.top_p, seed=cfg.philox_seed, workspace=ws_f,
+                               out=(tok, acc, None), bits=bits, block=block)
+            return
         sph.fuse_verify(q, s, h_e, we[c], sub, cfg.sessions, cfg.rows_per_session,
                         drafts if cfg.k else None, mode=mode, temperature=cfg.temperature,
                         top_p=cfg.top_p, seed=cfg.philox_seed, workspace=ws_f,
@@ -322,6 +337,7 @@ def main():
             "payload": f"b={bits} " + ("one scale per row" if block == 0 else
                                        f"one scale per {block} positions"),
             "payload_bytes_per_row": code_bytes + 4 * nb,
+            "hidden_state": "int8 codes + fp32 scale per row" if args.hidden_int8 else "bf16",
         },
         "roofline": roof,
         "attainable": att,

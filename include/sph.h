@@ -215,6 +215,41 @@ int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t blo
                         size_t ws_bytes, void* stream);
 
 /*
+ * Hidden-state codes (Section 5.3: every tensor the cloud returns, the hidden
+ * state included, is quantised with the Q_b of eq. 18 before it is sent).
+ * Format: int8 codes with one fp32 scale per row,
+ *   a_m = max_i |x[m, i]| over the row's d values (bf16, exact in fp32),
+ *   s_m = fp32(a_m / 127) (0 for an all-zero row),
+ *   q[m, i] = clamp(rint_half_even(fp32(x[m, i] / s_m)), -127, 127), 0 if s_m = 0.
+ * The endpoint's projection (eq. 11) then runs on the dequantised values
+ * q * s; it computes s_m * sum_i q[m, i] W_end[S_j, i] in fp32, which equals
+ * the sum over q * s up to the order of the fp32 additions.
+ */
+
+/* Quantise M bf16 rows h [M, ldh] (first d columns; d = the full hidden row
+ * when the whole state is returned) into q_out int8 [M, ldq] and scale_out
+ * fp32 [M].  ldh, ldq >= d.  Device pointers, caller-owned; enqueues one
+ * kernel on `stream`.  d = 0 gives scales 0. */
+int sph_hidden_quantize(const void* h, int64_t ldh, int64_t M, int64_t d, int8_t* q_out,
+                        int64_t ldq, float* scale_out, void* stream);
+
+/* Workspace of sph_fuse_verify_hq: that of sph_fuse_verify plus, for more
+ * than 8 rows, M * round_up(d_end, 8) bf16 operands. */
+size_t sph_fuse_verify_hq_workspace(int64_t M, int64_t d_end, sph_subset subset, int mode);
+
+/* sph_fuse_verify_fmt with the endpoint's hidden state as codes: hq int8
+ * [M, ldhq] (its first d_end columns enter eq. 11) and h_scale fp32 [M], as
+ * written by sph_hidden_quantize.  ldhq >= d_end; every other argument and
+ * all outputs as in sph_fuse_verify_fmt. */
+int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t block,
+                       const int8_t* hq, int64_t ldhq, const float* h_scale, int64_t d_end,
+                       const void* w_end, int64_t ldw, sph_subset subset, int64_t n_sessions,
+                       int64_t rows_per_session, const int32_t* drafts, int mode,
+                       float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                       int32_t* accept_len_out, float* fused_out, void* workspace,
+                       size_t ws_bytes, void* stream);
+
+/*
  * Kernel tracing.  While a trace is active, each call records one duration
  * per kernel it launches: start and stop HIP events are attached to the
  * kernel dispatches themselves (hipExtLaunchKernelGGL), so a duration is

@@ -15,6 +15,9 @@ from .api import (  # noqa: F401
     fuse_verify,
     fuse_verify_workspace,
     payload_code_bytes,
+    hidden_quantize,
+    fuse_verify_hq,
+    fuse_verify_hq_workspace,
     payload_scale_count,
     probe_mfma,
     probe_read,

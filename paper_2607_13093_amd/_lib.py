@@ -56,6 +56,18 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_uint64,  # mode, temperature, top_p, seed
         c_vp, c_vp, c_vp,                   # tokens_out, accept_len_out, fused_out
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_hidden_quantize": (ctypes.c_int, [
+        c_vp, c_i64, c_i64, c_i64,          # h, ldh, M, d
+        c_vp, c_i64, c_vp, c_vp]),          # q_out, ldq, scale_out, stream
+    "sph_fuse_verify_hq_workspace": (ctypes.c_size_t, [c_i64, c_i64, c_vp, ctypes.c_int]),
+    "sph_fuse_verify_hq": (ctypes.c_int, [
+        c_vp, c_vp, ctypes.c_int, c_i64,    # q, scale, bits, block
+        c_vp, c_i64, c_vp, c_i64,           # hq, ldhq, h_scale, d_end
+        c_vp, c_i64, c_vp,                  # w_end, ldw, subset
+        c_i64, c_i64, c_vp,                 # n_sessions, rows_per_session, drafts
+        ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_uint64,  # mode, temperature, top_p, seed
+        c_vp, c_vp, c_vp,                   # tokens_out, accept_len_out, fused_out
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
     "sph_trace_start": (ctypes.c_int, [ctypes.c_int]),
     "sph_trace_stop": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
     # include/sph_probe.h

@@ -186,6 +186,67 @@ def fuse_verify(q: torch.Tensor, scale: torch.Tensor, h_end: Optional[torch.Tens
     return tokens, accept, fused
 
 
+def hidden_quantize(h: torch.Tensor, out=None):
+    """Per-row int8 codes of bf16 hidden rows h [M, d] (rows may be strided):
+    returns (codes int8 [M, d], scales fp32 [M])."""
+    lib = _lib.load()
+    _require_gpu("h", h)
+    h = _as_bits16(h)
+    M, d = h.shape
+    if out is None:
+        hq = torch.empty((M, d), dtype=torch.int8, device=h.device)
+        hs = torch.empty((M,), dtype=torch.float32, device=h.device)
+    else:
+        hq, hs = out
+    check(lib.sph_hidden_quantize(h.data_ptr(), h.stride(0) if M > 0 else d, M, d, hq.data_ptr(),
+                                  hq.stride(0) if M > 0 else d, hs.data_ptr(),
+                                  _stream_handle(h.device)))
+    return hq, hs
+
+
+def fuse_verify_hq_workspace(M: int, d_end: int, subset: Subset, mode: int = GREEDY) -> int:
+    return int(_lib.load().sph_fuse_verify_hq_workspace(int(M), int(d_end), subset.handle, int(mode)))
+
+
+def fuse_verify_hq(q: torch.Tensor, scale: torch.Tensor, hq: torch.Tensor, h_scale: torch.Tensor,
+                   d_end: int, w_end: Optional[torch.Tensor], subset: Subset, n_sessions: int,
+                   rows_per_session: int, drafts: Optional[torch.Tensor], mode: int = GREEDY,
+                   temperature: float = 1.0, top_p: float = 1.0, seed: int = 0,
+                   want_fused: bool = False, workspace: Optional[torch.Tensor] = None, out=None,
+                   bits: int = 8, block: int = 0):
+    """Endpoint half on hidden-state codes: hq int8 [M, >= d_end] and h_scale
+    fp32 [M] from hidden_quantize; the first d_end columns enter eq. 11.
+    Returns (tokens int32 [M], accept_len int32 [S], fused fp32 or None)."""
+    lib = _lib.load()
+    dev = q.device
+    M = int(n_sessions) * int(rows_per_session)
+    d_end = int(d_end)
+    if d_end > 0:
+        _require_gpu("hq", hq)
+        _require_gpu("w_end", w_end)
+        w_end = _as_bits16(w_end)
+        hp, ldh, sp = hq.data_ptr(), hq.stride(0), h_scale.data_ptr()
+        wp, ldw = w_end.data_ptr(), w_end.stride(0)
+    else:
+        hp, ldh, sp, wp, ldw = None, 0, None, None, 0
+    if out is None:
+        tokens = torch.empty((M,), dtype=torch.int32, device=dev)
+        accept = torch.empty((int(n_sessions),), dtype=torch.int32, device=dev)
+        fused = torch.empty((M, subset.n), dtype=torch.float32, device=dev) if want_fused else None
+    else:
+        tokens, accept, fused = out
+    need = fuse_verify_hq_workspace(M, d_end, subset, mode)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_fuse_verify_hq(
+        q.data_ptr(), scale.data_ptr(), int(bits), int(block), hp, ldh, sp, d_end, wp, ldw,
+        subset.handle, int(n_sessions), int(rows_per_session), _ptr(drafts),
+        int(mode), float(temperature), float(top_p), int(seed) & 0xFFFFFFFFFFFFFFFF,
+        tokens.data_ptr(), accept.data_ptr(), _ptr(fused),
+        workspace.data_ptr(), workspace.numel(), _stream_handle(dev)))
+    return tokens, accept, fused
+
+
 def trace_start(capacity: int) -> None:
     """Record HIP events around the next `capacity` kernel launches."""
     check(_lib.load().sph_trace_start(int(capacity)))

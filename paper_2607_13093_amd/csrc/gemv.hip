@@ -183,6 +183,7 @@ void k_gemv(const GemvArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ uint32_t s_amax[MR];
   __shared__ unsigned long long s_best[MR];
+  __shared__ float s_hsc[MR];  // fuse: row factors of int8 hidden-state codes
 
   const int Kp = a.Kp;
   uint16_t* hs = reinterpret_cast<uint16_t*>(smem);
@@ -315,7 +316,16 @@ void k_gemv(const GemvArgs a) {
     s_best[tid] = 0ull;
   }
   // Stage h[0:MR, 0:K] into LDS, zero padded to Kp, and this block's ids.
-  if ((reinterpret_cast<uintptr_t>(a.h) & 15) == 0 && (a.ldh & 7) == 0 && (a.K & 7) == 0) {
+  // int8 hidden-state codes are staged as bf16 (exact: at most 8 significant
+  // bits) and their row scales applied to the dot products in the epilogue.
+  if (EPI == kEpiFuse && a.hq) {
+    for (int idx = tid; idx < MR * Kp; idx += kBS) {
+      const int m = idx / Kp, k = idx - m * Kp;
+      hs[idx] = k < a.K ? (uint16_t)(__float_as_uint((float)a.hq[(int64_t)m * a.ldhq + k]) >> 16)
+                        : (uint16_t)0;
+    }
+    if (tid < MR) s_hsc[tid] = a.hscale[tid];
+  } else if ((reinterpret_cast<uintptr_t>(a.h) & 15) == 0 && (a.ldh & 7) == 0 && (a.K & 7) == 0) {
     const int vpr = Kp / 8;  // 16-byte vectors per staged row
     for (int idx = tid; idx < MR * vpr; idx += kBS) {
       const int m = idx / vpr, c = idx - m * vpr;
@@ -398,7 +408,8 @@ void k_gemv(const GemvArgs a) {
         const float y = fminf(fmaxf(z, -a.clip), a.clip);
         run_amax[i] = fmaxf(run_amax[i], fabsf(y));
       } else {
-        const float f = __builtin_fmaf(e.e0[i], e.e1[i], dot);
+        const float ze = a.hscale ? dot * s_hsc[m] : dot;
+        const float f = __builtin_fmaf(e.e0[i], e.e1[i], ze);
         if (a.f) a.f[(int64_t)m * n + j] = f;
         const unsigned long long key = argmax_key(f, j);
         run_key[i] = key > run_key[i] ? key : run_key[i];

@@ -148,7 +148,8 @@ __device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
 // 8*(r/4) + 4*(lane/32) + r%4; column: lane % 32.
 // For the fuse epilogue the payload tile q[m0:m0+BM, n0:n0+BN] and the row
 // scales are first staged in LDS the main loop no longer needs (s_q: BM*BN
-// bytes, s_qs: BM floats) with coalesced loads, instead of one byte load per
+// bytes, s_qs: BM payload scales, then BM factors of the dot products: the
+// hidden-state code scales, or 1) with coalesced loads, instead of one byte load per
 // accumulator.  The caller has passed a barrier after its last LDS read.
 template <int BM, int BN, int WM, int WN, int WT, int EPI, int FM, int FN>
 __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const MfmaArgs& a,
@@ -199,7 +200,10 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
     }
     // a tile lies in one block of positions (blocks are multiples of BN)
     const int kb = a.qshift < 0 ? 0 : (n0 >> a.qshift);
-    for (int r = tid; r < BM; r += NT) s_qs[r] = m0 + r < M ? a.qscale[(int64_t)(m0 + r) * a.qnb + kb] : 0.0f;
+    for (int r = tid; r < BM; r += NT) {
+      s_qs[r] = m0 + r < M ? a.qscale[(int64_t)(m0 + r) * a.qnb + kb] : 0.0f;
+      s_qs[BM + r] = (a.hscale && m0 + r < M) ? a.hscale[m0 + r] : 1.0f;
+    }
     __syncthreads();
   }
   using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
@@ -234,7 +238,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
               const int nib = (lcol & 1) ? (byte >> 4) : (byte & 15);
               code = nib >= 8 ? nib - 16 : nib;
             }
-            const float f = __builtin_fmaf((float)code, s_qs[lrow], dot);
+            const float f = __builtin_fmaf((float)code, s_qs[lrow], dot * s_qs[BM + lrow]);
             if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
             const unsigned long long key = argmax_key_m(f, col);
             best = key > best ? key : best;

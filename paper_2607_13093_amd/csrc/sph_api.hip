@@ -146,6 +146,13 @@ size_t fuse_ws(int64_t M, int64_t n, int mode) {
   return b;
 }
 
+// int8 hidden-state codes of more rows than the skinny projection takes are
+// widened to bf16 operands [M, round_up(d_end, 8)] after the fuse workspace.
+size_t widen_ws(int64_t M, int64_t d_end) {
+  if (M <= sph::kGemvMaxRows || d_end <= 0) return 0;
+  return align256((size_t)M * (size_t)((d_end + 7) / 8 * 8) * 2);
+}
+
 }  // namespace
 
 extern "C" {
@@ -214,6 +221,31 @@ size_t sph_cloud_partial_workspace(int64_t M, sph_subset subset) {
 size_t sph_fuse_verify_workspace(int64_t M, sph_subset subset, int mode) {
   if (!subset || M < 0) return 0;
   return fuse_ws(M, subset->n, mode);
+}
+
+size_t sph_fuse_verify_hq_workspace(int64_t M, int64_t d_end, sph_subset subset, int mode) {
+  if (!subset || M < 0 || d_end < 0) return 0;
+  return fuse_ws(M, subset->n, mode) + widen_ws(M, d_end);
+}
+
+int sph_hidden_quantize(const void* h, int64_t ldh, int64_t M, int64_t d, int8_t* q_out,
+                        int64_t ldq, float* scale_out, void* stream) {
+  const char* fn = "sph_hidden_quantize";
+  if (M < 0 || M > (1 << 24)) return fail(SPH_E_INVALID_ARG, "%s: M=%lld out of range", fn, (long long)M);
+  if (d < 0 || d > (1 << 20)) return fail(SPH_E_INVALID_ARG, "%s: d=%lld out of range", fn, (long long)d);
+  if (ldh < d || ldq < d)
+    return fail(SPH_E_INVALID_ARG, "%s: row strides (ldh=%lld, ldq=%lld) below d=%lld", fn,
+                (long long)ldh, (long long)ldq, (long long)d);
+  if (M == 0) return ok();
+  if (!scale_out || (d > 0 && (!h || !q_out)))
+    return fail(SPH_E_INVALID_ARG, "%s: h/q_out/scale_out is NULL", fn);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = traced("hidden_quantize", s, [&] {
+    return sph::launch_hidden_quantize(static_cast<const uint16_t*>(h), ldh, (int)M, (int)d, q_out,
+                                       ldq, scale_out, s);
+  });
+  if (e != hipSuccess) return hip_fail(e, "hidden-state quantiser launch");
+  return ok();
 }
 
 int64_t sph_payload_code_bytes(int64_t n_sub, int bits) {
@@ -355,14 +387,17 @@ int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int6
                              accept_len_out, fused_out, workspace, ws_bytes, stream);
 }
 
-int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t block,
-                        const void* h_end, int64_t ldh, int64_t d_end, const void* w_end,
-                        int64_t ldw, sph_subset subset, int64_t n_sessions,
-                        int64_t rows_per_session, const int32_t* drafts, int mode,
-                        float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
-                        int32_t* accept_len_out, float* fused_out, void* workspace,
-                        size_t ws_bytes, void* stream) {
-  const char* fn = "sph_fuse_verify";
+namespace {
+
+// The endpoint call, with the endpoint's hidden state either as bf16 rows
+// (h_end, ldh) or as int8 codes with row scales (hq, ldh, h_scale).
+int fuse_verify_impl(const char* fn, bool codes, const void* q, const float* scale, int bits,
+                     int64_t block, const void* h_end, const int8_t* hq, const float* h_scale,
+                     int64_t ldh, int64_t d_end, const void* w_end, int64_t ldw,
+                     sph_subset subset, int64_t n_sessions, int64_t rows_per_session,
+                     const int32_t* drafts, int mode, float temperature, float top_p,
+                     uint64_t seed, int32_t* tokens_out, int32_t* accept_len_out,
+                     float* fused_out, void* workspace, size_t ws_bytes, void* stream) {
   if (bits != 8 && bits != 4) return fail(SPH_E_INVALID_ARG, "%s: bits=%d not 4 or 8", fn, bits);
   const int qshift = block_shift(block);
   if (qshift == -2)
@@ -390,12 +425,15 @@ int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t blo
   if (!subset) return fail(SPH_E_INVALID_ARG, "%s: subset is NULL", fn);
   if (M == 0) return ok();
   if (!q || !scale) return fail(SPH_E_INVALID_ARG, "%s: q/scale is NULL", fn);
-  if (d_end > 0 && (!h_end || !w_end)) return fail(SPH_E_INVALID_ARG, "%s: h_end/w_end is NULL", fn);
+  if (d_end > 0 && !w_end) return fail(SPH_E_INVALID_ARG, "%s: w_end is NULL", fn);
+  if (d_end > 0 && !codes && !h_end) return fail(SPH_E_INVALID_ARG, "%s: h_end is NULL", fn);
+  if (d_end > 0 && codes && (!hq || !h_scale))
+    return fail(SPH_E_INVALID_ARG, "%s: hq/h_scale is NULL", fn);
   if (k > 0 && !drafts) return fail(SPH_E_INVALID_ARG, "%s: drafts is NULL with k=%lld", fn, (long long)k);
   if (!tokens_out || !accept_len_out)
     return fail(SPH_E_INVALID_ARG, "%s: tokens_out/accept_len_out is NULL", fn);
   const int64_t n = subset->n;
-  const size_t need = fuse_ws(M, n, mode);
+  const size_t need = fuse_ws(M, n, mode) + (codes ? widen_ws(M, d_end) : 0);
   if (!workspace || ws_bytes < need)
     return fail(SPH_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
                 workspace ? ws_bytes : (size_t)0);
@@ -415,12 +453,26 @@ int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t blo
   float* fused = fused_out;
   if (mode == SPH_SAMPLE && !fused)
     fused = reinterpret_cast<float*>(ws + align256((size_t)M * sph::kMaxBlocks * 8));
-  const bool h_vec = d_end == 0 || ((reinterpret_cast<uintptr_t>(h_end) & 15) == 0 && ldh % 8 == 0);
+  // int8 codes take part only where there is an endpoint partial
+  const bool hcodes = codes && d_end > 0;
+  const bool h_vec = d_end == 0 || hcodes ||
+                     ((reinterpret_cast<uintptr_t>(h_end) & 15) == 0 && ldh % 8 == 0);
   int nblk;
   if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks) {
     sph::MfmaArgs a{};
     a.h = static_cast<const uint16_t*>(h_end);
     a.ldh = ldh;
+    if (hcodes) {
+      // codes -> bf16 operands in the workspace, row scales in the epilogue
+      uint16_t* wide = reinterpret_cast<uint16_t*>(ws + fuse_ws(M, n, mode));
+      hipError_t e = traced("fuse_widen_codes", s, [&] {
+        return sph::launch_widen_codes(hq, ldh, (int)M, (int)d_end, (int)Kp, wide, s);
+      });
+      if (e != hipSuccess) return hip_fail(e, "hidden-code widening launch");
+      a.h = wide;
+      a.ldh = Kp;
+      a.hscale = h_scale;
+    }
     a.M = (int)M;
     a.K = (int)d_end;
     a.w = static_cast<const uint8_t*>(w_end);
@@ -448,8 +500,13 @@ int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t blo
     for (int64_t m0 = 0; m0 < M; m0 += mr) {
       const int rows = (int)std::min<int64_t>(mr, M - m0);
       sph::GemvArgs a{};
-      a.h = static_cast<const uint16_t*>(h_end) + (d_end > 0 ? m0 * ldh : 0);
+      a.h = hcodes ? nullptr : static_cast<const uint16_t*>(h_end) + (d_end > 0 ? m0 * ldh : 0);
       a.ldh = ldh;
+      if (hcodes) {
+        a.hq = hq + m0 * ldh;
+        a.ldhq = ldh;
+        a.hscale = h_scale + m0;
+      }
       a.K = (int)d_end;
       a.Kp = (int)Kp;
       a.w = static_cast<const uint8_t*>(w_end);
@@ -490,6 +547,34 @@ int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t blo
   });
   if (e != hipSuccess) return hip_fail(e, "greedy finaliser launch");
   return ok();
+}
+
+}  // namespace
+
+int sph_fuse_verify_fmt(const void* q, const float* scale, int bits, int64_t block,
+                        const void* h_end, int64_t ldh, int64_t d_end, const void* w_end,
+                        int64_t ldw, sph_subset subset, int64_t n_sessions,
+                        int64_t rows_per_session, const int32_t* drafts, int mode,
+                        float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                        int32_t* accept_len_out, float* fused_out, void* workspace,
+                        size_t ws_bytes, void* stream) {
+  return fuse_verify_impl("sph_fuse_verify", false, q, scale, bits, block, h_end, nullptr, nullptr,
+                          ldh, d_end, w_end, ldw, subset, n_sessions, rows_per_session, drafts,
+                          mode, temperature, top_p, seed, tokens_out, accept_len_out, fused_out,
+                          workspace, ws_bytes, stream);
+}
+
+int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t block,
+                       const int8_t* hq, int64_t ldhq, const float* h_scale, int64_t d_end,
+                       const void* w_end, int64_t ldw, sph_subset subset, int64_t n_sessions,
+                       int64_t rows_per_session, const int32_t* drafts, int mode,
+                       float temperature, float top_p, uint64_t seed, int32_t* tokens_out,
+                       int32_t* accept_len_out, float* fused_out, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  return fuse_verify_impl("sph_fuse_verify_hq", true, q, scale, bits, block, nullptr, hq, h_scale,
+                          ldhq, d_end, w_end, ldw, subset, n_sessions, rows_per_session, drafts,
+                          mode, temperature, top_p, seed, tokens_out, accept_len_out, fused_out,
+                          workspace, ws_bytes, stream);
 }
 
 int sph_trace_start(int capacity) {

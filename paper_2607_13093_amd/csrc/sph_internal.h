@@ -69,6 +69,11 @@ struct GemvArgs {
   int qbits, qshift, qnb;
   float* f;               // fp32 [rows, n] or null
   uint64_t* best_part;    // argmax keys [rows, kMaxBlocks]
+  // fuse only: int8 hidden-state codes instead of bf16 h (then h is unused)
+  // and their row scales, which multiply the row's dot products
+  const int8_t* hq;       // [rows, ldhq] or null
+  int64_t ldhq;
+  const float* hscale;    // fp32 [rows] or null
 };
 
 // Arguments of the dense (MFMA) gathered projection: C = h[M, K] * W[S]^T.
@@ -96,6 +101,7 @@ struct MfmaArgs {
   int qbits, qshift, qnb;
   float* f;               // fp32 [M, n] or null
   uint64_t* best_part;    // argmax keys [M, kMaxBlocks], slot = n-tile
+  const float* hscale;    // fuse only: fp32 [M] factors of the dot products, or null
 };
 
 constexpr int kMfmaBN = 256;  // subset positions per MFMA tile
@@ -129,6 +135,14 @@ hipError_t launch_accept(const int32_t* tokens, const int32_t* drafts, int n_ses
 hipError_t launch_final_greedy(const uint64_t* best_part, int nblk, const int32_t* ids, int n,
                                int n_sessions, int R, const int32_t* drafts,
                                int32_t* tokens, int32_t* accept, hipStream_t s);
+
+// Hidden-state codes (hidden.hip): per-row int8 codes and scales of bf16
+// rows h [M, ldh] (d columns), and the widening of codes [M, ldhq] (K
+// columns) into bf16 operands out [M, Kp] (Kp a multiple of 8, pad zero).
+hipError_t launch_hidden_quantize(const uint16_t* h, int64_t ldh, int M, int d, int8_t* q,
+                                  int64_t ldq, float* scale, hipStream_t s);
+hipError_t launch_widen_codes(const int8_t* hq, int64_t ldhq, int M, int K, int Kp,
+                              uint16_t* out, hipStream_t s);
 
 // Measurement kernels (probe.hip).
 hipError_t launch_probe_read(const void* buf, int64_t bytes, float* sink, hipStream_t s);

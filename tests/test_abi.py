@@ -174,6 +174,39 @@ def test_payload_sizes_reject(lib):
     assert lib.sph_payload_scale_count(-5, 0) == -1
 
 
+@pytest.mark.parametrize("kw,msg", [
+    (dict(M=-1), "M=-1"),
+    (dict(d=-3), "d=-3"),
+    (dict(ldh=100), "row strides"),
+    (dict(ldq=100), "row strides"),
+    (dict(h=None), "NULL"),
+    (dict(q=None), "NULL"),
+    (dict(s=None), "NULL"),
+])
+def test_hidden_quantize_validation(lib, kw, msg):
+    a = dict(h=16, ldh=256, M=3, d=256, q=16, ldq=256, s=16)
+    a.update(kw)
+    rc = lib.sph_hidden_quantize(a["h"], a["ldh"], a["M"], a["d"], a["q"], a["ldq"], a["s"], None)
+    assert rc == _lib.SPH_E_INVALID_ARG
+    assert msg in lib.sph_last_error().decode()
+
+
+def test_hidden_quantize_empty_batch_launches_nothing(lib):
+    assert lib.sph_hidden_quantize(None, 8, 0, 8, None, 8, None, None) == 0
+
+
+def test_fuse_verify_hq_validation(lib):
+    # strides are checked before anything else needs the subset or a device
+    rc = lib.sph_fuse_verify_hq(1, 1, 8, 0, 1, 32, 1, 64, 16, 64, None, 2, 3, 1,
+                                _lib.SPH_GREEDY, 1.0, 1.0, 0, 1, 1, None, 1, 0, None)
+    assert rc == _lib.SPH_E_INVALID_ARG
+    assert "row strides" in lib.sph_last_error().decode()
+    rc = lib.sph_fuse_verify_hq(1, 1, 5, 0, 1, 64, 1, 64, 16, 64, None, 2, 3, 1,
+                                _lib.SPH_GREEDY, 1.0, 1.0, 0, 1, 1, None, 1, 0, None)
+    assert rc == _lib.SPH_E_INVALID_ARG and b"bits=5" in lib.sph_last_error()
+    assert lib.sph_fuse_verify_hq_workspace(5, 256, None, 0) == 0
+
+
 def test_error_string_is_thread_local(lib):
     import threading
     assert _cloud(lib, M=-1) == _lib.SPH_E_INVALID_ARG
