@@ -37,3 +37,5 @@ from .split_head import (  # noqa: F401
     cloud_call,
     endpoint_call,
 )
+
+from . import gcm  # noqa: F401,E402  (AES-GCM of eq. 19)
