@@ -250,6 +250,45 @@ int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t bloc
                        size_t ws_bytes, void* stream);
 
 /*
+ * Payload sealing (eq. 19): AES-GCM (AES per FIPS-197, GCM per NIST
+ * SP 800-38D, 96-bit IVs, 128-bit tags) of batches of rows, each row its
+ * own message: row m of `rows` rows of row_bytes bytes is encrypted under
+ * iv[m] (12 bytes; J0 = iv || 00000001, the data keystream starts at
+ * counter 2) with associated data aad[m] (aad_bytes bytes, e.g. session,
+ * block and cache-control fields).  A nonce must never repeat under one
+ * key; the caller chooses the scheme (the paper derives GPU-mode nonces from
+ * the session and the message type).  Seal codes and scales of a payload as
+ * two batches (two message types).  All buffers are device memory; rows are
+ * ld_* bytes apart, iv [rows][12], tag [rows][16].  Limits: rows <= 65535,
+ * aad_bytes <= 1024, ceil(aad_bytes/16) + ceil(row_bytes/16) + 1 <= 16384.
+ * Seal and open may work in place (out == in, same stride).
+ */
+typedef struct sph_gcm_key_s* sph_gcm_key;
+
+/* Expand a 16- or 32-byte AES key (host memory) into a device key object
+ * (round keys, tables and the powers of the GHASH key, ~264 KB); blocks
+ * until the upload on `stream` has finished.  Destroy with
+ * sph_gcm_key_destroy. */
+int sph_gcm_key_create(const uint8_t* key, int key_bytes, void* stream, sph_gcm_key* out);
+void sph_gcm_key_destroy(sph_gcm_key key);
+
+/* Device workspace bytes of a seal or open of rows x row_bytes. */
+size_t sph_gcm_workspace(int64_t rows, int64_t row_bytes);
+
+/* ct[m] = plaintext row m xor its keystream; tag[m] its authentication tag. */
+int sph_gcm_seal(sph_gcm_key key, const void* pt, int64_t ld_pt, int64_t rows, int64_t row_bytes,
+                 const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes, void* ct,
+                 int64_t ld_ct, uint8_t* tag, void* workspace, size_t ws_bytes, void* stream);
+
+/* pt[m] = ciphertext row m xor its keystream; ok_out[m] = 1 if tag[m] is the
+ * row's tag, else 0.  A row with ok_out[m] = 0 must not be used: its pt row
+ * holds unauthenticated bytes. */
+int sph_gcm_open(sph_gcm_key key, const void* ct, int64_t ld_ct, int64_t rows, int64_t row_bytes,
+                 const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                 const uint8_t* tag, void* pt, int64_t ld_pt, int32_t* ok_out, void* workspace,
+                 size_t ws_bytes, void* stream);
+
+/*
  * Kernel tracing.  While a trace is active, each call records one duration
  * per kernel it launches: start and stop HIP events are attached to the
  * kernel dispatches themselves (hipExtLaunchKernelGGL), so a duration is

@@ -16,6 +16,10 @@ from .api import (  # noqa: F401
     fuse_verify_workspace,
     payload_code_bytes,
     hidden_quantize,
+    GcmKey,
+    gcm_seal,
+    gcm_open,
+    gcm_workspace,
     fuse_verify_hq,
     fuse_verify_hq_workspace,
     payload_scale_count,

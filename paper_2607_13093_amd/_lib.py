@@ -68,6 +68,19 @@ SIGNATURES = {
         ctypes.c_int, ctypes.c_float, ctypes.c_float, ctypes.c_uint64,  # mode, temperature, top_p, seed
         c_vp, c_vp, c_vp,                   # tokens_out, accept_len_out, fused_out
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_gcm_key_create": (ctypes.c_int, [c_vp, ctypes.c_int, c_vp, ctypes.POINTER(c_vp)]),
+    "sph_gcm_key_destroy": (None, [c_vp]),
+    "sph_gcm_workspace": (ctypes.c_size_t, [c_i64, c_i64]),
+    "sph_gcm_seal": (ctypes.c_int, [
+        c_vp, c_vp, c_i64, c_i64, c_i64,    # key, pt, ld_pt, rows, row_bytes
+        c_vp, c_vp, c_i64, c_i64,           # iv, aad, ld_aad, aad_bytes
+        c_vp, c_i64, c_vp,                  # ct, ld_ct, tag
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_gcm_open": (ctypes.c_int, [
+        c_vp, c_vp, c_i64, c_i64, c_i64,    # key, ct, ld_ct, rows, row_bytes
+        c_vp, c_vp, c_i64, c_i64,           # iv, aad, ld_aad, aad_bytes
+        c_vp, c_vp, c_i64, c_vp,            # tag, pt, ld_pt, ok_out
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
     "sph_trace_start": (ctypes.c_int, [ctypes.c_int]),
     "sph_trace_stop": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
     # include/sph_probe.h

@@ -79,6 +79,96 @@ class Subset:
             pass
 
 
+class GcmKey:
+    """Device AES-GCM key (16- or 32-byte key) for sealing payload rows (eq. 19)."""
+
+    def __init__(self, key: bytes, device=None):
+        import ctypes
+        lib = _lib.load()
+        self._lib = lib
+        self.handle = ctypes_vp()
+        key = bytes(key)
+        buf = ctypes.create_string_buffer(key, len(key))
+        dev = torch.device("cuda") if device is None else torch.device(device)
+        with torch.cuda.device(dev):
+            check(lib.sph_gcm_key_create(ctypes.addressof(buf), len(key), _stream_handle(dev),
+                                         self.handle))
+        ctypes.memset(buf, 0, len(key))
+        self.device = dev
+
+    def close(self) -> None:
+        if self.handle is not None and self.handle.value:
+            self._lib.sph_gcm_key_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def gcm_workspace(rows: int, row_bytes: int) -> int:
+    return int(_lib.load().sph_gcm_workspace(int(rows), int(row_bytes)))
+
+
+def _rows_u8(t: torch.Tensor, name: str):
+    _require_gpu(name, t)
+    if t.dim() != 2 or (t.shape[0] > 0 and t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"{name}: expected a 2-D tensor whose rows are contiguous")
+    rows = t.shape[0]
+    row_bytes = t.shape[1] * t.element_size()
+    ld = t.stride(0) * t.element_size() if rows > 0 else row_bytes
+    return rows, row_bytes, ld
+
+
+def gcm_seal(key: GcmKey, pt: torch.Tensor, iv: torch.Tensor, aad: Optional[torch.Tensor] = None,
+             out=None, workspace: Optional[torch.Tensor] = None):
+    """Seal each row of pt (a 2-D device tensor; rows are the messages) under
+    iv uint8 [rows, 12] and aad uint8 [rows, a].  Returns (ct uint8 [rows,
+    row_bytes], tag uint8 [rows, 16])."""
+    lib = _lib.load()
+    rows, row_bytes, ld = _rows_u8(pt, "pt")
+    dev = pt.device
+    if out is None:
+        ct = torch.empty((rows, row_bytes), dtype=torch.uint8, device=dev)
+        tag = torch.empty((rows, 16), dtype=torch.uint8, device=dev)
+    else:
+        ct, tag = out
+    na = 0 if aad is None else aad.shape[1]
+    if workspace is None:
+        workspace = torch.empty(max(gcm_workspace(rows, row_bytes), 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_gcm_seal(key.handle, pt.data_ptr(), ld, rows, row_bytes, iv.data_ptr(),
+                           _ptr(aad), aad.stride(0) if aad is not None else 0, na,
+                           ct.data_ptr(), ct.stride(0) * ct.element_size() if rows > 0 else row_bytes,
+                           tag.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                           _stream_handle(dev)))
+    return ct, tag
+
+
+def gcm_open(key: GcmKey, ct: torch.Tensor, iv: torch.Tensor, tag: torch.Tensor,
+             aad: Optional[torch.Tensor] = None, out=None, workspace: Optional[torch.Tensor] = None):
+    """Open each row of ct; returns (pt uint8 [rows, row_bytes], ok int32
+    [rows]): ok[m] = 1 when row m's tag verifies (use no row with ok 0)."""
+    lib = _lib.load()
+    rows, row_bytes, ld = _rows_u8(ct, "ct")
+    dev = ct.device
+    if out is None:
+        pt = torch.empty((rows, row_bytes), dtype=torch.uint8, device=dev)
+        ok = torch.empty((rows,), dtype=torch.int32, device=dev)
+    else:
+        pt, ok = out
+    na = 0 if aad is None else aad.shape[1]
+    if workspace is None:
+        workspace = torch.empty(max(gcm_workspace(rows, row_bytes), 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_gcm_open(key.handle, ct.data_ptr(), ld, rows, row_bytes, iv.data_ptr(),
+                           _ptr(aad), aad.stride(0) if aad is not None else 0, na, tag.data_ptr(),
+                           pt.data_ptr(), pt.stride(0) * pt.element_size() if rows > 0 else row_bytes,
+                           ok.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                           _stream_handle(dev)))
+    return pt, ok
+
+
 def ctypes_vp():
     return _lib.c_vp()
 

@@ -1,0 +1,333 @@
+// AES-GCM seal and open of payload rows (eq. 19: the quantised payload is
+// encrypted with AES-GCM under a key K and a nonce IV, with session, block
+// and cache metadata as associated data).  AES per FIPS-197, GCM per NIST
+// SP 800-38D with 96-bit IVs; every row is its own message.
+//
+// Key set-up (host, once per key): the S-box from its definition (inverse
+// in GF(2^8) by discrete logarithms to the generator 3, then the affine map
+// bit by bit), one 256-entry table T0[x] = (2S(x), S(x), S(x), 3S(x)) whose
+// byte rotations give the other three column tables, the round keys, the
+// hash key H = E_K(0^128) and the powers H^1 .. H^kGcmMaxPow.
+//
+// GHASH of a message with a AAD blocks, n ciphertext blocks and the length
+// block is S = sum_k X_k H^(m-k+1), m = a + n + 1, so with the powers in a
+// table every block's term is independent: ciphertext block j (0-based)
+// contributes C_j H^(n+1-j).  k_gcm_blocks runs one thread per 16-byte
+// block (counter-mode keystream from inc32 counters 2, 3, ... and the
+// block's GHASH term) and XOR-reduces the terms of its 256 blocks;
+// k_gcm_finish adds the partial sums, the AAD and length terms and forms
+// (seal) or checks (open) the tag E_K(J0) xor S.  XOR is exact and
+// associative, so the result does not depend on the reduction order.
+#include <cstring>
+#include <vector>
+
+#include "sph_internal.h"
+
+namespace sph {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// host: S-box, tables, key schedule, powers of H
+// ---------------------------------------------------------------------------
+
+uint8_t xtime(uint8_t b) { return (uint8_t)((b << 1) ^ ((b & 0x80) ? 0x1B : 0x00)); }
+
+void build_sbox(uint8_t sbox[256]) {
+  // 3 generates the multiplicative group of GF(2^8): log / antilog tables
+  uint8_t alog[255];
+  int lg[256] = {0};
+  uint8_t x = 1;
+  for (int i = 0; i < 255; ++i) {
+    alog[i] = x;
+    lg[x] = i;
+    x = (uint8_t)(x ^ xtime(x));  // x * 3
+  }
+  for (int a = 0; a < 256; ++a) {
+    const uint8_t inv = a == 0 ? 0 : alog[(255 - lg[a]) % 255];
+    // affine map: bit i of the result = b_i ^ b_(i+4) ^ b_(i+5) ^ b_(i+6) ^ b_(i+7) ^ c_i (indices mod 8)
+    uint8_t r = 0;
+    for (int i = 0; i < 8; ++i) {
+      const int bit = ((inv >> i) ^ (inv >> ((i + 4) & 7)) ^ (inv >> ((i + 5) & 7)) ^
+                       (inv >> ((i + 6) & 7)) ^ (inv >> ((i + 7) & 7)) ^ (0x63 >> i)) & 1;
+      r = (uint8_t)(r | (bit << i));
+    }
+    sbox[a] = r;
+  }
+}
+
+uint32_t rotr32(uint32_t v, int k) { return (v >> k) | (v << (32 - k)); }
+
+}  // namespace
+
+// words are big-endian: byte 0 of a column (row 0) is the most significant
+__host__ __device__ __forceinline__ uint32_t gcm_rotr(uint32_t v, int k) {
+  return (v >> k) | (v << (32 - k));
+}
+
+// One AES block: in/out as four big-endian column words.  te: the T0 table,
+// sb: the S-box, rk: 4 (nr + 1) round-key words.
+template <class TE, class SB, class RK>
+__host__ __device__ __forceinline__ void aes_block(TE te, SB sb, RK rk, int nr, const uint32_t in[4],
+                                                   uint32_t out[4]) {
+  uint32_t s0 = in[0] ^ rk[0], s1 = in[1] ^ rk[1], s2 = in[2] ^ rk[2], s3 = in[3] ^ rk[3];
+  for (int r = 1; r < nr; ++r) {
+    // column c of the next state: T0[row 0 of column c] ^ T1[row 1 of c+1]
+    // ^ T2[row 2 of c+2] ^ T3[row 3 of c+3] ^ round key (ShiftRows folded in)
+    const uint32_t t0 = te[s0 >> 24] ^ gcm_rotr(te[(s1 >> 16) & 255], 8) ^
+                        gcm_rotr(te[(s2 >> 8) & 255], 16) ^ gcm_rotr(te[s3 & 255], 24) ^ rk[4 * r];
+    const uint32_t t1 = te[s1 >> 24] ^ gcm_rotr(te[(s2 >> 16) & 255], 8) ^
+                        gcm_rotr(te[(s3 >> 8) & 255], 16) ^ gcm_rotr(te[s0 & 255], 24) ^ rk[4 * r + 1];
+    const uint32_t t2 = te[s2 >> 24] ^ gcm_rotr(te[(s3 >> 16) & 255], 8) ^
+                        gcm_rotr(te[(s0 >> 8) & 255], 16) ^ gcm_rotr(te[s1 & 255], 24) ^ rk[4 * r + 2];
+    const uint32_t t3 = te[s3 >> 24] ^ gcm_rotr(te[(s0 >> 16) & 255], 8) ^
+                        gcm_rotr(te[(s1 >> 8) & 255], 16) ^ gcm_rotr(te[s2 & 255], 24) ^ rk[4 * r + 3];
+    s0 = t0; s1 = t1; s2 = t2; s3 = t3;
+  }
+  // last round: SubBytes and ShiftRows only
+  auto last = [&](uint32_t a, uint32_t b, uint32_t c, uint32_t d, uint32_t k) {
+    return (((uint32_t)sb[a >> 24]) << 24 | ((uint32_t)sb[(b >> 16) & 255]) << 16 |
+            ((uint32_t)sb[(c >> 8) & 255]) << 8 | (uint32_t)sb[d & 255]) ^ k;
+  };
+  out[0] = last(s0, s1, s2, s3, rk[4 * nr]);
+  out[1] = last(s1, s2, s3, s0, rk[4 * nr + 1]);
+  out[2] = last(s2, s3, s0, s1, rk[4 * nr + 2]);
+  out[3] = last(s3, s0, s1, s2, rk[4 * nr + 3]);
+}
+
+// z = x . y in GF(2^128) (the standard's bit-serial product: bit i of x
+// from the left selects V_i, V_(i+1) = V_i >> 1 reduced by R = 0xE1 || 0^120).
+__host__ __device__ __forceinline__ void gf128_mul(const uint32_t x[4], const uint32_t y[4],
+                                                   uint32_t z[4]) {
+  uint32_t v0 = y[0], v1 = y[1], v2 = y[2], v3 = y[3];
+  uint32_t z0 = 0, z1 = 0, z2 = 0, z3 = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t xw = x[w];
+#pragma unroll 8
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t m = 0u - ((xw >> b) & 1u);
+      z0 ^= v0 & m; z1 ^= v1 & m; z2 ^= v2 & m; z3 ^= v3 & m;
+      const uint32_t lsb = 0u - (v3 & 1u);
+      v3 = (v3 >> 1) | (v2 << 31);
+      v2 = (v2 >> 1) | (v1 << 31);
+      v1 = (v1 >> 1) | (v0 << 31);
+      v0 = (v0 >> 1) ^ (0xE1000000u & lsb);
+    }
+  }
+  z[0] = z0; z[1] = z1; z[2] = z2; z[3] = z3;
+}
+
+bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_image, int& nr) {
+  if (key_bytes != 16 && key_bytes != 32) return false;
+  uint8_t sbox[256];
+  build_sbox(sbox);
+  uint32_t te[256];
+  for (int x = 0; x < 256; ++x) {
+    const uint8_t s = sbox[x], s2 = xtime(s), s3 = (uint8_t)(s2 ^ s);
+    te[x] = ((uint32_t)s2 << 24) | ((uint32_t)s << 16) | ((uint32_t)s << 8) | s3;
+  }
+  const int nk = key_bytes / 4;
+  nr = nk + 6;
+  uint32_t w[60];
+  for (int i = 0; i < nk; ++i)
+    w[i] = ((uint32_t)key[4 * i] << 24) | ((uint32_t)key[4 * i + 1] << 16) |
+           ((uint32_t)key[4 * i + 2] << 8) | key[4 * i + 3];
+  uint8_t rc = 1;
+  auto subword = [&](uint32_t v) {
+    return ((uint32_t)sbox[v >> 24] << 24) | ((uint32_t)sbox[(v >> 16) & 255] << 16) |
+           ((uint32_t)sbox[(v >> 8) & 255] << 8) | sbox[v & 255];
+  };
+  for (int i = nk; i < 4 * (nr + 1); ++i) {
+    uint32_t t = w[i - 1];
+    if (i % nk == 0) {
+      t = subword(rotr32(t, 24)) ^ ((uint32_t)rc << 24);  // RotWord is a left byte rotation
+      rc = xtime(rc);
+    } else if (nk > 6 && i % nk == 4) {
+      t = subword(t);
+    }
+    w[i] = w[i - nk] ^ t;
+  }
+  // device image: te | sbox | round keys | powers of H
+  dev_image.assign(kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16, 0);
+  std::memcpy(dev_image.data(), te, sizeof(te));
+  std::memcpy(dev_image.data() + 1024, sbox, 256);
+  std::memcpy(dev_image.data() + kGcmRkOffset, w, sizeof(uint32_t) * 4 * (nr + 1));
+  const uint32_t zero[4] = {0, 0, 0, 0};
+  uint32_t h[4];
+  aes_block(te, sbox, w, nr, zero, h);
+  uint32_t* pw = reinterpret_cast<uint32_t*>(dev_image.data() + kGcmPowOffset);  // pw[4e .. 4e+3] = H^e
+  std::memcpy(pw + 4, h, 16);
+  for (int e = 2; e <= kGcmMaxPow; ++e) gf128_mul(pw + 4 * (e - 1), h, pw + 4 * e);
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// device
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void load_be_words(const uint8_t* p, int valid, uint32_t w[4]) {
+  uint8_t b[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) b[i] = i < valid ? p[i] : 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    w[k] = ((uint32_t)b[4 * k] << 24) | ((uint32_t)b[4 * k + 1] << 16) | ((uint32_t)b[4 * k + 2] << 8) |
+           b[4 * k + 3];
+}
+
+struct GcmShared {
+  uint32_t te[256];
+  uint8_t sb[256];
+  uint32_t rk[60];
+  uint32_t red[4][4];
+};
+
+__device__ __forceinline__ void stage_key(GcmShared& sh, const uint8_t* key_dev, int nr) {
+  const int tid = threadIdx.x;
+  const uint32_t* te = reinterpret_cast<const uint32_t*>(key_dev);
+  sh.te[tid] = te[tid];
+  sh.sb[tid] = key_dev[1024 + tid];
+  if (tid < 4 * (nr + 1)) sh.rk[tid] = reinterpret_cast<const uint32_t*>(key_dev + kGcmRkOffset)[tid];
+  __syncthreads();
+}
+
+// One thread per 16-byte block of a row (grid: blocks / 256 x rows).
+template <bool OPEN>
+__global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ key_dev, int nr,
+                                                    const uint8_t* __restrict__ in, int64_t ld_in,
+                                                    uint8_t* __restrict__ out, int64_t ld_out,
+                                                    int64_t L, int n, const uint8_t* __restrict__ iv,
+                                                    uint32_t* __restrict__ partial, int nparts) {
+  __shared__ GcmShared sh;
+  stage_key(sh, key_dev, nr);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t row = blockIdx.y;
+  const int j = blockIdx.x * 256 + tid;
+  uint32_t t[4] = {0u, 0u, 0u, 0u};
+  if (j < n) {
+    const uint8_t* ivr = iv + row * 12;
+    uint32_t ctr[4];
+    load_be_words(ivr, 12, ctr);
+    ctr[3] = (uint32_t)(2 + j);  // inc32 from J0 + 1
+    uint32_t ks[4];
+    aes_block(sh.te, sh.sb, sh.rk, nr, ctr, ks);
+    const int valid = (int)min<int64_t>(16, L - (int64_t)j * 16);
+    const uint8_t* src = in + row * ld_in + (int64_t)j * 16;
+    uint8_t* dst = out + row * ld_out + (int64_t)j * 16;
+    uint32_t x[4], y[4];
+    load_be_words(src, valid, x);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) y[k] = x[k] ^ ks[k];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+    // the GHASH input is the ciphertext: the output when sealing, the input
+    // when opening; bytes past the message are zero
+    uint32_t c[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) c[k] = OPEN ? x[k] : y[k];
+    if (!OPEN && valid < 16) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i >= valid) c[i >> 2] &= ~(0xFFu << (24 - 8 * (i & 3)));
+    }
+    const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset) + 4 * (n + 1 - j);
+    const uint32_t hp[4] = {pw[0], pw[1], pw[2], pw[3]};
+    gf128_mul(c, hp, t);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) t[k] ^= __shfl_xor(t[k], o, 64);
+    if (lane == 0) sh.red[wave][k] = t[k];
+  }
+  __syncthreads();
+  if (tid < 4)
+    partial[(row * nparts + blockIdx.x) * 4 + tid] = sh.red[0][tid] ^ sh.red[1][tid] ^ sh.red[2][tid] ^ sh.red[3][tid];
+}
+
+// One thread per row: partial sums + AAD terms + length term, then the tag.
+template <bool OPEN>
+__global__ __launch_bounds__(256) void k_gcm_finish(const uint8_t* __restrict__ key_dev, int nr, int rows,
+                                                    int64_t L, int n, const uint8_t* __restrict__ iv,
+                                                    const uint8_t* __restrict__ aad, int64_t ld_aad,
+                                                    int la, const uint32_t* __restrict__ partial,
+                                                    int nparts, uint8_t* __restrict__ tag,
+                                                    int32_t* __restrict__ ok) {
+  __shared__ GcmShared sh;
+  stage_key(sh, key_dev, nr);
+  const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (row >= rows) return;
+  const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset);
+  const int na = (la + 15) / 16;
+  const int m = na + n + 1;
+  uint32_t s[4] = {0u, 0u, 0u, 0u};
+  for (int p = 0; p < nparts; ++p)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] ^= partial[(row * nparts + p) * 4 + k];
+  for (int i = 0; i < na; ++i) {
+    uint32_t a[4], t[4];
+    load_be_words(aad + row * ld_aad + (int64_t)i * 16, min(16, la - 16 * i), a);
+    const uint32_t hp[4] = {pw[4 * (m - i)], pw[4 * (m - i) + 1], pw[4 * (m - i) + 2], pw[4 * (m - i) + 3]};
+    gf128_mul(a, hp, t);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] ^= t[k];
+  }
+  {
+    const uint64_t abits = (uint64_t)la * 8, cbits = (uint64_t)L * 8;
+    const uint32_t lb[4] = {(uint32_t)(abits >> 32), (uint32_t)abits, (uint32_t)(cbits >> 32), (uint32_t)cbits};
+    const uint32_t h1[4] = {pw[4], pw[5], pw[6], pw[7]};
+    uint32_t t[4];
+    gf128_mul(lb, h1, t);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s[k] ^= t[k];
+  }
+  uint32_t j0[4], e0[4];
+  load_be_words(iv + row * 12, 12, j0);
+  j0[3] = 1u;
+  aes_block(sh.te, sh.sb, sh.rk, nr, j0, e0);
+  uint8_t* tg = tag + row * 16;
+  if (OPEN) {
+    uint32_t diff = 0;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const uint8_t b = (uint8_t)((e0[i >> 2] ^ s[i >> 2]) >> (24 - 8 * (i & 3)));
+      diff |= (uint32_t)(b ^ tg[i]);
+    }
+    ok[row] = diff == 0 ? 1 : 0;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tg[i] = (uint8_t)((e0[i >> 2] ^ s[i >> 2]) >> (24 - 8 * (i & 3)));
+  }
+}
+
+hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const uint8_t* in, int64_t ld_in,
+                      uint8_t* out, int64_t ld_out, int rows, int64_t L, const uint8_t* iv,
+                      const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag, int32_t* ok,
+                      uint32_t* partial, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int n = (int)((L + 15) / 16);
+  const int nparts = (n + 255) / 256;
+  if (rows > 65535 && nparts > 0) return hipErrorInvalidValue;
+  if (nparts > 0) {
+    if (open)
+      launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, in, ld_in,
+                    out, ld_out, L, n, iv, partial, nparts);
+    else
+      launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, in, ld_in,
+                    out, ld_out, L, n, iv, partial, nparts);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int fb = (rows + 255) / 256;
+  if (open)
+    launch_kernel(k_gcm_finish<true>, dim3(fb), dim3(256), 0, s, key_dev, nr, rows, L, n, iv, aad,
+                  ld_aad, la, partial, nparts, tag, ok);
+  else
+    launch_kernel(k_gcm_finish<false>, dim3(fb), dim3(256), 0, s, key_dev, nr, rows, L, n, iv, aad,
+                  ld_aad, la, partial, nparts, tag, ok);
+  return hipGetLastError();
+}
+
+}  // namespace sph

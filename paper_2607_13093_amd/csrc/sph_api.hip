@@ -7,6 +7,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <algorithm>
 #include <vector>
 
 #include "sph.h"
@@ -18,6 +19,11 @@ struct sph_subset_s {
   int64_t n;
   int64_t vocab;
   int device;
+};
+
+struct sph_gcm_key_s {
+  uint8_t* d_image;  // T0 | S-box | round keys | powers of H (device)
+  int nr;            // AES rounds: 10 (128-bit key) or 14 (256-bit key)
 };
 
 namespace {
@@ -575,6 +581,97 @@ int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t bloc
                           ldhq, d_end, w_end, ldw, subset, n_sessions, rows_per_session, drafts,
                           mode, temperature, top_p, seed, tokens_out, accept_len_out, fused_out,
                           workspace, ws_bytes, stream);
+}
+
+int sph_gcm_key_create(const uint8_t* key, int key_bytes, void* stream, sph_gcm_key* out) {
+  if (!out) return fail(SPH_E_INVALID_ARG, "sph_gcm_key_create: out is NULL");
+  *out = nullptr;
+  if (!key) return fail(SPH_E_INVALID_ARG, "sph_gcm_key_create: key is NULL");
+  if (key_bytes != 16 && key_bytes != 32)
+    return fail(SPH_E_INVALID_ARG, "sph_gcm_key_create: key_bytes=%d not 16 or 32", key_bytes);
+  std::vector<uint8_t> image;
+  int nr = 0;
+  if (!sph::gcm_key_setup(key, key_bytes, image, nr))
+    return fail(SPH_E_INVALID_ARG, "sph_gcm_key_create: key set-up failed");
+  uint8_t* d = nullptr;
+  hipError_t e = hipMalloc(&d, image.size());
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(gcm key)");
+  hipStream_t st = (hipStream_t)stream;
+  e = hipMemcpyAsync(d, image.data(), image.size(), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);  // the host image is freed on return
+  // the image holds key material: clear the host copy
+  std::fill(image.begin(), image.end(), (uint8_t)0);
+  if (e != hipSuccess) {
+    (void)hipFree(d);
+    return hip_fail(e, "sph_gcm_key_create: upload");
+  }
+  *out = new sph_gcm_key_s{d, nr};
+  return ok();
+}
+
+void sph_gcm_key_destroy(sph_gcm_key key) {
+  if (!key) return;
+  (void)hipFree(key->d_image);
+  delete key;
+}
+
+size_t sph_gcm_workspace(int64_t rows, int64_t row_bytes) {
+  if (rows <= 0 || row_bytes < 0) return 0;
+  const int64_t n = (row_bytes + 15) / 16;
+  return align256((size_t)rows * (size_t)((n + 255) / 256) * 16);
+}
+
+namespace {
+
+int gcm_call(const char* fn, bool open, sph_gcm_key key, const void* in, int64_t ld_in,
+             int64_t rows, int64_t row_bytes, const uint8_t* iv, const void* aad, int64_t ld_aad,
+             int64_t aad_bytes, void* out, int64_t ld_out, uint8_t* tag, int32_t* okf,
+             void* workspace, size_t ws_bytes, void* stream) {
+  if (!key) return fail(SPH_E_INVALID_ARG, "%s: key is NULL", fn);
+  if (rows < 0 || rows > 65535) return fail(SPH_E_INVALID_ARG, "%s: rows=%lld out of range", fn, (long long)rows);
+  if (row_bytes < 0) return fail(SPH_E_INVALID_ARG, "%s: row_bytes=%lld", fn, (long long)row_bytes);
+  if (aad_bytes < 0 || aad_bytes > 1024)
+    return fail(SPH_E_INVALID_ARG, "%s: aad_bytes=%lld not in [0, 1024]", fn, (long long)aad_bytes);
+  const int64_t m = (aad_bytes + 15) / 16 + (row_bytes + 15) / 16 + 1;
+  if (m > sph::kGcmMaxPow)
+    return fail(SPH_E_UNSUPPORTED, "%s: message of %lld bytes (+%lld AAD) exceeds %d blocks", fn,
+                (long long)row_bytes, (long long)aad_bytes, sph::kGcmMaxPow);
+  if (ld_in < row_bytes || ld_out < row_bytes || (aad_bytes > 0 && ld_aad < aad_bytes))
+    return fail(SPH_E_INVALID_ARG, "%s: row strides below the row lengths", fn);
+  if (rows == 0) return ok();
+  if (!iv || !tag || (open && !okf)) return fail(SPH_E_INVALID_ARG, "%s: iv/tag/ok is NULL", fn);
+  if (row_bytes > 0 && (!in || !out)) return fail(SPH_E_INVALID_ARG, "%s: input/output is NULL", fn);
+  if (aad_bytes > 0 && !aad) return fail(SPH_E_INVALID_ARG, "%s: aad is NULL", fn);
+  const size_t need = sph_gcm_workspace(rows, row_bytes);
+  if (need > 0 && (!workspace || ws_bytes < need))
+    return fail(SPH_E_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, need,
+                workspace ? ws_bytes : (size_t)0);
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = traced(open ? "gcm_open" : "gcm_seal", s, [&] {
+    return sph::launch_gcm(open, key->d_image, key->nr, static_cast<const uint8_t*>(in), ld_in,
+                           static_cast<uint8_t*>(out), ld_out, (int)rows, row_bytes, iv,
+                           static_cast<const uint8_t*>(aad), ld_aad, (int)aad_bytes, tag, okf,
+                           static_cast<uint32_t*>(workspace), s);
+  });
+  if (e != hipSuccess) return hip_fail(e, open ? "AES-GCM open launch" : "AES-GCM seal launch");
+  return ok();
+}
+
+}  // namespace
+
+int sph_gcm_seal(sph_gcm_key key, const void* pt, int64_t ld_pt, int64_t rows, int64_t row_bytes,
+                 const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes, void* ct,
+                 int64_t ld_ct, uint8_t* tag, void* workspace, size_t ws_bytes, void* stream) {
+  return gcm_call("sph_gcm_seal", false, key, pt, ld_pt, rows, row_bytes, iv, aad, ld_aad, aad_bytes,
+                  ct, ld_ct, tag, nullptr, workspace, ws_bytes, stream);
+}
+
+int sph_gcm_open(sph_gcm_key key, const void* ct, int64_t ld_ct, int64_t rows, int64_t row_bytes,
+                 const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                 const uint8_t* tag, void* pt, int64_t ld_pt, int32_t* ok_out, void* workspace,
+                 size_t ws_bytes, void* stream) {
+  return gcm_call("sph_gcm_open", true, key, ct, ld_ct, rows, row_bytes, iv, aad, ld_aad, aad_bytes,
+                  pt, ld_pt, const_cast<uint8_t*>(tag), ok_out, workspace, ws_bytes, stream);
 }
 
 int sph_trace_start(int capacity) {

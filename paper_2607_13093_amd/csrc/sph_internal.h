@@ -3,6 +3,7 @@
 
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+#include <vector>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -143,6 +144,20 @@ hipError_t launch_hidden_quantize(const uint16_t* h, int64_t ldh, int M, int d, 
                                   int64_t ldq, float* scale, hipStream_t s);
 hipError_t launch_widen_codes(const int8_t* hq, int64_t ldhq, int M, int K, int Kp,
                               uint16_t* out, hipStream_t s);
+
+// AES-GCM of payload rows (gcm.hip).  A key's device image holds the T0
+// table (1 KB), the S-box (256 B), the round keys (at kGcmRkOffset) and the
+// powers H^0 .. H^kGcmMaxPow of the hash key (16 B each, at kGcmPowOffset).
+constexpr int kGcmMaxPow = 16384;  // AAD + ciphertext + length blocks of one message
+constexpr int kGcmRkOffset = 1280;
+constexpr int kGcmPowOffset = 1536;
+constexpr size_t kGcmImageBytes = (size_t)kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16;
+bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_image, int& nr);
+// rows <= 65535 messages of L bytes; partial: rows * ceil(ceil(L/16)/256) * 16 bytes
+hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const uint8_t* in, int64_t ld_in,
+                      uint8_t* out, int64_t ld_out, int rows, int64_t L, const uint8_t* iv,
+                      const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag, int32_t* ok,
+                      uint32_t* partial, hipStream_t s);
 
 // Measurement kernels (probe.hip).
 hipError_t launch_probe_read(const void* buf, int64_t bytes, float* sink, hipStream_t s);

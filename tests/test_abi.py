@@ -207,6 +207,28 @@ def test_fuse_verify_hq_validation(lib):
     assert lib.sph_fuse_verify_hq_workspace(5, 256, None, 0) == 0
 
 
+def test_gcm_validation(lib):
+    # rejected on the host before any device access
+    E = _lib.SPH_E_INVALID_ARG
+    assert lib.sph_gcm_seal(None, 1, 16, 1, 16, 1, None, 0, 0, 1, 16, 1, 1, 1 << 20, None) == E
+    assert b"key is NULL" in lib.sph_last_error()
+    out = ctypes.c_void_p()
+    key = (ctypes.c_uint8 * 24)()
+    assert lib.sph_gcm_key_create(key, 24, None, out) == E and b"key_bytes=24" in lib.sph_last_error()
+    assert lib.sph_gcm_key_create(None, 16, None, out) == E
+    assert lib.sph_gcm_key_create(key, 16, None, None) == E
+    lib.sph_gcm_key_destroy(None)
+
+
+@pytest.mark.parametrize("rows,row_bytes,need", [
+    (0, 100, 0), (5, 0, 0), (1, 1, 256), (5, 49152, 1024), (2048, 32768, 2048 * 8 * 16),
+    (3, 16 * 256 + 1, 256),
+])
+def test_gcm_workspace_sizes(lib, rows, row_bytes, need):
+    # one 16-byte partial GHASH sum per row and 256 blocks, rounded up to 256 bytes
+    assert lib.sph_gcm_workspace(rows, row_bytes) == need
+
+
 def test_error_string_is_thread_local(lib):
     import threading
     assert _cloud(lib, M=-1) == _lib.SPH_E_INVALID_ARG

@@ -1,0 +1,153 @@
+"""GPU parity of the AES-GCM payload seal (eq. 19) against the CPU oracle
+(oracle/gcm.py): ciphertexts and tags bit for bit, authenticated opening,
+tamper detection per row, in-place operation, strided rows, and a payload
+sealed between the two halves of the projection."""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import gcm as ogcm
+import paper_2607_13093_amd as sph
+from synth import CONFIGS, Config, make_workload
+
+import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+CASES = [
+    # (key bytes, rows, row bytes, aad bytes)
+    (16, 1, 0, 0),
+    (16, 3, 1, 5),
+    (16, 2, 15, 16),
+    (32, 4, 16, 0),
+    (16, 5, 17, 40),
+    (32, 3, 4099, 13),
+    (16, 33, 300, 24),
+    (16, 5, 49152, 24),     # the decode payload's code rows
+    (32, 2, 65536, 1024),   # 4096 + 64 + 1 blocks, the largest AAD
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"k{k}r{r}L{l}a{a}" for k, r, l, a in CASES])
+def test_seal_matches_oracle_and_opens(case):
+    klen, rows, L, la = case
+    rng = np.random.default_rng(7 * rows + L + la + klen)
+    key = rng.bytes(klen)
+    pt = rng.integers(0, 256, (rows, L), dtype=np.uint8)
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    aad = rng.integers(0, 256, (rows, la), dtype=np.uint8)
+    ct_ref, tag_ref = ogcm.seal_rows(key, pt, iv, aad)
+    say(f"[gpu] gcm seal key={klen} rows={rows} L={L} aad={la}")
+    k = sph.GcmKey(key)
+    ct, tag = sph.gcm_seal(k, _dev(pt), _dev(iv), _dev(aad) if la else None)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(P.host(ct), ct_ref)
+    np.testing.assert_array_equal(P.host(tag), tag_ref)
+    say(f"[gpu] gcm open key={klen} rows={rows} L={L}")
+    back, ok = sph.gcm_open(k, ct, _dev(iv), tag, _dev(aad) if la else None)
+    torch.cuda.synchronize()
+    assert P.host(ok).tolist() == [1] * rows
+    np.testing.assert_array_equal(P.host(back), pt)
+
+
+def test_open_flags_exactly_the_tampered_rows():
+    rng = np.random.default_rng(21)
+    key = rng.bytes(16)
+    rows, L, la = 6, 1000, 20
+    pt = rng.integers(0, 256, (rows, L), dtype=np.uint8)
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    aad = rng.integers(0, 256, (rows, la), dtype=np.uint8)
+    k = sph.GcmKey(key)
+    say("[gpu] gcm tamper")
+    ct, tag = sph.gcm_seal(k, _dev(pt), _dev(iv), _dev(aad))
+    ct_h, tag_h, aad_t, iv_t = P.host(ct).copy(), P.host(tag).copy(), aad.copy(), iv.copy()
+    ct_h[1, 999] ^= 0x01        # last ciphertext byte
+    tag_h[2, 0] ^= 0x80         # tag
+    aad_t[3, 7] ^= 0x10         # associated data
+    iv_t[4, 11] ^= 0x01         # nonce
+    ct_h[5, 0] ^= 0x00          # untouched
+    back, ok = sph.gcm_open(k, _dev(ct_h), _dev(iv_t), _dev(tag_h), _dev(aad_t))
+    torch.cuda.synchronize()
+    assert P.host(ok).tolist() == [1, 0, 0, 0, 0, 1]
+    np.testing.assert_array_equal(P.host(back)[[0, 5]], pt[[0, 5]])
+
+
+def test_in_place_and_strided_rows():
+    rng = np.random.default_rng(22)
+    key = rng.bytes(32)
+    rows, L, ld = 4, 777, 1024
+    buf = rng.integers(0, 256, (rows, ld), dtype=np.uint8)
+    pt = buf[:, :L].copy()
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    ct_ref, tag_ref = ogcm.seal_rows(key, pt, iv, np.zeros((rows, 0), np.uint8))
+    k = sph.GcmKey(key)
+    say("[gpu] gcm in place, strided")
+    d = _dev(buf)
+    view = d[:, :L]
+    tag = torch.empty((rows, 16), dtype=torch.uint8, device="cuda")
+    sph.gcm_seal(k, view, _dev(iv), None, out=(view, tag))
+    torch.cuda.synchronize()
+    got = P.host(d)
+    np.testing.assert_array_equal(got[:, :L], ct_ref)
+    np.testing.assert_array_equal(got[:, L:], buf[:, L:])          # bytes past each row untouched
+    np.testing.assert_array_equal(P.host(tag), tag_ref)
+    ok = torch.empty((rows,), dtype=torch.int32, device="cuda")
+    sph.gcm_open(k, view, _dev(iv), tag, None, out=(view, ok))
+    torch.cuda.synchronize()
+    assert P.host(ok).tolist() == [1] * rows
+    np.testing.assert_array_equal(P.host(d)[:, :L], pt)
+
+
+def test_sealed_payload_between_the_halves():
+    # cloud partial -> seal codes and scales -> open -> endpoint call; the
+    # endpoint's results equal those on the unsealed payload bit for bit
+    cfg = Config("gcm_payload", 95, d=1032, d_end=64, vocab=6000, n_sub=2501, subset_kind="choice",
+                 sessions=3, rows_per_session=4)
+    wl = make_workload(cfg)
+    dw = P.DeviceWorkload(wl)
+    say("[gpu] gcm sealed payload, b=4 block=256")
+    q, s, _ = dw.cloud(want_z=False, bits=4, block=256)
+    rng = np.random.default_rng(23)
+    key = rng.bytes(16)
+    k = sph.GcmKey(key)
+    M = cfg.M
+    # nonces: (session, message type, row) -- distinct for every message
+    iv = np.zeros((2, M, 12), np.uint8)
+    for t in range(2):
+        for m in range(M):
+            iv[t, m, :4] = np.frombuffer(np.uint32(m // cfg.rows_per_session).tobytes()[::-1], np.uint8)
+            iv[t, m, 4] = t
+            iv[t, m, 8:] = np.frombuffer(np.uint32(m).tobytes()[::-1], np.uint8)
+    aad = np.tile(np.frombuffer(b"session-meta", np.uint8), (M, 1))
+    cq, tq = sph.gcm_seal(k, q, _dev(iv[0]), _dev(aad))
+    cs, ts = sph.gcm_seal(k, s.view(torch.uint8).reshape(M, -1), _dev(iv[1]), _dev(aad))
+    torch.cuda.synchronize()
+    ct_ref, tag_ref = ogcm.seal_rows(key, P.host(q).view(np.uint8), iv[0], aad)
+    np.testing.assert_array_equal(P.host(cq), ct_ref)
+    np.testing.assert_array_equal(P.host(tq), tag_ref)
+    q2, okq = sph.gcm_open(k, cq, _dev(iv[0]), tq, _dev(aad))
+    s2, oks = sph.gcm_open(k, cs, _dev(iv[1]), ts, _dev(aad))
+    torch.cuda.synchronize()
+    assert P.host(okq).all() and P.host(oks).all()
+    s2 = s2.view(torch.float32).reshape(s.shape)
+    drafts = np.zeros((cfg.sessions, cfg.k), np.int32)
+    t1, a1, f1 = dw.fuse(q, s, drafts, bits=4, block=256)
+    t2, a2, f2 = dw.fuse(q2, s2, drafts, bits=4, block=256)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(P.host(q2), P.host(q))
+    np.testing.assert_array_equal(P.host(t2), P.host(t1))
+    np.testing.assert_array_equal(P.host(f2).view(np.uint32), P.host(f1).view(np.uint32))
