@@ -44,6 +44,9 @@ def parse():
                    help="payload code width b (eq. 18)")
     p.add_argument("--block", type=int, default=0,
                    help="payload scale block: 0 = one scale per row, else 256..4096 positions")
+    p.add_argument("--seal", action="store_true",
+                   help="seal the payload (codes and scales) with AES-GCM after the cloud call and "
+                        "open it before the endpoint call (eq. 19)")
     p.add_argument("--hidden-int8", action="store_true",
                    help="the cloud also quantises the whole hidden row to int8 codes and the "
                         "endpoint projects from them (sph_hidden_quantize + sph_fuse_verify_hq)")
@@ -230,6 +233,26 @@ def main():
     acc = torch.empty((cfg.sessions,), dtype=torch.int32, device=dev)
     ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
     ws_f = torch.empty(max(1, sph.fuse_verify_workspace(M, sub, mode)), dtype=torch.uint8, device=dev)
+    if args.seal:
+        gkey = sph.GcmKey(bytes(range(16)))
+        s_bytes = s.view(torch.uint8).reshape(M, -1)
+        iv_q = torch.zeros((M, 12), dtype=torch.uint8, device=dev)
+        iv_s = torch.zeros((M, 12), dtype=torch.uint8, device=dev)
+        rows_idx = torch.arange(M, device=dev)
+        for ivt in (iv_q, iv_s):                            # row number, big-endian, in the last 3 bytes
+            ivt[:, 9] = (rows_idx >> 16).to(torch.uint8)
+            ivt[:, 10] = ((rows_idx >> 8) & 255).to(torch.uint8)
+            ivt[:, 11] = (rows_idx & 255).to(torch.uint8)
+        iv_s[:, 4] = 1                                      # message type: scales
+        aad = torch.zeros((M, 16), dtype=torch.uint8, device=dev)
+        cq = torch.empty_like(q, dtype=torch.uint8)
+        cs = torch.empty_like(s_bytes)
+        tq = torch.empty((M, 16), dtype=torch.uint8, device=dev)
+        ts = torch.empty((M, 16), dtype=torch.uint8, device=dev)
+        okq = torch.empty((M,), dtype=torch.int32, device=dev)
+        oks = torch.empty((M,), dtype=torch.int32, device=dev)
+        ws_g = torch.empty(max(1, sph.gcm_workspace(M, q.shape[1] * q.element_size())), dtype=torch.uint8,
+                           device=dev)
     hq = torch.empty((M, cfg.d), dtype=torch.int8, device=dev)
     hs = torch.empty((M,), dtype=torch.float32, device=dev)
     if args.hidden_int8:
@@ -241,6 +264,12 @@ def main():
         c = i % N_COPIES
         sph.cloud_partial(h_c, wc[c], sub, cfg.clip_c, w_row_scale=wsc, workspace=ws_c,
                           out=(q, s, None), bits=bits, block=block)
+        if args.seal:
+            qb = q.view(torch.uint8)
+            sph.gcm_seal(gkey, qb, iv_q, aad, out=(cq, tq), workspace=ws_g)
+            sph.gcm_seal(gkey, s_bytes, iv_s, aad, out=(cs, ts), workspace=ws_g)
+            sph.gcm_open(gkey, cq, iv_q, tq, aad, out=(qb, okq), workspace=ws_g)
+            sph.gcm_open(gkey, cs, iv_s, ts, aad, out=(s_bytes, oks), workspace=ws_g)
         if args.hidden_int8:
             sph.hidden_quantize(h, out=(hq, hs))
             sph.fuse_verify_hq(q, s, hq, hs, de, we[c], sub, cfg.sessions, cfg.rows_per_session,
@@ -338,6 +367,7 @@ def main():
                                        f"one scale per {block} positions"),
             "payload_bytes_per_row": code_bytes + 4 * nb,
             "hidden_state": "int8 codes + fp32 scale per row" if args.hidden_int8 else "bf16",
+            "sealed": "AES-128-GCM per row (codes, scales)" if args.seal else "no",
         },
         "roofline": roof,
         "attainable": att,
