@@ -52,6 +52,11 @@ def parse():
                         "endpoint projects from them (sph_hidden_quantize + sph_fuse_verify_hq)")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the oracle's CPU baseline run (0 to skip)")
+    p.add_argument("--sweep", choices=("d_end", "subset", "drafts", "all"), default=None,
+                   help="paper-shape sweeps of the decode step instead of the benchmark line: "
+                        "hidden 4096, vocabulary 150000, one session; d_end in "
+                        "{48,96,128,256,512}, subset 30/40/100%% of V, drafts k in {1,2,4,5,6,8}; "
+                        "one JSON line per point")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run plain device copies of MIB MiB (to scale rocprofv3 "
                         "FETCH_SIZE / WRITE_SIZE counters), then exit")
@@ -184,8 +189,109 @@ def cpu_baseline(wl, seconds):
             "sample": f"{reps} {what} of {cfg.name} (cloud + endpoint oracle, fp64 NumPy), {dt:.1f} s"}
 
 
+SWEEP_D, SWEEP_V = 4096, 150000
+
+
+def sweep_points(which):
+    """(d_end, subset fraction, k) of each point; defaults d_end 256, 40%, k 4."""
+    pts = []
+    if which in ("d_end", "all"):
+        pts += [(de, 0.4, 4) for de in (48, 96, 128, 256, 512)]
+    if which in ("subset", "all"):
+        pts += [(256, f, 4) for f in (0.3, 0.4, 1.0)]
+    if which in ("drafts", "all"):
+        pts += [(256, 0.4, k) for k in (1, 2, 4, 5, 6, 8)]
+    seen, out = set(), []
+    for p in pts:
+        if p not in seen:
+            seen.add(p)
+            out.append(p)
+    return out
+
+
+def sweep(args):
+    """Decode-step sweeps at the paper's shapes (Table 6: d_end; the language
+    subset fraction; Table 7: draft length).  Weights, hidden states and
+    subsets are seeded synthetic data generated on the device; every point
+    runs the whole step (cloud call + endpoint call, greedy) on rotated
+    weight copies, like the benchmark."""
+    import numpy as np
+    import torch
+
+    import paper_2607_13093_amd as sph
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(2607)
+    w = []
+    for _ in range(N_COPIES):
+        t = torch.randn((SWEEP_V, SWEEP_D), generator=g, device=dev, dtype=torch.float32)
+        w.append((t * (1.0 / SWEEP_D ** 0.5)).to(torch.bfloat16))
+        del t
+    rng = np.random.default_rng(2607)
+    full_perm = rng.permutation(SWEEP_V)
+    for de, frac, k in sweep_points(args.sweep):
+        M = k + 1
+        n = int(round(frac * SWEEP_V))
+        ids = np.sort(full_perm[:n]).astype(np.int32)
+        sub = sph.Subset(vocab=SWEEP_V, full=True) if n == SWEEP_V else sph.Subset(ids, vocab=SWEEP_V)
+        h = torch.randn((M, SWEEP_D), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        q = torch.empty((M, n), dtype=torch.int8, device=dev)
+        sc = torch.empty((M,), dtype=torch.float32, device=dev)
+        tok = torch.empty((M,), dtype=torch.int32, device=dev)
+        acc = torch.empty((1,), dtype=torch.int32, device=dev)
+        ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
+        ws_f = torch.empty(max(1, sph.fuse_verify_workspace(M, sub, sph.GREEDY)), dtype=torch.uint8, device=dev)
+        drafts = torch.from_numpy(rng.choice(ids if n < SWEEP_V else np.arange(SWEEP_V, dtype=np.int32),
+                                             size=(1, k)).astype(np.int32)).to(dev)
+
+        def step(i):
+            c = i % N_COPIES
+            sph.cloud_partial(h[:, de:], w[c][:, de:], sub, 30.0, workspace=ws_c, out=(q, sc, None))
+            sph.fuse_verify(q, sc, h[:, :de], w[c][:, :de], sub, 1, M, drafts, workspace=ws_f,
+                            out=(tok, acc, None))
+
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream(dev)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for i in range(args.steps):
+            step(i)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / args.steps
+        cap = 16 * args.steps + 16
+        sph.trace_start(cap)
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize()
+        by = {}
+        for name, kms in sph.trace_collect(cap):
+            by.setdefault(name, []).append(kms)
+        kern = {kk: float(np.mean(v)) * 1e3 for kk, v in by.items()}
+        dc = SWEEP_D - de
+        cloud_bytes = n * (dc * 2 + 4) + M * dc * 2
+        ck = kern.get("cloud_gemv", kern.get("cloud_mfma"))
+        print(json.dumps({
+            "sweep": args.sweep, "d": SWEEP_D, "vocab": SWEEP_V, "d_end": de, "subset": n,
+            "subset_frac": frac, "k": k, "rows": M, "ms_per_step": ms,
+            "rows_vocab_per_s": M * n / (ms * 1e-3), "kernels_us": kern,
+            "cloud_hbm_frac": cloud_bytes / (ck * 1e-6) / 1e9 / HBM_PEAK_GBS if ck else None,
+            "payload_bytes_per_row": n + 4}), flush=True)
+        sub.close()
+
+
 def main():
     args = parse()
+    if args.sweep:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        sweep(args)
+        return
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
         return
