@@ -743,12 +743,13 @@ constexpr size_t mfma_dma8_lds_bytes() {
 // rows per lane instead of 64 halve the argmax butterfly.  128-row tiles use
 // 2 x 2.  On the dense 2048-row shapes 8 waves ran the cloud projection 9%
 // and the endpoint projection 28% faster than 4 (wave tile 128 x 128).
+// 32-row tiles (9 to 32 rows, direct-to-LDS only) use 1 x 4 waves of 32 x 64.
 template <int BM, int EPI>
 struct WaveGrid {
   static constexpr bool kEight = BM >= 256;
   static constexpr bool kTall = kEight && !(BM == 256 && EPI == kEpiFuse);
-  static constexpr int WM = kEight ? (kTall ? 2 : 4) : 2;
-  static constexpr int WN = kEight ? (kTall ? 4 : 2) : 2;
+  static constexpr int WM = BM == 32 ? 1 : kEight ? (kTall ? 2 : 4) : 2;
+  static constexpr int WN = BM == 32 ? 4 : kEight ? (kTall ? 4 : 2) : 2;
 };
 
 template <int BM, int BN, int WT, int EPI>
@@ -767,8 +768,9 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
     return hipGetLastError();
   }
   // K not a multiple of the K step: the register-staged kernel (2 x 2 waves),
-  // which exists for 128- and 256-row tiles (the tile rule never picks 320)
-  if constexpr (BM <= 256) {
+  // which exists for 128- and 256-row tiles (the tile rule picks neither 32
+  // nor 320 then)
+  if constexpr (BM >= 128 && BM <= 256) {
     auto kern = k_mfma<BM, BN, WT, EPI>;
     constexpr size_t lds = mfma_lds_bytes<BM, BN>();
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
@@ -780,12 +782,17 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// Row tile for M rows: 128 up to 128 rows, else whichever of 256 and 320
+// Row tile for M rows: 32 up to 32 rows (K a multiple of the K step), 128
+// up to 128 rows, else whichever of 256 and 320
 // pads M less (320-row tiles need K a multiple of the K step).  Measured on
 // the batched shape (M = 320, 60000 ids): 320-row tiles, one per 256 ids,
 // 156 us against 265 us for 256-row and 289 us for 128-row tiles; M = 640
 // with fp8 weights: 460 us against 537 us for 256-row tiles.
 static int mfma_bm(int M, int K) {
+  // up to 32 rows the projection streams its weights like the skinny kernel
+  // does; a 32-row tile wastes at most 23 of 32 rows of MFMA work instead of
+  // 119 of 128, and two blocks fit on a CU
+  if (M <= 32 && K % kBK == 0) return 32;
   if (M <= 128) return 128;
   const int pad256 = (M + 255) / 256 * 256 - M;
   const int pad320 = (M + 319) / 320 * 320 - M;
@@ -797,6 +804,7 @@ int mfma_n_tiles(int n) { return (n + kMfmaBN - 1) / kMfmaBN; }
 template <int WT, int EPI>
 static hipError_t launch_bm(const MfmaArgs& a, hipStream_t s) {
   switch (mfma_bm(a.M, a.K)) {
+    case 32: return launch_tile<32, kMfmaBN, WT, EPI>(a, s);
     case 320: return launch_tile<320, kMfmaBN, WT, EPI>(a, s);
     case 256: return launch_tile<256, kMfmaBN, WT, EPI>(a, s);
     default: return launch_tile<128, kMfmaBN, WT, EPI>(a, s);

@@ -122,6 +122,10 @@ RAGGED = [
     (17, 17, 1096, 72, 9000, 4097), # 289 rows: one 320-row m-tile (8 waves), ragged n
     (24, 25, 1096, 72, 9000, 4097), # 600 rows: two 320-row m-tiles, the second ragged
     (13, 10, 2056, 8, 9000, 8193),  # 130 rows: two m-tiles, last n-tile of one column
+    # 32-row tiles (9..32 rows, K a multiple of 64 in both calls)
+    (3, 3, 1088, 64, 5000, 2501),   # 9 rows
+    (4, 8, 2304, 256, 9000, 4097),  # 32 rows, ragged n
+    (1, 9, 4096, 256, 20000, 9001), # the decode step with k = 8 drafts
 ]
 
 
@@ -198,6 +202,12 @@ def test_fp8_cloud_partial_dense_320_row_tiles():
     cfg = Config("fp8_dense_320", 29, d=1088, d_end=64, vocab=7000, n_sub=3003, subset_kind="choice",
                  sessions=60, rows_per_session=5, wtype="fp8", with_bias=True)
     run_greedy_case(make_workload(cfg), tag="fp8 dense, 320-row tiles")
+
+
+def test_fp8_cloud_partial_32_row_tiles():
+    cfg = Config("fp8_32", 31, d=1088, d_end=64, vocab=5000, n_sub=3001, subset_kind="choice",
+                 sessions=4, rows_per_session=5, wtype="fp8", with_bias=True)
+    run_greedy_case(make_workload(cfg), tag="fp8, 20 rows in a 32-row tile")
 
 
 def test_fp8_cloud_partial_dense_k_not_multiple_of_64():
