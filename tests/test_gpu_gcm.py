@@ -64,6 +64,33 @@ def test_seal_matches_oracle_and_opens(case):
     np.testing.assert_array_equal(P.host(back), pt)
 
 
+def test_large_batch():
+    # 40 rows x 3277 blocks (2 MB, ragged last block, AAD): the size of a
+    # batched payload; three rows checked against the oracle
+    rng = np.random.default_rng(31)
+    key = rng.bytes(32)
+    rows, L, la = 40, 52429, 24
+    pt = rng.integers(0, 256, (rows, L), dtype=np.uint8)
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    aad = rng.integers(0, 256, (rows, la), dtype=np.uint8)
+    say(f"[gpu] gcm chunked rows={rows} L={L}")
+    k = sph.GcmKey(key)
+    ct, tag = sph.gcm_seal(k, _dev(pt), _dev(iv), _dev(aad))
+    torch.cuda.synchronize()
+    ct_h, tag_h = P.host(ct), P.host(tag)
+    check = [0, 17, 39]                      # the oracle is slow: three rows
+    ct_ref, tag_ref = ogcm.seal_rows(key, pt[check], iv[check], aad[check])
+    np.testing.assert_array_equal(ct_h[check], ct_ref)
+    np.testing.assert_array_equal(tag_h[check], tag_ref)
+    bad = ct_h.copy()
+    bad[5, 30000] ^= 0x04
+    back, ok = sph.gcm_open(k, _dev(bad), _dev(iv), _dev(tag_h), _dev(aad))
+    torch.cuda.synchronize()
+    okh = P.host(ok)
+    assert okh[5] == 0 and okh.sum() == rows - 1
+    np.testing.assert_array_equal(np.delete(P.host(back), 5, axis=0), np.delete(pt, 5, axis=0))
+
+
 def test_open_flags_exactly_the_tampered_rows():
     rng = np.random.default_rng(21)
     key = rng.bytes(16)
