@@ -478,6 +478,14 @@ def main():
         "roofline": roof,
         "attainable": att,
         "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
+        # kernel time of each call per step (the cloud call's and the endpoint
+        # call's kernels; launch gaps excluded) and of the pair
+        "calls_ms": {
+            "cloud": float(sum(np.mean(v) for k, v in by.items() if k.startswith("cloud_"))),
+            "endpoint": float(sum(np.mean(v) for k, v in by.items() if k.startswith("fuse_"))),
+            "pair": float(sum(np.mean(v) for k, v in by.items()
+                              if k.startswith("cloud_") or k.startswith("fuse_"))),
+        },
         "ms_per_step_traced": ms_step_traced,
     }
     if args.cpu_seconds > 0:

@@ -122,6 +122,21 @@ def _rows_u8(t: torch.Tensor, name: str):
     return rows, row_bytes, ld
 
 
+def _check_bytes(t: torch.Tensor, name: str, shape) -> None:
+    _require_gpu(name, t)
+    if t.dtype != torch.uint8 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous uint8 {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+def _check_msg_args(rows: int, iv: torch.Tensor, aad: Optional[torch.Tensor]) -> None:
+    _check_bytes(iv, "iv", (rows, 12))
+    if aad is not None:
+        _require_gpu("aad", aad)
+        if aad.dtype != torch.uint8 or aad.dim() != 2 or aad.shape[0] != rows or \
+                (aad.shape[1] > 1 and aad.stride(1) != 1):
+            raise ValueError("aad: expected uint8 [rows, a] with contiguous rows")
+
+
 def gcm_seal(key: GcmKey, pt: torch.Tensor, iv: torch.Tensor, aad: Optional[torch.Tensor] = None,
              out=None, workspace: Optional[torch.Tensor] = None):
     """Seal each row of pt (a 2-D device tensor; rows are the messages) under
@@ -129,6 +144,7 @@ def gcm_seal(key: GcmKey, pt: torch.Tensor, iv: torch.Tensor, aad: Optional[torc
     row_bytes], tag uint8 [rows, 16])."""
     lib = _lib.load()
     rows, row_bytes, ld = _rows_u8(pt, "pt")
+    _check_msg_args(rows, iv, aad)
     dev = pt.device
     if out is None:
         ct = torch.empty((rows, row_bytes), dtype=torch.uint8, device=dev)
@@ -152,6 +168,8 @@ def gcm_open(key: GcmKey, ct: torch.Tensor, iv: torch.Tensor, tag: torch.Tensor,
     [rows]): ok[m] = 1 when row m's tag verifies (use no row with ok 0)."""
     lib = _lib.load()
     rows, row_bytes, ld = _rows_u8(ct, "ct")
+    _check_msg_args(rows, iv, aad)
+    _check_bytes(tag, "tag", (rows, 16))
     dev = ct.device
     if out is None:
         pt = torch.empty((rows, row_bytes), dtype=torch.uint8, device=dev)
@@ -313,6 +331,11 @@ def fuse_verify_hq(q: torch.Tensor, scale: torch.Tensor, hq: torch.Tensor, h_sca
     d_end = int(d_end)
     if d_end > 0:
         _require_gpu("hq", hq)
+        if hq.dtype != torch.int8 or hq.dim() != 2 or hq.shape[0] != M or hq.shape[1] < d_end or \
+                hq.stride(1) != 1:
+            raise ValueError(f"hq: expected int8 [{M}, >= {d_end}] with contiguous rows")
+        if h_scale.dtype != torch.float32 or tuple(h_scale.shape) != (M,) or not h_scale.is_contiguous():
+            raise ValueError(f"h_scale: expected contiguous float32 [{M}]")
         _require_gpu("w_end", w_end)
         w_end = _as_bits16(w_end)
         hp, ldh, sp = hq.data_ptr(), hq.stride(0), h_scale.data_ptr()
