@@ -28,6 +28,7 @@
 // fp32 partial logits and the tile's row maxima of |clamp(z)|; the fuse
 // epilogue dequantises the payload (eq. 13), writes fused logits on request
 // and the tile's per-row (value, position) argmax key.
+#include <atomic>
 #include <type_traits>
 
 #include "sph_internal.h"
@@ -752,8 +753,23 @@ struct WaveGrid {
   static constexpr int WN = BM == 32 ? 4 : kEight ? (kTall ? 4 : 2) : 2;
 };
 
+// The dynamic-LDS limit of a kernel is raised once per device (a host call,
+// kept out of every launch so that launches can be captured in a graph).
+// `done` is one instantiation's mask of devices already set.
+static hipError_t set_lds_limit_once(std::atomic<uint64_t>& done, const void* kern, size_t bytes) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev < 64 ? (uint64_t(1) << dev) : 0;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_release);
+  return e;
+}
+
 template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
+  static std::atomic<uint64_t> lds_set_dma{0}, lds_set_reg{0};
   constexpr int WM = WaveGrid<BM, EPI>::WM, WN = WaveGrid<BM, EPI>::WN, NT = 64 * WM * WN;
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
@@ -761,8 +777,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   if (a.K % kBK == 0) {
     auto kd = WT == 0 ? k_mfma_dma<BM, BN, WM, WN, EPI> : k_mfma_dma8<BM, BN, WM, WN, EPI>;
     constexpr size_t lds_d = WT == 0 ? mfma_dma_lds_bytes<BM, BN>() : mfma_dma8_lds_bytes<BM, BN>();
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kd),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_d);
+    hipError_t e = set_lds_limit_once(lds_set_dma, reinterpret_cast<const void*>(kd), lds_d);
     if (e != hipSuccess) return e;
     launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(NT), lds_d, s, a);
     return hipGetLastError();
@@ -773,8 +788,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   if constexpr (BM >= 128 && BM <= 256) {
     auto kern = k_mfma<BM, BN, WT, EPI>;
     constexpr size_t lds = mfma_lds_bytes<BM, BN>();
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = set_lds_limit_once(lds_set_reg, reinterpret_cast<const void*>(kern), lds);
     if (e != hipSuccess) return e;
     launch_kernel(kern, dim3(a.m_tiles * a.n_tiles), dim3(256), lds, s, a);
     return hipGetLastError();
