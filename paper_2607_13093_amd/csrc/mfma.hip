@@ -152,6 +152,15 @@ __device__ __forceinline__ void half_wave_max_transpose(T (&v)[P], int lane) {
 // bytes, s_qs: BM payload scales, then BM factors of the dot products: the
 // hidden-state code scales, or 1) with coalesced loads, instead of one byte load per
 // accumulator.  The caller has passed a barrier after its last LDS read.
+// z of one accumulator: fp8 row scale, then the bias (eq. 12)
+template <int WT>
+__device__ __forceinline__ float cloud_value(float dot, const MfmaArgs& a, int id) {
+  float zv = dot;
+  if constexpr (WT == 1) zv = zv * a.wscale[id];
+  if (a.bias) zv = zv + a.bias[id];
+  return zv;
+}
+
 template <int BM, int BN, int WM, int WN, int WT, int EPI, int FM, int FN>
 __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const MfmaArgs& a,
                                               const int32_t* s_ids, uint32_t* s_rmax,
@@ -207,7 +216,8 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
     }
     __syncthreads();
   }
-  using V = typename std::conditional<EPI == kEpiCloud, float, unsigned long long>::type;
+  constexpr bool kCloud = EPI != kEpiFuse;  // kEpiCloud or kEpiCloudQ
+  using V = typename std::conditional<kCloud, float, unsigned long long>::type;
   V red[P];
 #pragma unroll
   for (int t = FM * 16; t < P; ++t) red[t] = V(0);
@@ -224,11 +234,9 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
         const int col = n0 + lcol;
         if (row < M && col < n) {
           const float dot = acc[i][j][r];
-          if constexpr (EPI == kEpiCloud) {
-            float zv = dot;
-            if constexpr (WT == 1) zv = zv * a.wscale[s_ids[lcol]];
-            if (a.bias) zv = zv + a.bias[s_ids[lcol]];
-            __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
+          if constexpr (kCloud) {
+            const float zv = cloud_value<WT>(dot, a, s_ids[lcol]);
+            if (EPI == kEpiCloud || a.z) __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
             best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
           } else {
             int code;
@@ -257,16 +265,85 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
     if (idx >= FM * 16) continue;
     const int i = idx / 16, r = idx % 16;
     const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    if constexpr (EPI == kEpiCloud)
+    if constexpr (kCloud)
       atomicMax(&s_rmax[lrow], __float_as_uint(red[t]));
     else
       atomicMax(&s_rkey[lrow], red[t]);
   }
   __syncthreads();
+  if constexpr (EPI == kEpiCloudQ) {
+    // The tile is one scale block of every row: s = a / qmax from the tile's
+    // row maximum of |clamp(z)|, codes rint(clamp(z) / s) from the
+    // accumulators still in registers (the same fp32 operations as the
+    // quantiser kernel), one byte per code in LDS (the A staging area), then
+    // stored row by row, two codes per byte for b = 4; codes of positions
+    // past n are 0 (the pad nibble).
+    const float qmax = a.qout_bits == 8 ? 127.0f : 7.0f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const float sc = __uint_as_float(s_rmax[lrow]) / qmax;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int lcol = wn * TN + j * 32 + (lane & 31);
+          int code = 0;
+          if (n0 + lcol < n) {
+            const float y = fminf(fmaxf(cloud_value<WT>(acc[i][j][r], a, s_ids[lcol]), -a.clip), a.clip);
+            const float t = sc > 0.0f ? y / sc : 0.0f;
+            code = (int)fminf(fmaxf(rintf(t), -qmax), qmax);
+          }
+          s_q[lrow * BN + lcol] = (int8_t)code;
+        }
+      }
+    }
+    __syncthreads();
+    const int bits = a.qout_bits;
+    const int TB = BN * bits / 8;                      // code bytes of a tile row
+    const int64_t c0 = (int64_t)n0 * bits / 8;
+    const int64_t rowbytes = ((int64_t)n * bits + 7) / 8;
+    const bool vec = (a.qout_stride & 15) == 0 && (reinterpret_cast<uintptr_t>(a.qout) & 15) == 0;
+    for (int c = tid; c < BM * (TB / 16); c += NT) {
+      const int r = c / (TB / 16), k = c % (TB / 16);
+      const int row = m0 + r;
+      const int64_t col = c0 + (int64_t)k * 16;
+      if (row >= M || col >= rowbytes) continue;
+      uint32_t wv[4];
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int byte = 4 * e4 + e;
+          uint32_t v;
+          if (bits == 8) {
+            v = (uint8_t)s_q[r * BN + k * 16 + byte];
+          } else {
+            const int p0 = k * 32 + 2 * byte;
+            v = ((uint32_t)s_q[r * BN + p0] & 15u) | (((uint32_t)s_q[r * BN + p0 + 1] & 15u) << 4);
+          }
+          w |= v << (8 * e);
+        }
+        wv[e4] = w;
+      }
+      uint8_t* dst = a.qout + (int64_t)row * a.qout_stride + col;
+      if (vec && col + 16 <= rowbytes) {
+        *reinterpret_cast<u32x4_t*>(dst) = u32x4_t{wv[0], wv[1], wv[2], wv[3]};
+      } else {
+        for (int b = 0; b < 16 && col + b < rowbytes; ++b) dst[b] = (uint8_t)(wv[b >> 2] >> (8 * (b & 3)));
+      }
+    }
+    for (int i = tid; i < BM; i += NT) {
+      const int row = m0 + i;
+      if (row < M) a.qout_scale[(int64_t)row * a.qout_nb + nt] = __uint_as_float(s_rmax[i]) / qmax;
+    }
+    return;
+  }
   for (int i = tid; i < BM; i += NT) {
     const int row = m0 + i;
     if (row >= M) continue;
-    if constexpr (EPI == kEpiCloud)
+    if constexpr (kCloud)
       a.amax_part[(int64_t)row * kMaxBlocks + nt] = __uint_as_float(s_rmax[i]);
     else
       a.best_part[(int64_t)row * kMaxBlocks + nt] = s_rkey[i];
@@ -785,7 +862,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   // K not a multiple of the K step: the register-staged kernel (2 x 2 waves),
   // which exists for 128- and 256-row tiles (the tile rule picks neither 32
   // nor 320 then)
-  if constexpr (BM >= 128 && BM <= 256) {
+  if constexpr (BM >= 128 && BM <= 256 && EPI != kEpiCloudQ) {
     auto kern = k_mfma<BM, BN, WT, EPI>;
     constexpr size_t lds = mfma_lds_bytes<BM, BN>();
     hipError_t e = set_lds_limit_once(lds_set_reg, reinterpret_cast<const void*>(kern), lds);
@@ -825,7 +902,27 @@ static hipError_t launch_bm(const MfmaArgs& a, hipStream_t s) {
   }
 }
 
+// Cloud projection with the block quantiser in the epilogue, for the row
+// tiles whose accumulators and row maxima fit in the registers together
+// (32, 128, 256 rows, K a multiple of the K step).  Where the tile rule picks
+// 320 rows the separate quantiser is used: on 640 rows, 256-row tiles with
+// the fused quantiser ran 598 us against 428 + 43 us.
+bool mfma_quantises_in_epilogue(int M, int K) {
+  return K % kBK == 0 && mfma_bm(M, K) != 320;
+}
+
+template <int WT>
+static hipError_t launch_bm_q(const MfmaArgs& a, hipStream_t s) {
+  if (!mfma_quantises_in_epilogue(a.M, a.K)) return hipErrorInvalidValue;
+  switch (mfma_bm(a.M, a.K)) {
+    case 32: return launch_tile<32, kMfmaBN, WT, kEpiCloudQ>(a, s);
+    case 128: return launch_tile<128, kMfmaBN, WT, kEpiCloudQ>(a, s);
+    default: return launch_tile<256, kMfmaBN, WT, kEpiCloudQ>(a, s);
+  }
+}
+
 hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s) {
+  if (epi == kEpiCloudQ) return wtype == 0 ? launch_bm_q<0>(a, s) : launch_bm_q<1>(a, s);
   if (epi == kEpiCloud)
     return wtype == 0 ? launch_bm<0, kEpiCloud>(a, s) : launch_bm<1, kEpiCloud>(a, s);
   if (wtype != 0) return hipErrorInvalidValue;

@@ -325,7 +325,35 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
 
   // Dense path: more rows than one skinny launch covers, 16-byte aligned h rows.
   const bool h_vec = (reinterpret_cast<uintptr_t>(h_cloud) & 15) == 0 && ldh % 8 == 0;
+  const int64_t qstride = sph_payload_code_bytes(n, bits);
+  const int qnb = (int)sph_payload_scale_count(n, block);
   int nblk;
+  if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks &&
+      block == sph::kMfmaBN && sph::mfma_quantises_in_epilogue((int)M, (int)d_cloud)) {
+    // a scale block is one 256-position tile: the projection's epilogue
+    // quantises from its accumulators, z is written only on request
+    sph::MfmaArgs a{};
+    a.h = static_cast<const uint16_t*>(h_cloud);
+    a.ldh = ldh;
+    a.M = (int)M;
+    a.K = (int)d_cloud;
+    a.w = static_cast<const uint8_t*>(w_cloud);
+    a.ldw_bytes = ldw * wbytes;
+    a.wscale = w_row_scale;
+    a.ids = subset->d_ids;
+    a.n = (int)n;
+    a.bias = bias;
+    a.clip = clip_c;
+    a.z = z_out;
+    a.qout = static_cast<uint8_t*>(q_out);
+    a.qout_stride = qstride;
+    a.qout_scale = scale_out;
+    a.qout_bits = bits;
+    a.qout_nb = qnb;
+    hipError_t e = traced("cloud_mfma", s, [&] { return sph::launch_mfma(sph::kEpiCloudQ, wtype, a, s); });
+    if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
+    return ok();
+  }
   if (M > sph::kGemvMaxRows && h_vec && sph::mfma_n_tiles((int)n) <= sph::kMaxBlocks) {
     sph::MfmaArgs a{};
     a.h = static_cast<const uint16_t*>(h_cloud);
@@ -372,8 +400,6 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
       if (e != hipSuccess) return hip_fail(e, "cloud projection launch");
     }
   }
-  const int64_t qstride = sph_payload_code_bytes(n, bits);
-  const int qnb = (int)sph_payload_scale_count(n, block);
   hipError_t e = traced("cloud_quantize", s, [&] {
     return sph::launch_quantize(z, amax, nblk, (int)M, (int)n, clip_c, bits, qshift,
                                 static_cast<uint8_t*>(q_out), qstride, scale_out, qnb, s);

@@ -103,11 +103,18 @@ struct MfmaArgs {
   float* f;               // fp32 [M, n] or null
   uint64_t* best_part;    // argmax keys [M, kMaxBlocks], slot = n-tile
   const float* hscale;    // fuse only: fp32 [M] factors of the dot products, or null
+  // cloud with the payload quantised in the epilogue (scale blocks of one
+  // 256-position tile): codes rows of qout_stride bytes, scales [M, qout_nb];
+  // z is then written only if non-null
+  uint8_t* qout;
+  int64_t qout_stride;
+  float* qout_scale;
+  int qout_bits, qout_nb;
 };
 
 constexpr int kMfmaBN = 256;  // subset positions per MFMA tile
 
-enum Epilogue { kEpiCloud = 0, kEpiFuse = 1 };
+enum Epilogue { kEpiCloud = 0, kEpiFuse = 1, kEpiCloudQ = 2 };
 
 // Launchers (return the HIP launch status).
 hipError_t launch_gemv(int epi, int wtype, int rows, const GemvArgs& a, hipStream_t s);
@@ -115,6 +122,8 @@ int gemv_rows_per_iter(int lpr);
 int gemv_lpr(int K, int wtype);
 
 hipError_t launch_mfma(int epi, int wtype, const MfmaArgs& a, hipStream_t s);
+// true where the cloud projection can quantise blocks of 256 positions in its epilogue
+bool mfma_quantises_in_epilogue(int M, int K);
 int mfma_n_tiles(int n);
 
 // Clip + quantise z [M, n] to b-bit codes (bits 8 or 4; 4-bit codes two per

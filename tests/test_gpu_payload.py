@@ -35,6 +35,9 @@ SHAPES = [
     (8, 5, 1032, 0, 4000, 2560),     # 40 rows, d_end = 0, 16-byte payload rows at b = 4
     (13, 10, 2056, 8, 9000, 8193),   # 130 rows: 256-row tile
     (24, 25, 1096, 72, 9000, 4097),  # 600 rows: two 320-row tiles, the second ragged
+    # K a multiple of 64: at block 256 the projection's epilogue quantises
+    (3, 3, 1088, 64, 5000, 2501),    # 9 rows: 32-row tile
+    (8, 5, 1088, 64, 4000, 2560),    # 40 rows: 128-row tile
 ]
 
 
@@ -155,3 +158,22 @@ def test_payload_format_sampling():
     np.testing.assert_array_equal(ah, oracle.accept_lengths(th, drafts, cfg.sessions,
                                                             cfg.rows_per_session))
     say(f"[gpu] payload sampling: ok, exempt {int(exempt.sum())}")
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_epilogue_quantiser_without_z(bits):
+    # block 256 on the MFMA path: the payload is the same whether or not the
+    # fp32 partials are also written
+    cfg = Config("payload_noz", 74, d=2112, d_end=64, vocab=9000, n_sub=6001, subset_kind="choice",
+                 sessions=60, rows_per_session=5)
+    wl = make_workload(cfg)
+    dw = P.DeviceWorkload(wl)
+    say(f"[gpu] epilogue quantiser b={bits}: with and without z")
+    q1, s1, z1 = dw.cloud(want_z=True, bits=bits, block=256)
+    q2, s2, z2 = dw.cloud(want_z=False, bits=bits, block=256)
+    torch.cuda.synchronize()
+    assert z2 is None
+    np.testing.assert_array_equal(P.host(q1), P.host(q2))
+    np.testing.assert_array_equal(P.host(s1).view(np.uint32), P.host(s2).view(np.uint32))
+    codes = P.stage_b_fmt(P.host(z1), P.host(q1).view(np.uint8), P.host(s1), cfg.clip_c, bits, 256)
+    assert codes.shape == (cfg.M, len(wl.subset))
