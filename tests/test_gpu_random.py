@@ -1,0 +1,56 @@
+"""Seeded random configurations through the staged parity checks.
+
+Each case draws a shape (sessions, rows per session, d, d_end, V, |S|) within
+the documented limits, a weight type and a payload format, so that the
+skinny and MFMA projections, every row tile, ragged tiles on both axes,
+bf16 and fp8 weights, every payload format and the hidden-state codes meet
+shapes no hand-picked case has.  The checks are those of the format and
+hidden-code tests (stages A-E of tests/parity.py)."""
+
+import numpy as np
+import pytest
+
+from synth import Config, make_workload
+
+from test_gpu_hidden import run_hq_case
+from test_gpu_payload import run_format_case
+
+pytestmark = pytest.mark.gpu
+
+_FORMATS = [(8, 0), (4, 0), (4, 256), (8, 256), (4, 1024), (8, 4096)]
+
+
+def _draw(i, rng):
+    sessions = int(rng.integers(1, 21))
+    R = int(rng.integers(1, 10))
+    wtype = "fp8" if rng.random() < 0.3 else "bf16"
+    step = 16 if wtype == "fp8" else 8
+    d_end = int(rng.choice([0, 8, 40, 64, 72, 128, 256, 264, 512]))
+    d_cloud = step * int(rng.integers(1, 2048 // step + 1))
+    n = int(rng.integers(1, 12001))
+    V = n + int(rng.integers(0, 8000))
+    bits, block = _FORMATS[int(rng.integers(0, len(_FORMATS)))]
+    hq = rng.random() < 0.35
+    return dict(i=i, sessions=sessions, R=R, d=d_end + d_cloud, d_end=d_end, V=V, n=n,
+                wtype=wtype, bits=bits, block=block, hq=hq)
+
+
+_RNG = np.random.default_rng(2607)
+CASES = [_draw(i, _RNG) for i in range(24)]
+
+
+def _id(c):
+    return (f"{c['i']}-S{c['sessions']}R{c['R']}d{c['d']}de{c['d_end']}n{c['n']}"
+            f"-{c['wtype']}-b{c['bits']}k{c['block']}{'-hq' if c['hq'] else ''}")
+
+
+@pytest.mark.parametrize("c", CASES, ids=[_id(c) for c in CASES])
+def test_random_configuration(c):
+    cfg = Config("random", 300 + c["i"], d=c["d"], d_end=c["d_end"], vocab=c["V"], n_sub=c["n"],
+                 subset_kind="choice", sessions=c["sessions"], rows_per_session=c["R"],
+                 wtype=c["wtype"], with_bias=bool(c["i"] % 3 == 0))
+    wl = make_workload(cfg)
+    if c["hq"]:
+        run_hq_case(wl, f"random {_id(c)}", bits=c["bits"], block=c["block"])
+    else:
+        run_format_case(wl, c["bits"], c["block"], f"random {_id(c)}")
