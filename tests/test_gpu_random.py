@@ -14,6 +14,7 @@ from synth import Config, make_workload
 
 from test_gpu_hidden import run_hq_case
 from test_gpu_payload import run_format_case
+from test_gpu_sampling import run_sample_case
 
 pytestmark = pytest.mark.gpu
 
@@ -54,3 +55,26 @@ def test_random_configuration(c):
         run_hq_case(wl, f"random {_id(c)}", bits=c["bits"], block=c["block"])
     else:
         run_format_case(wl, c["bits"], c["block"], f"random {_id(c)}")
+
+
+def _draw_sample(i, rng):
+    c = _draw(100 + i, rng)
+    c["tau"] = float(np.round(rng.uniform(0.2, 2.0), 3))
+    c["top_p"] = float(np.round(rng.choice([rng.uniform(0.05, 0.99), 1.0]), 3))
+    return c
+
+
+_RNG_S = np.random.default_rng(2608)
+SAMPLE_CASES = [_draw_sample(i, _RNG_S) for i in range(10)]
+
+
+@pytest.mark.parametrize("c", SAMPLE_CASES,
+                         ids=[f"{c['i']}-S{c['sessions']}R{c['R']}d{c['d']}de{c['d_end']}n{c['n']}-"
+                              f"{c['wtype']}-t{c['tau']}-p{c['top_p']}" for c in SAMPLE_CASES])
+def test_random_sampling_configuration(c):
+    cfg = Config("random_sample", 500 + c["i"], d=c["d"], d_end=c["d_end"], vocab=c["V"],
+                 n_sub=c["n"], subset_kind="choice", sessions=c["sessions"],
+                 rows_per_session=c["R"], wtype=c["wtype"], mode="sample",
+                 temperature=c["tau"], top_p=c["top_p"],
+                 philox_seed=0x2607_1309_0000_0000 + c["i"])
+    run_sample_case(make_workload(cfg), tag=f"random sample {c['i']}")
