@@ -340,25 +340,21 @@ def main():
     ws_c = torch.empty(max(1, sph.cloud_partial_workspace(M, sub)), dtype=torch.uint8, device=dev)
     ws_f = torch.empty(max(1, sph.fuse_verify_workspace(M, sub, mode)), dtype=torch.uint8, device=dev)
     if args.seal:
+        # one message per payload row: its codes, then its scales
         gkey = sph.GcmKey(bytes(range(16)))
         s_bytes = s.view(torch.uint8).reshape(M, -1)
-        iv_q = torch.zeros((M, 12), dtype=torch.uint8, device=dev)
-        iv_s = torch.zeros((M, 12), dtype=torch.uint8, device=dev)
+        iv = torch.zeros((M, 12), dtype=torch.uint8, device=dev)
         rows_idx = torch.arange(M, device=dev)
-        for ivt in (iv_q, iv_s):                            # row number, big-endian, in the last 3 bytes
-            ivt[:, 9] = (rows_idx >> 16).to(torch.uint8)
-            ivt[:, 10] = ((rows_idx >> 8) & 255).to(torch.uint8)
-            ivt[:, 11] = (rows_idx & 255).to(torch.uint8)
-        iv_s[:, 4] = 1                                      # message type: scales
+        iv[:, 9] = (rows_idx >> 16).to(torch.uint8)        # row number, big-endian, in the last 3 bytes
+        iv[:, 10] = ((rows_idx >> 8) & 255).to(torch.uint8)
+        iv[:, 11] = (rows_idx & 255).to(torch.uint8)
         aad = torch.zeros((M, 16), dtype=torch.uint8, device=dev)
         cq = torch.empty_like(q, dtype=torch.uint8)
         cs = torch.empty_like(s_bytes)
-        tq = torch.empty((M, 16), dtype=torch.uint8, device=dev)
-        ts = torch.empty((M, 16), dtype=torch.uint8, device=dev)
-        okq = torch.empty((M,), dtype=torch.int32, device=dev)
-        oks = torch.empty((M,), dtype=torch.int32, device=dev)
-        ws_g = torch.empty(max(1, sph.gcm_workspace(M, q.shape[1] * q.element_size())), dtype=torch.uint8,
-                           device=dev)
+        tg = torch.empty((M, 16), dtype=torch.uint8, device=dev)
+        okm = torch.empty((M,), dtype=torch.int32, device=dev)
+        msg_bytes = q.shape[1] * q.element_size() + s_bytes.shape[1]
+        ws_g = torch.empty(max(1, sph.gcm_workspace(M, msg_bytes)), dtype=torch.uint8, device=dev)
     hq = torch.empty((M, cfg.d), dtype=torch.int8, device=dev)
     hs = torch.empty((M,), dtype=torch.float32, device=dev)
     if args.hidden_int8:
@@ -372,10 +368,9 @@ def main():
                           out=(q, s, None), bits=bits, block=block)
         if args.seal:
             qb = q.view(torch.uint8)
-            sph.gcm_seal(gkey, qb, iv_q, aad, out=(cq, tq), workspace=ws_g)
-            sph.gcm_seal(gkey, s_bytes, iv_s, aad, out=(cs, ts), workspace=ws_g)
-            sph.gcm_open(gkey, cq, iv_q, tq, aad, out=(qb, okq), workspace=ws_g)
-            sph.gcm_open(gkey, cs, iv_s, ts, aad, out=(s_bytes, oks), workspace=ws_g)
+            sph.gcm_seal_segments(gkey, (qb, s_bytes), iv, aad, out=(cq, cs), tag=tg, workspace=ws_g)
+            sph.gcm_open_segments(gkey, (cq, cs), iv, tg, aad, out=(qb, s_bytes), ok=okm,
+                                  workspace=ws_g)
         if args.hidden_int8:
             sph.hidden_quantize(h, out=(hq, hs))
             sph.fuse_verify_hq(q, s, hq, hs, de, we[c], sub, cfg.sessions, cfg.rows_per_session,
@@ -413,6 +408,8 @@ def main():
 
     # Timed region: K steps, no instrumentation.
     ms_step = timed_loop()
+    if args.seal and int(okm.min()) != 1:
+        raise SystemExit("sealed payload rows failed authentication")
     # Kernel durations: the same K steps again with the library's trace on
     # (HIP events recorded on the launch stream around every kernel).
     cap = 16 * args.steps + 16
@@ -473,7 +470,7 @@ def main():
                                        f"one scale per {block} positions"),
             "payload_bytes_per_row": code_bytes + 4 * nb,
             "hidden_state": "int8 codes + fp32 scale per row" if args.hidden_int8 else "bf16",
-            "sealed": "AES-128-GCM per row (codes, scales)" if args.seal else "no",
+            "sealed": "AES-128-GCM, one message per row (codes, then scales)" if args.seal else "no",
         },
         "roofline": roof,
         "attainable": att,

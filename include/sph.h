@@ -257,11 +257,12 @@ int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t bloc
  * counter 2) with associated data aad[m] (aad_bytes bytes, e.g. session,
  * block and cache-control fields).  A nonce must never repeat under one
  * key; the caller chooses the scheme (the paper derives GPU-mode nonces from
- * the session and the message type).  Seal codes and scales of a payload as
- * two batches (two message types).  All buffers are device memory; rows are
- * ld_* bytes apart, iv [rows][12], tag [rows][16].  Limits: rows <= 65535,
- * aad_bytes <= 1024, ceil(aad_bytes/16) + ceil(row_bytes/16) + 1 <= 16384.
- * Seal and open may work in place (out == in, same stride).
+ * the session and the message type).  A payload row's codes and scales can
+ * be sealed as one message (sph_gcm_seal_segments) or as two batches (two
+ * message types).  All buffers are device memory; rows are ld_* bytes apart,
+ * iv [rows][12], tag [rows][16].  Limits: rows <= 65535, aad_bytes <= 1024,
+ * ceil(aad_bytes/16) + ceil(row_bytes/16) + 1 <= 16384.  Seal and open may
+ * work in place (out == in, same stride).
  */
 typedef struct sph_gcm_key_s* sph_gcm_key;
 
@@ -287,6 +288,37 @@ int sph_gcm_open(sph_gcm_key key, const void* ct, int64_t ld_ct, int64_t rows, i
                  const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
                  const uint8_t* tag, void* pt, int64_t ld_pt, int32_t* ok_out, void* workspace,
                  size_t ws_bytes, void* stream);
+
+/* Messages made of several row-aligned pieces: message m is the
+ * concatenation, in order, of row m of each segment (bytes bytes of
+ * in + m * ld_in), and its output bytes go to the same places of out +
+ * m * ld_out.  E.g. one payload row = its codes followed by its scales, with
+ * no copy into a staging buffer.  `segments` is a host array of nseg (1 ..
+ * SPH_GCM_MAX_SEGMENTS) entries, read during the call only; a segment may
+ * be empty (bytes = 0, pointers unused).  Segments must not overlap one
+ * another; each may work in place (out == in, ld_out == ld_in).  The
+ * message length is the sum of the segment lengths; the workspace is
+ * sph_gcm_workspace(rows, that sum), and every limit above applies to it.
+ * The result is that of sph_gcm_seal / sph_gcm_open on the concatenated
+ * rows. */
+#define SPH_GCM_MAX_SEGMENTS 4
+typedef struct {
+  const void* in;  /* device, rows x bytes, ld_in bytes apart */
+  int64_t ld_in;
+  void* out;       /* device, rows x bytes, ld_out bytes apart */
+  int64_t ld_out;
+  int64_t bytes;   /* bytes this segment adds to each message */
+} sph_gcm_segment;
+
+int sph_gcm_seal_segments(sph_gcm_key key, const sph_gcm_segment* segments, int nseg, int64_t rows,
+                          const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                          uint8_t* tag, void* workspace, size_t ws_bytes, void* stream);
+
+/* Opening counterpart: ok_out[m] as in sph_gcm_open. */
+int sph_gcm_open_segments(sph_gcm_key key, const sph_gcm_segment* segments, int nseg, int64_t rows,
+                          const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                          const uint8_t* tag, int32_t* ok_out, void* workspace, size_t ws_bytes,
+                          void* stream);
 
 /*
  * Kernel tracing.  While a trace is active, each call records one duration

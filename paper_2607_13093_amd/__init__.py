@@ -19,6 +19,8 @@ from .api import (  # noqa: F401
     GcmKey,
     gcm_seal,
     gcm_open,
+    gcm_seal_segments,
+    gcm_open_segments,
     gcm_workspace,
     fuse_verify_hq,
     fuse_verify_hq_workspace,

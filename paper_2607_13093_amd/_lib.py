@@ -81,6 +81,15 @@ SIGNATURES = {
         c_vp, c_vp, c_i64, c_i64,           # iv, aad, ld_aad, aad_bytes
         c_vp, c_vp, c_i64, c_vp,            # tag, pt, ld_pt, ok_out
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_gcm_seal_segments": (ctypes.c_int, [
+        c_vp, c_vp, ctypes.c_int, c_i64,    # key, segments, nseg, rows
+        c_vp, c_vp, c_i64, c_i64,           # iv, aad, ld_aad, aad_bytes
+        c_vp, c_vp, ctypes.c_size_t, c_vp]),  # tag, workspace, ws_bytes, stream
+    "sph_gcm_open_segments": (ctypes.c_int, [
+        c_vp, c_vp, ctypes.c_int, c_i64,    # key, segments, nseg, rows
+        c_vp, c_vp, c_i64, c_i64,           # iv, aad, ld_aad, aad_bytes
+        c_vp, c_vp,                         # tag, ok_out
+        c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
     "sph_trace_start": (ctypes.c_int, [ctypes.c_int]),
     "sph_trace_stop": (ctypes.c_int, [c_vp, ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
     # include/sph_probe.h
@@ -91,6 +100,15 @@ SIGNATURES = {
 
 class TraceRecord(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_char * 32), ("ms", ctypes.c_float)]
+
+
+class GcmSegment(ctypes.Structure):
+    """sph_gcm_segment."""
+    _fields_ = [("in_", c_vp), ("ld_in", c_i64), ("out", c_vp), ("ld_out", c_i64),
+                ("bytes", c_i64)]
+
+
+SPH_GCM_MAX_SEGMENTS = 4
 
 
 SPH_OK = 0

@@ -187,6 +187,79 @@ def gcm_open(key: GcmKey, ct: torch.Tensor, iv: torch.Tensor, tag: torch.Tensor,
     return pt, ok
 
 
+def _segment_array(ins, outs, rows: int, what: str):
+    if not 1 <= len(ins) <= _lib.SPH_GCM_MAX_SEGMENTS or len(outs) != len(ins):
+        raise ValueError(f"{what}: 1..{_lib.SPH_GCM_MAX_SEGMENTS} segments with one output each")
+    arr = (_lib.GcmSegment * len(ins))()
+    total = 0
+    for k, (a, b) in enumerate(zip(ins, outs)):
+        r, nb, ld = _rows_u8(a, f"{what} segment {k}")
+        ro, nbo, ldo = _rows_u8(b, f"{what} output {k}")
+        if r != rows or ro != rows or nbo != nb:
+            raise ValueError(f"{what}: segment {k} is {r} x {nb} bytes, output {ro} x {nbo}, rows {rows}")
+        arr[k] = _lib.GcmSegment(a.data_ptr(), ld, b.data_ptr(), ldo, nb)
+        total += nb
+    return arr, total
+
+
+def gcm_seal_segments(key: GcmKey, segments, iv: torch.Tensor, aad: Optional[torch.Tensor] = None,
+                      out=None, tag: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None):
+    """Seal messages that are the concatenation of row m of each tensor in
+    `segments` (2-D device tensors with the same number of rows, e.g. the
+    payload codes and their scales).  Returns ([ct per segment, uint8, same
+    rows x bytes], tag uint8 [rows, 16]); pass `out` (a list of uint8
+    tensors, may be the inputs themselves) to write in place."""
+    lib = _lib.load()
+    segments = list(segments)
+    rows = segments[0].shape[0] if segments else 0
+    dev = segments[0].device if segments else torch.device("cuda")
+    if out is None:
+        out = [torch.empty((rows, _rows_u8(a, "segment")[1]), dtype=torch.uint8, device=dev)
+               for a in segments]
+    arr, total = _segment_array(segments, list(out), rows, "gcm_seal_segments")
+    _check_msg_args(rows, iv, aad)
+    if tag is None:
+        tag = torch.empty((rows, 16), dtype=torch.uint8, device=dev)
+    _check_bytes(tag, "tag", (rows, 16))
+    na = 0 if aad is None else aad.shape[1]
+    if workspace is None:
+        workspace = torch.empty(max(gcm_workspace(rows, total), 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_gcm_seal_segments(key.handle, arr, len(segments), rows, iv.data_ptr(), _ptr(aad),
+                                    aad.stride(0) if aad is not None else 0, na, tag.data_ptr(),
+                                    workspace.data_ptr(), workspace.numel(), _stream_handle(dev)))
+    return list(out), tag
+
+
+def gcm_open_segments(key: GcmKey, segments, iv: torch.Tensor, tag: torch.Tensor,
+                      aad: Optional[torch.Tensor] = None, out=None, ok: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None):
+    """Open messages sealed by gcm_seal_segments; returns ([pt per segment],
+    ok int32 [rows]) with ok[m] = 1 when message m's tag verifies."""
+    lib = _lib.load()
+    segments = list(segments)
+    rows = segments[0].shape[0] if segments else 0
+    dev = segments[0].device if segments else torch.device("cuda")
+    if out is None:
+        out = [torch.empty((rows, _rows_u8(a, "segment")[1]), dtype=torch.uint8, device=dev)
+               for a in segments]
+    arr, total = _segment_array(segments, list(out), rows, "gcm_open_segments")
+    _check_msg_args(rows, iv, aad)
+    _check_bytes(tag, "tag", (rows, 16))
+    if ok is None:
+        ok = torch.empty((rows,), dtype=torch.int32, device=dev)
+    elif ok.dtype != torch.int32 or tuple(ok.shape) != (rows,) or not ok.is_cuda:
+        raise ValueError(f"ok: expected int32 ({rows},) on the GPU")
+    na = 0 if aad is None else aad.shape[1]
+    if workspace is None:
+        workspace = torch.empty(max(gcm_workspace(rows, total), 1), dtype=torch.uint8, device=dev)
+    check(lib.sph_gcm_open_segments(key.handle, arr, len(segments), rows, iv.data_ptr(), _ptr(aad),
+                                    aad.stride(0) if aad is not None else 0, na, tag.data_ptr(),
+                                    ok.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                    _stream_handle(dev)))
+    return list(out), ok
+
+
 def ctypes_vp():
     return _lib.c_vp()
 

@@ -166,14 +166,46 @@ bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_
 // device
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ void load_be_words(const uint8_t* p, int valid, uint32_t w[4]) {
-  uint8_t b[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) b[i] = i < valid ? p[i] : 0;
+__device__ __forceinline__ void pack_be_words(const uint8_t b[16], uint32_t w[4]) {
 #pragma unroll
   for (int k = 0; k < 4; ++k)
     w[k] = ((uint32_t)b[4 * k] << 24) | ((uint32_t)b[4 * k + 1] << 16) | ((uint32_t)b[4 * k + 2] << 8) |
            b[4 * k + 3];
+}
+
+__device__ __forceinline__ void load_be_words(const uint8_t* p, int valid, uint32_t w[4]) {
+  uint8_t b[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) b[i] = i < valid ? p[i] : 0;
+  pack_be_words(b, w);
+}
+
+// Segment of a message row that holds message byte p (p < L): the last
+// segment starting at or before p, so empty segments are passed over.
+__device__ __forceinline__ int seg_of(const GcmSegs& g, int64_t p, int64_t& start) {
+  int s = 0;
+  start = 0;
+#pragma unroll
+  for (int k = 0; k < kGcmMaxSegs - 1; ++k)
+    if (k + 1 < g.nseg && p >= g.end[k]) {
+      s = k + 1;
+      start = g.end[k];
+    }
+  return s;
+}
+
+template <typename T>
+__device__ __forceinline__ T* seg_ptr(T* const (&base)[kGcmMaxSegs], const int64_t (&ld)[kGcmMaxSegs],
+                                      int s, int64_t row, int64_t off) {
+  T* b = base[0];
+  int64_t l = ld[0];
+#pragma unroll
+  for (int k = 1; k < kGcmMaxSegs; ++k)
+    if (s == k) {
+      b = base[k];
+      l = ld[k];
+    }
+  return b + row * l + off;
 }
 
 struct GcmShared {
@@ -195,9 +227,8 @@ __device__ __forceinline__ void stage_key(GcmShared& sh, const uint8_t* key_dev,
 // One thread per 16-byte block of a row (grid: blocks / 256 x rows).
 template <bool OPEN>
 __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ key_dev, int nr,
-                                                    const uint8_t* __restrict__ in, int64_t ld_in,
-                                                    uint8_t* __restrict__ out, int64_t ld_out,
-                                                    int64_t L, int n, const uint8_t* __restrict__ iv,
+                                                    const GcmSegs segs, int64_t L, int n,
+                                                    const uint8_t* __restrict__ iv,
                                                     uint32_t* __restrict__ partial, int nparts) {
   __shared__ GcmShared sh;
   stage_key(sh, key_dev, nr);
@@ -212,16 +243,49 @@ __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ 
     ctr[3] = (uint32_t)(2 + j);  // inc32 from J0 + 1
     uint32_t ks[4];
     aes_block(sh.te, sh.sb, sh.rk, nr, ctr, ks);
-    const int valid = (int)min<int64_t>(16, L - (int64_t)j * 16);
-    const uint8_t* src = in + row * ld_in + (int64_t)j * 16;
-    uint8_t* dst = out + row * ld_out + (int64_t)j * 16;
+    const int64_t p0 = (int64_t)j * 16;
+    const int valid = (int)min<int64_t>(16, L - p0);
+    int64_t st;
+    const int s0 = seg_of(segs, p0, st);
+    int64_t e0 = segs.end[0];
+#pragma unroll
+    for (int k = 1; k < kGcmMaxSegs; ++k)
+      if (s0 == k) e0 = segs.end[k];
+    // a block inside one segment takes the plain path; one that straddles
+    // a segment boundary maps every byte on its own
+    const bool whole = p0 + valid <= e0;
     uint32_t x[4], y[4];
-    load_be_words(src, valid, x);
+    if (whole) {
+      load_be_words(seg_ptr(segs.in, segs.ld_in, s0, row, p0 - st), valid, x);
+    } else {
+      uint8_t b[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        b[i] = 0;
+        if (i < valid) {
+          int64_t sti;
+          const int si = seg_of(segs, p0 + i, sti);
+          b[i] = *seg_ptr(segs.in, segs.ld_in, si, row, p0 + i - sti);
+        }
+      }
+      pack_be_words(b, x);
+    }
 #pragma unroll
     for (int k = 0; k < 4; ++k) y[k] = x[k] ^ ks[k];
+    if (whole) {
+      uint8_t* dst = seg_ptr(segs.out, segs.ld_out, s0, row, p0 - st);
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+      for (int i = 0; i < 16; ++i)
+        if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (i < valid) {
+          int64_t sti;
+          const int si = seg_of(segs, p0 + i, sti);
+          *seg_ptr(segs.out, segs.ld_out, si, row, p0 + i - sti) = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+        }
+    }
     // the GHASH input is the ciphertext: the output when sealing, the input
     // when opening; bytes past the message are zero
     uint32_t c[4];
@@ -302,21 +366,22 @@ __global__ __launch_bounds__(256) void k_gcm_finish(const uint8_t* __restrict__ 
   }
 }
 
-hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const uint8_t* in, int64_t ld_in,
-                      uint8_t* out, int64_t ld_out, int rows, int64_t L, const uint8_t* iv,
-                      const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag, int32_t* ok,
-                      uint32_t* partial, hipStream_t s) {
+hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const GcmSegs& segs, int rows,
+                      const uint8_t* iv, const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag,
+                      int32_t* ok, uint32_t* partial, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (segs.nseg < 1 || segs.nseg > kGcmMaxSegs) return hipErrorInvalidValue;
+  const int64_t L = segs.end[segs.nseg - 1];
   const int n = (int)((L + 15) / 16);
   const int nparts = (n + 255) / 256;
   if (rows > 65535 && nparts > 0) return hipErrorInvalidValue;
   if (nparts > 0) {
     if (open)
-      launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, in, ld_in,
-                    out, ld_out, L, n, iv, partial, nparts);
+      launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, segs, L, n,
+                    iv, partial, nparts);
     else
-      launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, in, ld_in,
-                    out, ld_out, L, n, iv, partial, nparts);
+      launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, segs, L, n,
+                    iv, partial, nparts);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -649,24 +649,42 @@ size_t sph_gcm_workspace(int64_t rows, int64_t row_bytes) {
 
 namespace {
 
-int gcm_call(const char* fn, bool open, sph_gcm_key key, const void* in, int64_t ld_in,
-             int64_t rows, int64_t row_bytes, const uint8_t* iv, const void* aad, int64_t ld_aad,
-             int64_t aad_bytes, void* out, int64_t ld_out, uint8_t* tag, int32_t* okf,
-             void* workspace, size_t ws_bytes, void* stream) {
+int gcm_call(const char* fn, bool open, sph_gcm_key key, const sph_gcm_segment* segs, int nseg,
+             int64_t rows, const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+             uint8_t* tag, int32_t* okf, void* workspace, size_t ws_bytes, void* stream) {
   if (!key) return fail(SPH_E_INVALID_ARG, "%s: key is NULL", fn);
+  if (!segs || nseg < 1 || nseg > SPH_GCM_MAX_SEGMENTS)
+    return fail(SPH_E_INVALID_ARG, "%s: nseg=%d not in [1, %d] (or segments NULL)", fn, nseg,
+                SPH_GCM_MAX_SEGMENTS);
   if (rows < 0 || rows > 65535) return fail(SPH_E_INVALID_ARG, "%s: rows=%lld out of range", fn, (long long)rows);
-  if (row_bytes < 0) return fail(SPH_E_INVALID_ARG, "%s: row_bytes=%lld", fn, (long long)row_bytes);
+  sph::GcmSegs g{};
+  g.nseg = nseg;
+  int64_t row_bytes = 0;
+  for (int k = 0; k < nseg; ++k) {
+    const sph_gcm_segment& sg = segs[k];
+    if (sg.bytes < 0 || sg.bytes > (int64_t)sph::kGcmMaxPow * 16)
+      return fail(SPH_E_INVALID_ARG, "%s: segment %d has %lld bytes", fn, k, (long long)sg.bytes);
+    if (sg.ld_in < sg.bytes || sg.ld_out < sg.bytes)
+      return fail(SPH_E_INVALID_ARG, "%s: segment %d: row strides below the row length", fn, k);
+    if (rows > 0 && sg.bytes > 0 && (!sg.in || !sg.out))
+      return fail(SPH_E_INVALID_ARG, "%s: segment %d: input/output is NULL", fn, k);
+    row_bytes += sg.bytes;
+    g.in[k] = static_cast<const uint8_t*>(sg.in);
+    g.out[k] = static_cast<uint8_t*>(sg.out);
+    g.ld_in[k] = sg.ld_in;
+    g.ld_out[k] = sg.ld_out;
+    g.end[k] = row_bytes;
+  }
   if (aad_bytes < 0 || aad_bytes > 1024)
     return fail(SPH_E_INVALID_ARG, "%s: aad_bytes=%lld not in [0, 1024]", fn, (long long)aad_bytes);
   const int64_t m = (aad_bytes + 15) / 16 + (row_bytes + 15) / 16 + 1;
   if (m > sph::kGcmMaxPow)
     return fail(SPH_E_UNSUPPORTED, "%s: message of %lld bytes (+%lld AAD) exceeds %d blocks", fn,
                 (long long)row_bytes, (long long)aad_bytes, sph::kGcmMaxPow);
-  if (ld_in < row_bytes || ld_out < row_bytes || (aad_bytes > 0 && ld_aad < aad_bytes))
-    return fail(SPH_E_INVALID_ARG, "%s: row strides below the row lengths", fn);
+  if (aad_bytes > 0 && ld_aad < aad_bytes)
+    return fail(SPH_E_INVALID_ARG, "%s: AAD row stride below the AAD length", fn);
   if (rows == 0) return ok();
   if (!iv || !tag || (open && !okf)) return fail(SPH_E_INVALID_ARG, "%s: iv/tag/ok is NULL", fn);
-  if (row_bytes > 0 && (!in || !out)) return fail(SPH_E_INVALID_ARG, "%s: input/output is NULL", fn);
   if (aad_bytes > 0 && !aad) return fail(SPH_E_INVALID_ARG, "%s: aad is NULL", fn);
   const size_t need = sph_gcm_workspace(rows, row_bytes);
   if (need > 0 && (!workspace || ws_bytes < need))
@@ -674,8 +692,7 @@ int gcm_call(const char* fn, bool open, sph_gcm_key key, const void* in, int64_t
                 workspace ? ws_bytes : (size_t)0);
   hipStream_t s = (hipStream_t)stream;
   hipError_t e = traced(open ? "gcm_open" : "gcm_seal", s, [&] {
-    return sph::launch_gcm(open, key->d_image, key->nr, static_cast<const uint8_t*>(in), ld_in,
-                           static_cast<uint8_t*>(out), ld_out, (int)rows, row_bytes, iv,
+    return sph::launch_gcm(open, key->d_image, key->nr, g, (int)rows, iv,
                            static_cast<const uint8_t*>(aad), ld_aad, (int)aad_bytes, tag, okf,
                            static_cast<uint32_t*>(workspace), s);
   });
@@ -688,16 +705,33 @@ int gcm_call(const char* fn, bool open, sph_gcm_key key, const void* in, int64_t
 int sph_gcm_seal(sph_gcm_key key, const void* pt, int64_t ld_pt, int64_t rows, int64_t row_bytes,
                  const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes, void* ct,
                  int64_t ld_ct, uint8_t* tag, void* workspace, size_t ws_bytes, void* stream) {
-  return gcm_call("sph_gcm_seal", false, key, pt, ld_pt, rows, row_bytes, iv, aad, ld_aad, aad_bytes,
-                  ct, ld_ct, tag, nullptr, workspace, ws_bytes, stream);
+  const sph_gcm_segment sg{pt, ld_pt, ct, ld_ct, row_bytes};
+  return gcm_call("sph_gcm_seal", false, key, &sg, 1, rows, iv, aad, ld_aad, aad_bytes, tag, nullptr,
+                  workspace, ws_bytes, stream);
 }
 
 int sph_gcm_open(sph_gcm_key key, const void* ct, int64_t ld_ct, int64_t rows, int64_t row_bytes,
                  const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
                  const uint8_t* tag, void* pt, int64_t ld_pt, int32_t* ok_out, void* workspace,
                  size_t ws_bytes, void* stream) {
-  return gcm_call("sph_gcm_open", true, key, ct, ld_ct, rows, row_bytes, iv, aad, ld_aad, aad_bytes,
-                  pt, ld_pt, const_cast<uint8_t*>(tag), ok_out, workspace, ws_bytes, stream);
+  const sph_gcm_segment sg{ct, ld_ct, pt, ld_pt, row_bytes};
+  return gcm_call("sph_gcm_open", true, key, &sg, 1, rows, iv, aad, ld_aad, aad_bytes,
+                  const_cast<uint8_t*>(tag), ok_out, workspace, ws_bytes, stream);
+}
+
+int sph_gcm_seal_segments(sph_gcm_key key, const sph_gcm_segment* segments, int nseg, int64_t rows,
+                          const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                          uint8_t* tag, void* workspace, size_t ws_bytes, void* stream) {
+  return gcm_call("sph_gcm_seal_segments", false, key, segments, nseg, rows, iv, aad, ld_aad, aad_bytes,
+                  tag, nullptr, workspace, ws_bytes, stream);
+}
+
+int sph_gcm_open_segments(sph_gcm_key key, const sph_gcm_segment* segments, int nseg, int64_t rows,
+                          const uint8_t* iv, const void* aad, int64_t ld_aad, int64_t aad_bytes,
+                          const uint8_t* tag, int32_t* ok_out, void* workspace, size_t ws_bytes,
+                          void* stream) {
+  return gcm_call("sph_gcm_open_segments", true, key, segments, nseg, rows, iv, aad, ld_aad, aad_bytes,
+                  const_cast<uint8_t*>(tag), ok_out, workspace, ws_bytes, stream);
 }
 
 int sph_trace_start(int capacity) {

@@ -162,11 +162,24 @@ constexpr int kGcmRkOffset = 1280;
 constexpr int kGcmPowOffset = 1536;
 constexpr size_t kGcmImageBytes = (size_t)kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16;
 bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_image, int& nr);
-// rows <= 65535 messages of L bytes; partial: rows * ceil(ceil(L/16)/256) * 16 bytes
-hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const uint8_t* in, int64_t ld_in,
-                      uint8_t* out, int64_t ld_out, int rows, int64_t L, const uint8_t* iv,
-                      const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag, int32_t* ok,
-                      uint32_t* partial, hipStream_t s);
+// A message row is the concatenation of up to kGcmMaxSegs segments: bytes
+// [end[k-1], end[k]) of row r come from in[k] + r * ld_in[k] and go to
+// out[k] + r * ld_out[k] (end[-1] = 0; empty segments allowed).  Passed to
+// the kernels by value.
+constexpr int kGcmMaxSegs = 4;
+struct GcmSegs {
+  const uint8_t* in[kGcmMaxSegs];
+  uint8_t* out[kGcmMaxSegs];
+  int64_t ld_in[kGcmMaxSegs];
+  int64_t ld_out[kGcmMaxSegs];
+  int64_t end[kGcmMaxSegs];
+  int nseg;
+};
+// rows <= 65535 messages of L = segs.end[nseg-1] bytes; partial:
+// rows * ceil(ceil(L/16)/256) * 16 bytes
+hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const GcmSegs& segs, int rows,
+                      const uint8_t* iv, const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag,
+                      int32_t* ok, uint32_t* partial, hipStream_t s);
 
 // Measurement kernels (probe.hip).
 hipError_t launch_probe_read(const void* buf, int64_t bytes, float* sink, hipStream_t s);

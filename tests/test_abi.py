@@ -220,6 +220,41 @@ def test_gcm_validation(lib):
     lib.sph_gcm_key_destroy(None)
 
 
+def _segs(*specs):
+    arr = (_lib.GcmSegment * max(len(specs), 1))()
+    for k, (src, ld_in, dst, ld_out, nb) in enumerate(specs):
+        arr[k] = _lib.GcmSegment(src, ld_in, dst, ld_out, nb)
+    return arr
+
+
+@pytest.mark.parametrize("segs,nseg,rows,aad,code,msg", [
+    (_segs((1, 16, 1, 16, 16)), 0, 1, 0, -1, b"nseg=0"),
+    (_segs(*[(1, 16, 1, 16, 16)] * 4), 5, 1, 0, -1, b"nseg=5"),
+    (None, 1, 1, 0, -1, b"segments NULL"),
+    (_segs((1, 16, 1, 16, 16), (1, 8, 1, 8, -1)), 2, 1, 0, -1, b"segment 1 has -1 bytes"),
+    (_segs((1, 16, 1, 16, 16), (1, 7, 1, 8, 8)), 2, 1, 0, -1, b"segment 1: row strides"),
+    (_segs((1, 16, 1, 16, 16), (None, 8, 1, 8, 8)), 2, 1, 0, -1, b"segment 1: input/output is NULL"),
+    (_segs((1, 16, 1, 16, 16), (1, 8, 1, 8, 8)), 2, 65536, 0, -1, b"rows=65536"),
+    (_segs((1, 1 << 18, 1, 1 << 18, 1 << 17), (1, 1 << 18, 1, 1 << 18, 1 << 17)), 2, 1, 0, -3,
+     b"exceeds 16384 blocks"),
+    (_segs((1, 16, 1, 16, 16)), 1, 1, 2000, -1, b"aad_bytes=2000"),
+])
+def test_gcm_segment_validation(lib, segs, nseg, rows, aad, code, msg):
+    # a dummy key handle: every case is rejected on the host before the key
+    # or any buffer is touched
+    rc = lib.sph_gcm_seal_segments(1, segs, nseg, rows, 1, 1, 2048, aad, 1, 1, 1 << 20, None)
+    assert rc == code and msg in lib.sph_last_error(), lib.sph_last_error()
+    rc = lib.sph_gcm_open_segments(1, segs, nseg, rows, 1, 1, 2048, aad, 1, 1, 1, 1 << 20, None)
+    assert rc == code and msg in lib.sph_last_error(), lib.sph_last_error()
+
+
+def test_gcm_segments_empty_batch_and_empty_segment(lib):
+    # zero rows, and an empty segment with NULL pointers, launch nothing
+    segs = _segs((None, 0, None, 0, 0), (1, 16, 1, 16, 16))
+    assert lib.sph_gcm_seal_segments(1, segs, 2, 0, None, None, 0, 0, None, None, 0, None) == 0
+    assert lib.sph_gcm_workspace(0, 16) == 0
+
+
 @pytest.mark.parametrize("rows,row_bytes,need", [
     (0, 100, 0), (5, 0, 0), (1, 1, 256), (5, 49152, 1024), (2048, 32768, 2048 * 8 * 16),
     (3, 16 * 256 + 1, 256),

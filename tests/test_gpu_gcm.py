@@ -1,6 +1,7 @@
 """GPU parity of the AES-GCM payload seal (eq. 19) against the CPU oracle
 (oracle/gcm.py): ciphertexts and tags bit for bit, authenticated opening,
-tamper detection per row, in-place operation, strided rows, and a payload
+tamper detection per row, in-place operation, strided rows, messages made
+of several row segments (codes and scales as one message), and a payload
 sealed between the two halves of the projection."""
 
 import sys
@@ -177,4 +178,121 @@ def test_sealed_payload_between_the_halves():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(P.host(q2), P.host(q))
     np.testing.assert_array_equal(P.host(t2), P.host(t1))
+    np.testing.assert_array_equal(P.host(f2).view(np.uint32), P.host(f1).view(np.uint32))
+
+
+SEG_CASES = [
+    # (key bytes, rows, segment lengths, aad bytes)
+    (16, 3, (40, 12), 24),             # codes + scales of a small payload row
+    (16, 5, (0, 17, 0, 33), 5),        # empty segments around ragged ones
+    (32, 4, (5, 16, 1, 33), 0),        # boundaries inside, at and across blocks
+    (16, 2, (49152, 4), 24),           # decode payload row, 8 bits: codes, then the row scale
+    (16, 5, (24576, 768), 24),         # 4 bits, block 256: codes, then 192 block scales
+    (32, 7, (1, 1, 1, 1), 16),
+    (16, 3, (16 * 300, 16 * 300 + 3), 1024),
+]
+
+
+@pytest.mark.parametrize("case", SEG_CASES, ids=[f"k{k}r{r}s{'-'.join(map(str, s))}a{a}"
+                                                 for k, r, s, a in SEG_CASES])
+def test_segments_seal_the_concatenated_rows(case):
+    # one message per row = row m of every segment in order; the segments
+    # live in separate strided buffers with bytes between their rows
+    klen, rows, lens, la = case
+    rng = np.random.default_rng(sum(lens) + 13 * rows + la + klen)
+    key = rng.bytes(klen)
+    parts = [rng.integers(0, 256, (rows, n), dtype=np.uint8) for n in lens]
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    aad = rng.integers(0, 256, (rows, la), dtype=np.uint8)
+    msg = np.concatenate(parts, axis=1)
+    ct_ref, tag_ref = ogcm.seal_rows(key, msg, iv, aad)
+    pad_in = [rng.integers(0, 256, (rows, n + 7), dtype=np.uint8) for n in lens]
+    for p, q in zip(pad_in, parts):
+        p[:, :q.shape[1]] = q
+    bufs = [_dev(p) for p in pad_in]
+    ins = [b[:, :n] for b, n in zip(bufs, lens)]
+    outs_buf = [torch.full((rows, n + 9), 0xA5, dtype=torch.uint8, device="cuda") for n in lens]
+    outs = [b[:, :n] for b, n in zip(outs_buf, lens)]
+    say(f"[gpu] gcm segments seal key={klen} rows={rows} segs={lens} aad={la}")
+    k = sph.GcmKey(key)
+    cts, tag = sph.gcm_seal_segments(k, ins, _dev(iv), _dev(aad) if la else None, out=outs)
+    torch.cuda.synchronize()
+    got = np.concatenate([P.host(c) for c in cts], axis=1) if sum(lens) else np.zeros((rows, 0), np.uint8)
+    np.testing.assert_array_equal(got, ct_ref)
+    np.testing.assert_array_equal(P.host(tag), tag_ref)
+    for b, n in zip(outs_buf, lens):
+        assert (P.host(b)[:, n:] == 0xA5).all()                      # bytes past each row untouched
+    say(f"[gpu] gcm segments open key={klen} rows={rows} segs={lens}")
+    back, ok = sph.gcm_open_segments(k, cts, _dev(iv), tag, _dev(aad) if la else None)
+    torch.cuda.synchronize()
+    assert P.host(ok).tolist() == [1] * rows
+    for b, p in zip(back, parts):
+        np.testing.assert_array_equal(P.host(b), p)
+    # the same messages sealed as one contiguous batch agree
+    ct1, tag1 = sph.gcm_seal(k, _dev(msg), _dev(iv), _dev(aad) if la else None)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(P.host(ct1), ct_ref)
+    np.testing.assert_array_equal(P.host(tag1), tag_ref)
+
+
+def test_segments_in_place_and_tamper():
+    rng = np.random.default_rng(24)
+    key = rng.bytes(16)
+    rows, lens = 5, (100, 36, 7)
+    parts = [rng.integers(0, 256, (rows, n), dtype=np.uint8) for n in lens]
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    ct_ref, tag_ref = ogcm.seal_rows(key, np.concatenate(parts, axis=1), iv,
+                                     np.zeros((rows, 0), np.uint8))
+    k = sph.GcmKey(key)
+    say("[gpu] gcm segments in place")
+    d = [_dev(p) for p in parts]
+    _, tag = sph.gcm_seal_segments(k, d, _dev(iv), None, out=d)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(np.concatenate([P.host(x) for x in d], axis=1), ct_ref)
+    np.testing.assert_array_equal(P.host(tag), tag_ref)
+    # a flipped byte in any segment fails exactly its own row
+    d[0][1, 99] ^= 1
+    d[1][3, 0] ^= 0x40
+    d[2][4, 6] ^= 0x02
+    say("[gpu] gcm segments open, tampered rows 1, 3, 4")
+    _, ok = sph.gcm_open_segments(k, d, _dev(iv), tag, None, out=d)
+    torch.cuda.synchronize()
+    assert P.host(ok).tolist() == [1, 0, 1, 0, 0]
+    for x, p in zip(d, parts):
+        np.testing.assert_array_equal(P.host(x)[[0, 2]], p[[0, 2]])
+
+
+def test_segments_seal_a_payload_as_one_message():
+    # cloud partial -> one message per row (codes, then the row's block
+    # scales) -> open -> endpoint call, identical to the unsealed payload
+    cfg = Config("gcm_segments", 96, d=1032, d_end=64, vocab=6000, n_sub=2501, subset_kind="choice",
+                 sessions=3, rows_per_session=4)
+    wl = make_workload(cfg)
+    dw = P.DeviceWorkload(wl)
+    say("[gpu] gcm payload as one message, b=4 block=256")
+    q, s, _ = dw.cloud(want_z=False, bits=4, block=256)
+    rng = np.random.default_rng(25)
+    key = rng.bytes(16)
+    k = sph.GcmKey(key)
+    M = cfg.M
+    iv = rng.integers(0, 256, (M, 12), dtype=np.uint8)
+    aad = np.tile(np.frombuffer(b"session-meta", np.uint8), (M, 1))
+    s_bytes = s.view(torch.uint8).reshape(M, -1)
+    (cq, cs), tag = sph.gcm_seal_segments(k, [q, s_bytes], _dev(iv), _dev(aad))
+    torch.cuda.synchronize()
+    msg = np.concatenate([P.host(q).view(np.uint8).reshape(M, -1), P.host(s_bytes)], axis=1)
+    ct_ref, tag_ref = ogcm.seal_rows(key, msg, iv, aad)
+    np.testing.assert_array_equal(np.concatenate([P.host(cq), P.host(cs)], axis=1), ct_ref)
+    np.testing.assert_array_equal(P.host(tag), tag_ref)
+    (q2, s2), ok = sph.gcm_open_segments(k, [cq, cs], _dev(iv), tag, _dev(aad))
+    torch.cuda.synchronize()
+    assert P.host(ok).all()
+    q2 = q2.view(q.dtype).reshape(q.shape)
+    s2 = s2.view(torch.float32).reshape(s.shape)
+    drafts = np.zeros((cfg.sessions, cfg.k), np.int32)
+    t1, a1, f1 = dw.fuse(q, s, drafts, bits=4, block=256)
+    t2, a2, f2 = dw.fuse(q2, s2, drafts, bits=4, block=256)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(P.host(t2), P.host(t1))
+    np.testing.assert_array_equal(P.host(a2), P.host(a1))
     np.testing.assert_array_equal(P.host(f2).view(np.uint32), P.host(f1).view(np.uint32))
