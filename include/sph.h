@@ -267,13 +267,15 @@ int sph_fuse_verify_hq(const void* q, const float* scale, int bits, int64_t bloc
 typedef struct sph_gcm_key_s* sph_gcm_key;
 
 /* Expand a 16- or 32-byte AES key (host memory) into a device key object
- * (round keys, tables and the powers of the GHASH key, ~264 KB); blocks
+ * (round keys, tables, the powers of the GHASH key and the product tables
+ * of H^256, ~272 KB); blocks
  * until the upload on `stream` has finished.  Destroy with
  * sph_gcm_key_destroy. */
 int sph_gcm_key_create(const uint8_t* key, int key_bytes, void* stream, sph_gcm_key* out);
 void sph_gcm_key_destroy(sph_gcm_key key);
 
-/* Device workspace bytes of a seal or open of rows x row_bytes. */
+/* Device workspace bytes of a seal or open of rows x row_bytes (for any
+ * aad_bytes <= 1024; nonzero for rows > 0, also for empty messages). */
 size_t sph_gcm_workspace(int64_t rows, int64_t row_bytes);
 
 /* ct[m] = plaintext row m xor its keystream; tag[m] its authentication tag. */

@@ -149,7 +149,7 @@ bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_
     w[i] = w[i - nk] ^ t;
   }
   // device image: te | sbox | round keys | powers of H
-  dev_image.assign(kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16, 0);
+  dev_image.assign(kGcmImageBytes, 0);
   std::memcpy(dev_image.data(), te, sizeof(te));
   std::memcpy(dev_image.data() + 1024, sbox, 256);
   std::memcpy(dev_image.data() + kGcmRkOffset, w, sizeof(uint32_t) * 4 * (nr + 1));
@@ -159,6 +159,15 @@ bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_
   uint32_t* pw = reinterpret_cast<uint32_t*>(dev_image.data() + kGcmPowOffset);  // pw[4e .. 4e+3] = H^e
   std::memcpy(pw + 4, h, 16);
   for (int e = 2; e <= kGcmMaxPow; ++e) gf128_mul(pw + 4 * (e - 1), h, pw + 4 * e);
+  // nibble tables of the product by G = H^kGcmStride (the product is linear
+  // in its first factor, so Y.G is the xor of the entries of Y's nibbles)
+  uint32_t* tab = reinterpret_cast<uint32_t*>(dev_image.data() + kGcmTabOffset);
+  for (int p = 0; p < 32; ++p)
+    for (int v = 0; v < 16; ++v) {
+      uint32_t x[4] = {0u, 0u, 0u, 0u};
+      x[p >> 3] = (uint32_t)v << (28 - 4 * (p & 7));
+      gf128_mul(x, pw + 4 * kGcmStride, tab + 4 * (16 * p + v));
+    }
   return true;
 }
 
@@ -224,81 +233,169 @@ __device__ __forceinline__ void stage_key(GcmShared& sh, const uint8_t* key_dev,
   __syncthreads();
 }
 
-// One thread per 16-byte block of a row (grid: blocks / 256 x rows).
+// Y . G from the nibble tables in LDS: 32 independent lookups, no shifts.
+__device__ __forceinline__ void mul_by_g(uint32_t y[4], const uint4* __restrict__ tab) {
+  uint32_t r0 = 0u, r1 = 0u, r2 = 0u, r3 = 0u;
+#pragma unroll
+  for (int p = 0; p < 32; ++p) {
+    const uint32_t v = (y[p >> 3] >> (28 - 4 * (p & 7))) & 15u;
+    const uint4 e = tab[16 * p + v];
+    r0 ^= e.x;
+    r1 ^= e.y;
+    r2 ^= e.z;
+    r3 ^= e.w;
+  }
+  y[0] = r0;
+  y[1] = r1;
+  y[2] = r2;
+  y[3] = r3;
+}
+
+// Counter-mode output of data block j of a row and its GHASH input (the
+// ciphertext, zero past the message).
+template <bool OPEN>
+__device__ __forceinline__ void gcm_data_block(const GcmShared& sh, int nr, const GcmSegs& segs,
+                                               int64_t L, const uint32_t ivw[3], int64_t row, int j,
+                                               uint32_t c[4]) {
+  uint32_t ctr[4] = {ivw[0], ivw[1], ivw[2], (uint32_t)(2 + j)};  // inc32 from J0 + 1
+  uint32_t ks[4];
+  aes_block(sh.te, sh.sb, sh.rk, nr, ctr, ks);
+  const int64_t p0 = (int64_t)j * 16;
+  const int valid = (int)min<int64_t>(16, L - p0);
+  int64_t st;
+  const int s0 = seg_of(segs, p0, st);
+  int64_t e0 = segs.end[0];
+#pragma unroll
+  for (int k = 1; k < kGcmMaxSegs; ++k)
+    if (s0 == k) e0 = segs.end[k];
+  // a block inside one segment takes the plain path; one that straddles a
+  // segment boundary maps every byte on its own
+  const bool whole = p0 + valid <= e0;
+  uint32_t x[4], y[4];
+  if (whole) {
+    load_be_words(seg_ptr(segs.in, segs.ld_in, s0, row, p0 - st), valid, x);
+  } else {
+    uint8_t b[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      b[i] = 0;
+      if (i < valid) {
+        int64_t sti;
+        const int si = seg_of(segs, p0 + i, sti);
+        b[i] = *seg_ptr(segs.in, segs.ld_in, si, row, p0 + i - sti);
+      }
+    }
+    pack_be_words(b, x);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) y[k] = x[k] ^ ks[k];
+  if (whole) {
+    uint8_t* dst = seg_ptr(segs.out, segs.ld_out, s0, row, p0 - st);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i < valid) {
+        int64_t sti;
+        const int si = seg_of(segs, p0 + i, sti);
+        *seg_ptr(segs.out, segs.ld_out, si, row, p0 + i - sti) = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+      }
+  }
+  // the GHASH input is the ciphertext: the output when sealing, the input
+  // when opening
+#pragma unroll
+  for (int k = 0; k < 4; ++k) c[k] = OPEN ? x[k] : y[k];
+  if (!OPEN && valid < 16) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (i >= valid) c[i >> 2] &= ~(0xFFu << (24 - 8 * (i & 3)));
+  }
+}
+
+// GHASH of a message of na AAD blocks and n data blocks is the sum of the
+// m = na + n + 1 terms X_k . H^(m+1-k) (k = 1..m, X_m the length block), and
+// the tag is that sum xor E_K(J0).  Every term is independent given the
+// powers of H.  Workgroup q of a row (grid: parts x rows) covers data blocks
+// [q*S*chain, (q+1)*S*chain) with S = kGcmStride threads; thread t takes the
+// blocks j_i = q*S*chain + t + S*i (i < chain, j_i < n), produces their
+// output, and folds their terms by Horner's rule in G = H^S:
+//   sum_i C_{j_i} . H^(n+1-j_i) = H^(n+1-j_last) . (...(C_{j_0} . G + C_{j_1}) . G ...)
+// so each block costs one table product and each thread one bit-serial
+// product by a power of H.  The last na + 2 threads of workgroup xpart
+// (threads without a data block where threads take one block each) add the
+// remaining terms: AAD block i (A_i . H^(m-i)), the length block times H,
+// and E_K(J0).  Each workgroup xor-reduces its terms into one 16-byte
+// partial of the row.
 template <bool OPEN>
 __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ key_dev, int nr,
-                                                    const GcmSegs segs, int64_t L, int n,
-                                                    const uint8_t* __restrict__ iv,
-                                                    uint32_t* __restrict__ partial, int nparts) {
+                                                    const GcmSegs segs, int64_t L, int n, int chain,
+                                                    int xpart, const uint8_t* __restrict__ iv,
+                                                    const uint8_t* __restrict__ aad, int64_t ld_aad,
+                                                    int la, uint32_t* __restrict__ partial, int nparts) {
   __shared__ GcmShared sh;
-  stage_key(sh, key_dev, nr);
+  __shared__ uint4 tab[32 * 16];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (chain > 1) {
+    const uint4* src = reinterpret_cast<const uint4*>(key_dev + kGcmTabOffset);
+    tab[tid] = src[tid];
+    tab[tid + 256] = src[tid + 256];
+  }
+  stage_key(sh, key_dev, nr);  // ends with a barrier
   const int64_t row = blockIdx.y;
-  const int j = blockIdx.x * 256 + tid;
+  const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset);
+  uint32_t ivw[4];
+  load_be_words(iv + row * 12, 12, ivw);
   uint32_t t[4] = {0u, 0u, 0u, 0u};
-  if (j < n) {
-    const uint8_t* ivr = iv + row * 12;
-    uint32_t ctr[4];
-    load_be_words(ivr, 12, ctr);
-    ctr[3] = (uint32_t)(2 + j);  // inc32 from J0 + 1
-    uint32_t ks[4];
-    aes_block(sh.te, sh.sb, sh.rk, nr, ctr, ks);
-    const int64_t p0 = (int64_t)j * 16;
-    const int valid = (int)min<int64_t>(16, L - p0);
-    int64_t st;
-    const int s0 = seg_of(segs, p0, st);
-    int64_t e0 = segs.end[0];
+  // data blocks
+  {
+    const int j0 = blockIdx.x * kGcmStride * chain + tid;
+    uint32_t y[4] = {0u, 0u, 0u, 0u};
+    int jl = -1;
+    for (int i = 0; i < chain; ++i) {
+      const int j = j0 + kGcmStride * i;
+      if (j >= n) break;
+      uint32_t c[4];
+      gcm_data_block<OPEN>(sh, nr, segs, L, ivw, row, j, c);
+      if (i > 0) mul_by_g(y, tab);
 #pragma unroll
-    for (int k = 1; k < kGcmMaxSegs; ++k)
-      if (s0 == k) e0 = segs.end[k];
-    // a block inside one segment takes the plain path; one that straddles
-    // a segment boundary maps every byte on its own
-    const bool whole = p0 + valid <= e0;
-    uint32_t x[4], y[4];
-    if (whole) {
-      load_be_words(seg_ptr(segs.in, segs.ld_in, s0, row, p0 - st), valid, x);
+      for (int k = 0; k < 4; ++k) y[k] ^= c[k];
+      jl = j;
+    }
+    if (jl >= 0) {
+      const uint32_t* hp = pw + 4 * (n + 1 - jl);
+      const uint32_t h4[4] = {hp[0], hp[1], hp[2], hp[3]};
+      gf128_mul(y, h4, t);
+    }
+  }
+  // AAD, length and E_K(J0) terms
+  const int na = (la + 15) / 16;
+  const int u = tid - (kGcmStride - (na + 2));
+  if ((int)blockIdx.x == xpart && u >= 0) {
+    const int m = na + n + 1;
+    uint32_t c[4], r[4];
+    if (u == na + 1) {
+      const uint32_t j0b[4] = {ivw[0], ivw[1], ivw[2], 1u};
+      aes_block(sh.te, sh.sb, sh.rk, nr, j0b, r);
     } else {
-      uint8_t b[16];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        b[i] = 0;
-        if (i < valid) {
-          int64_t sti;
-          const int si = seg_of(segs, p0 + i, sti);
-          b[i] = *seg_ptr(segs.in, segs.ld_in, si, row, p0 + i - sti);
-        }
+      int e;
+      if (u < na) {
+        load_be_words(aad + row * ld_aad + (int64_t)u * 16, min(16, la - 16 * u), c);
+        e = m - u;
+      } else {
+        const uint64_t abits = (uint64_t)la * 8, cbits = (uint64_t)L * 8;
+        c[0] = (uint32_t)(abits >> 32);
+        c[1] = (uint32_t)abits;
+        c[2] = (uint32_t)(cbits >> 32);
+        c[3] = (uint32_t)cbits;
+        e = 1;
       }
-      pack_be_words(b, x);
+      const uint32_t h4[4] = {pw[4 * e], pw[4 * e + 1], pw[4 * e + 2], pw[4 * e + 3]};
+      gf128_mul(c, h4, r);
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) y[k] = x[k] ^ ks[k];
-    if (whole) {
-      uint8_t* dst = seg_ptr(segs.out, segs.ld_out, s0, row, p0 - st);
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i < valid) {
-          int64_t sti;
-          const int si = seg_of(segs, p0 + i, sti);
-          *seg_ptr(segs.out, segs.ld_out, si, row, p0 + i - sti) = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
-        }
-    }
-    // the GHASH input is the ciphertext: the output when sealing, the input
-    // when opening; bytes past the message are zero
-    uint32_t c[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) c[k] = OPEN ? x[k] : y[k];
-    if (!OPEN && valid < 16) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i)
-        if (i >= valid) c[i >> 2] &= ~(0xFFu << (24 - 8 * (i & 3)));
-    }
-    const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset) + 4 * (n + 1 - j);
-    const uint32_t hp[4] = {pw[0], pw[1], pw[2], pw[3]};
-    gf128_mul(c, hp, t);
+    for (int k = 0; k < 4; ++k) t[k] ^= r[k];
   }
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -311,58 +408,27 @@ __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ 
     partial[(row * nparts + blockIdx.x) * 4 + tid] = sh.red[0][tid] ^ sh.red[1][tid] ^ sh.red[2][tid] ^ sh.red[3][tid];
 }
 
-// One thread per row: partial sums + AAD terms + length term, then the tag.
+// One thread per row: the xor of the row's partials is its tag; write it
+// (seal) or compare it with the given one in constant time (open).
 template <bool OPEN>
-__global__ __launch_bounds__(256) void k_gcm_finish(const uint8_t* __restrict__ key_dev, int nr, int rows,
-                                                    int64_t L, int n, const uint8_t* __restrict__ iv,
-                                                    const uint8_t* __restrict__ aad, int64_t ld_aad,
-                                                    int la, const uint32_t* __restrict__ partial,
+__global__ __launch_bounds__(256) void k_gcm_finish(int rows, const uint32_t* __restrict__ partial,
                                                     int nparts, uint8_t* __restrict__ tag,
                                                     int32_t* __restrict__ ok) {
-  __shared__ GcmShared sh;
-  stage_key(sh, key_dev, nr);
   const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (row >= rows) return;
-  const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset);
-  const int na = (la + 15) / 16;
-  const int m = na + n + 1;
   uint32_t s[4] = {0u, 0u, 0u, 0u};
   for (int p = 0; p < nparts; ++p)
 #pragma unroll
     for (int k = 0; k < 4; ++k) s[k] ^= partial[(row * nparts + p) * 4 + k];
-  for (int i = 0; i < na; ++i) {
-    uint32_t a[4], t[4];
-    load_be_words(aad + row * ld_aad + (int64_t)i * 16, min(16, la - 16 * i), a);
-    const uint32_t hp[4] = {pw[4 * (m - i)], pw[4 * (m - i) + 1], pw[4 * (m - i) + 2], pw[4 * (m - i) + 3]};
-    gf128_mul(a, hp, t);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] ^= t[k];
-  }
-  {
-    const uint64_t abits = (uint64_t)la * 8, cbits = (uint64_t)L * 8;
-    const uint32_t lb[4] = {(uint32_t)(abits >> 32), (uint32_t)abits, (uint32_t)(cbits >> 32), (uint32_t)cbits};
-    const uint32_t h1[4] = {pw[4], pw[5], pw[6], pw[7]};
-    uint32_t t[4];
-    gf128_mul(lb, h1, t);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) s[k] ^= t[k];
-  }
-  uint32_t j0[4], e0[4];
-  load_be_words(iv + row * 12, 12, j0);
-  j0[3] = 1u;
-  aes_block(sh.te, sh.sb, sh.rk, nr, j0, e0);
   uint8_t* tg = tag + row * 16;
   if (OPEN) {
     uint32_t diff = 0;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const uint8_t b = (uint8_t)((e0[i >> 2] ^ s[i >> 2]) >> (24 - 8 * (i & 3)));
-      diff |= (uint32_t)(b ^ tg[i]);
-    }
+    for (int i = 0; i < 16; ++i) diff |= (uint32_t)((uint8_t)(s[i >> 2] >> (24 - 8 * (i & 3))) ^ tg[i]);
     ok[row] = diff == 0 ? 1 : 0;
   } else {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) tg[i] = (uint8_t)((e0[i >> 2] ^ s[i >> 2]) >> (24 - 8 * (i & 3)));
+    for (int i = 0; i < 16; ++i) tg[i] = (uint8_t)(s[i >> 2] >> (24 - 8 * (i & 3)));
   }
 }
 
@@ -370,28 +436,26 @@ hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const GcmSegs& 
                       const uint8_t* iv, const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag,
                       int32_t* ok, uint32_t* partial, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (segs.nseg < 1 || segs.nseg > kGcmMaxSegs) return hipErrorInvalidValue;
+  if (segs.nseg < 1 || segs.nseg > kGcmMaxSegs || rows > 65535 || la < 0 || la > kGcmMaxAad)
+    return hipErrorInvalidValue;
   const int64_t L = segs.end[segs.nseg - 1];
   const int n = (int)((L + 15) / 16);
-  const int nparts = (n + 255) / 256;
-  if (rows > 65535 && nparts > 0) return hipErrorInvalidValue;
-  if (nparts > 0) {
-    if (open)
-      launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, segs, L, n,
-                    iv, partial, nparts);
-    else
-      launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(256), 0, s, key_dev, nr, segs, L, n,
-                    iv, partial, nparts);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
+  const int chain = gcm_chain(rows, n);
+  int xpart = 0;
+  const int nparts = gcm_parts(n, (la + 15) / 16, chain, &xpart);
+  if (open)
+    launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(kGcmStride), 0, s, key_dev, nr, segs, L, n,
+                  chain, xpart, iv, aad, ld_aad, la, partial, nparts);
+  else
+    launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(kGcmStride), 0, s, key_dev, nr, segs, L, n,
+                  chain, xpart, iv, aad, ld_aad, la, partial, nparts);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int fb = (rows + 255) / 256;
   if (open)
-    launch_kernel(k_gcm_finish<true>, dim3(fb), dim3(256), 0, s, key_dev, nr, rows, L, n, iv, aad,
-                  ld_aad, la, partial, nparts, tag, ok);
+    launch_kernel(k_gcm_finish<true>, dim3(fb), dim3(256), 0, s, rows, partial, nparts, tag, ok);
   else
-    launch_kernel(k_gcm_finish<false>, dim3(fb), dim3(256), 0, s, key_dev, nr, rows, L, n, iv, aad,
-                  ld_aad, la, partial, nparts, tag, ok);
+    launch_kernel(k_gcm_finish<false>, dim3(fb), dim3(256), 0, s, rows, partial, nparts, tag, ok);
   return hipGetLastError();
 }
 

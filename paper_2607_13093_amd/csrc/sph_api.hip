@@ -644,7 +644,9 @@ void sph_gcm_key_destroy(sph_gcm_key key) {
 size_t sph_gcm_workspace(int64_t rows, int64_t row_bytes) {
   if (rows <= 0 || row_bytes < 0) return 0;
   const int64_t n = (row_bytes + 15) / 16;
-  return align256((size_t)rows * (size_t)((n + 255) / 256) * 16);
+  // sized for the largest AAD, so that one workspace serves every call
+  return align256((size_t)rows * (size_t)sph::gcm_parts(n, sph::kGcmMaxAad / 16, sph::gcm_chain(rows, n)) *
+                  16);
 }
 
 namespace {
@@ -675,8 +677,9 @@ int gcm_call(const char* fn, bool open, sph_gcm_key key, const sph_gcm_segment* 
     g.ld_out[k] = sg.ld_out;
     g.end[k] = row_bytes;
   }
-  if (aad_bytes < 0 || aad_bytes > 1024)
-    return fail(SPH_E_INVALID_ARG, "%s: aad_bytes=%lld not in [0, 1024]", fn, (long long)aad_bytes);
+  if (aad_bytes < 0 || aad_bytes > sph::kGcmMaxAad)
+    return fail(SPH_E_INVALID_ARG, "%s: aad_bytes=%lld not in [0, %d]", fn, (long long)aad_bytes,
+                sph::kGcmMaxAad);
   const int64_t m = (aad_bytes + 15) / 16 + (row_bytes + 15) / 16 + 1;
   if (m > sph::kGcmMaxPow)
     return fail(SPH_E_UNSUPPORTED, "%s: message of %lld bytes (+%lld AAD) exceeds %d blocks", fn,

@@ -155,12 +155,18 @@ hipError_t launch_widen_codes(const int8_t* hq, int64_t ldhq, int M, int K, int 
                               uint16_t* out, hipStream_t s);
 
 // AES-GCM of payload rows (gcm.hip).  A key's device image holds the T0
-// table (1 KB), the S-box (256 B), the round keys (at kGcmRkOffset) and the
-// powers H^0 .. H^kGcmMaxPow of the hash key (16 B each, at kGcmPowOffset).
+// table (1 KB), the S-box (256 B), the round keys (at kGcmRkOffset), the
+// powers H^0 .. H^kGcmMaxPow of the hash key (16 B each, at kGcmPowOffset)
+// and, at kGcmTabOffset, the product by G = H^kGcmStride as 32 nibble
+// tables: entry [p][v] (16 B) is G times the block whose nibble p (from the
+// most significant end) is v and whose other bits are zero.
 constexpr int kGcmMaxPow = 16384;  // AAD + ciphertext + length blocks of one message
 constexpr int kGcmRkOffset = 1280;
 constexpr int kGcmPowOffset = 1536;
-constexpr size_t kGcmImageBytes = (size_t)kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16;
+constexpr int kGcmStride = 256;    // blocks between the terms one thread chains
+constexpr int kGcmMaxChain = 16;   // blocks one thread chains at most
+constexpr size_t kGcmTabOffset = (size_t)kGcmPowOffset + (size_t)(kGcmMaxPow + 1) * 16;
+constexpr size_t kGcmImageBytes = kGcmTabOffset + 32 * 16 * 16;
 bool gcm_key_setup(const uint8_t* key, int key_bytes, std::vector<uint8_t>& dev_image, int& nr);
 // A message row is the concatenation of up to kGcmMaxSegs segments: bytes
 // [end[k-1], end[k]) of row r come from in[k] + r * ld_in[k] and go to
@@ -175,8 +181,32 @@ struct GcmSegs {
   int64_t end[kGcmMaxSegs];
   int nseg;
 };
-// rows <= 65535 messages of L = segs.end[nseg-1] bytes; partial:
-// rows * ceil(ceil(L/16)/256) * 16 bytes
+constexpr int kGcmMaxAad = 1024;  // bytes of associated data per message
+// Blocks each thread chains for a batch of rows messages of n data blocks:
+// 1 while the batch has few blocks (parallelism first), up to kGcmMaxChain
+// for large batches.
+inline int gcm_chain(int64_t rows, int64_t n) {
+  const int64_t k = (rows * n + 32767) / 32768;
+  return (int)(k < 1 ? 1 : (k > kGcmMaxChain ? kGcmMaxChain : k));
+}
+// Workgroups (of kGcmStride threads) per message of n data blocks and na
+// AAD blocks.  The last na + 2 threads of workgroup *extra_part take the
+// AAD blocks, the length block and E_K(J0): the last data workgroup, unless
+// threads chain single blocks (a latency-bound batch) and it has fewer than
+// na + 2 threads without a block; then one more workgroup.  (Adding a
+// workgroup per row to a large batch would double its grid.)
+inline int gcm_parts(int64_t n, int64_t na, int chain, int* extra_part = nullptr) {
+  const int64_t per = (int64_t)kGcmStride * chain;
+  const int64_t nd = (n + per - 1) / per;
+  const int64_t in_last = nd > 0 ? n - (nd - 1) * per : kGcmStride;
+  const int64_t idle = in_last < kGcmStride ? kGcmStride - in_last : 0;
+  const int64_t xp = nd > 0 && (chain > 1 || idle >= na + 2) ? nd - 1 : nd;
+  if (extra_part) *extra_part = (int)xp;
+  return (int)(xp + 1);
+}
+// rows <= 65535 messages of L = segs.end[nseg-1] bytes with la <= kGcmMaxAad
+// bytes of AAD; partial: rows * gcm_parts(n, ceil(la/16), gcm_chain(rows, n))
+// * 16 bytes with n = ceil(L/16)
 hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const GcmSegs& segs, int rows,
                       const uint8_t* iv, const uint8_t* aad, int64_t ld_aad, int la, uint8_t* tag,
                       int32_t* ok, uint32_t* partial, hipStream_t s);

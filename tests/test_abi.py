@@ -256,11 +256,15 @@ def test_gcm_segments_empty_batch_and_empty_segment(lib):
 
 
 @pytest.mark.parametrize("rows,row_bytes,need", [
-    (0, 100, 0), (5, 0, 0), (1, 1, 256), (5, 49152, 1024), (2048, 32768, 2048 * 8 * 16),
-    (3, 16 * 256 + 1, 256),
+    (0, 100, 0), (5, 0, 256), (1, 1, 256), (5, 49152, 1280), (2048, 32768, 2048 * 16),
+    (3, 16 * 256 + 1, 256), (16, 16 * 256, 512), (16, 16 * 257, 512), (40, 52429, 2048),
+    (64, 123457, 64 * 2 * 16),
 ])
 def test_gcm_workspace_sizes(lib, rows, row_bytes, need):
-    # one 16-byte partial GHASH sum per row and 256 blocks, rounded up to 256 bytes
+    # one 16-byte partial sum per row and workgroup of 256 threads, each
+    # thread chaining k = clamp(ceil(rows * blocks / 32768), 1, 16) blocks;
+    # for k = 1 one more workgroup when the last has fewer than 66 threads
+    # without a block (room for the largest AAD); rounded up to 256 bytes
     assert lib.sph_gcm_workspace(rows, row_bytes) == need
 
 

@@ -92,6 +92,33 @@ def test_large_batch():
     np.testing.assert_array_equal(np.delete(P.host(back), 5, axis=0), np.delete(pt, 5, axis=0))
 
 
+def test_longest_chains_with_a_ragged_part():
+    # 64 rows x 7717 blocks: every thread chains 16 blocks (two workgroups
+    # per row, the second ragged); two rows checked against the oracle, all
+    # rows opened, one tampered row rejected
+    rng = np.random.default_rng(33)
+    key = rng.bytes(16)
+    rows, L, la = 64, 123457, 13
+    pt = rng.integers(0, 256, (rows, L), dtype=np.uint8)
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    aad = rng.integers(0, 256, (rows, la), dtype=np.uint8)
+    say(f"[gpu] gcm chained rows={rows} L={L}")
+    k = sph.GcmKey(key)
+    ct, tag = sph.gcm_seal(k, _dev(pt), _dev(iv), _dev(aad))
+    torch.cuda.synchronize()
+    ct_h, tag_h = P.host(ct), P.host(tag)
+    for m in (0, rows - 1):
+        c, t = ogcm.gcm_encrypt(key, iv[m].tobytes(), pt[m].tobytes(), aad[m].tobytes())
+        assert ct_h[m].tobytes() == c and tag_h[m].tobytes() == t
+    ct_h = ct_h.copy()
+    ct_h[17, L - 1] ^= 4
+    back, ok = sph.gcm_open(k, _dev(ct_h), _dev(iv), tag, _dev(aad))
+    torch.cuda.synchronize()
+    okh = P.host(ok)
+    assert okh[17] == 0 and okh.sum() == rows - 1
+    np.testing.assert_array_equal(np.delete(P.host(back), 17, axis=0), np.delete(pt, 17, axis=0))
+
+
 def test_open_flags_exactly_the_tampered_rows():
     rng = np.random.default_rng(21)
     key = rng.bytes(16)
