@@ -1,4 +1,5 @@
-"""The two calls captured in a HIP graph (torch.cuda.graph) and replayed.
+"""The two calls captured in a HIP graph (torch.cuda.graph) and replayed,
+also with the payload sealed and opened between them.
 
 Every call only enqueues kernels on the caller's stream (no allocation,
 memset or synchronisation inside), so the whole step can be captured.  Each
@@ -38,9 +39,10 @@ def _step_buffers(dw, cfg, sub, M, n, bits, block):
     return q, s, tok, acc, f, ws_c, ws_f
 
 
-@pytest.mark.parametrize("name,bits,block", [("decode", 8, 0), ("batched_small", 4, 256)])
-def test_step_in_a_graph_replays_exactly(name, bits, block):
-    if name == "decode":
+@pytest.mark.parametrize("name,bits,block,sealed", [("decode", 8, 0, False), ("batched_small", 4, 256, False),
+                                                     ("decode_sealed", 8, 0, True)])
+def test_step_in_a_graph_replays_exactly(name, bits, block, sealed):
+    if name.startswith("decode"):
         cfg = CONFIGS["decode"]
     else:   # 40 rows: the MFMA path in both calls
         cfg = Config("graph", 97, d=1032, d_end=64, vocab=6000, n_sub=2560, subset_kind="choice",
@@ -50,17 +52,42 @@ def test_step_in_a_graph_replays_exactly(name, bits, block):
     M, n, de = cfg.M, len(wl.subset), cfg.d_end
     drafts = P.to_dev(make_drafts(cfg, np.zeros(M, np.int32), wl.subset))
     q, s, tok, acc, f, ws_c, ws_f = _step_buffers(dw, cfg, dw.subset, M, n, bits, block)
+    outs = [q, s, tok, acc, f]
+    if sealed:
+        # the payload crosses as one AES-GCM message per row (codes, then
+        # scales) and the endpoint works on the opened copy
+        key = sph.GcmKey(bytes(range(32)))
+        s_b = s.view(torch.uint8).reshape(M, -1)
+        cq, cs = torch.empty_like(q), torch.empty_like(s_b)
+        q2, s2 = torch.empty_like(q), torch.empty_like(s)
+        s2_b = s2.view(torch.uint8).reshape(M, -1)
+        tag = torch.empty((M, 16), dtype=torch.uint8, device="cuda")
+        ok = torch.empty((M,), dtype=torch.int32, device="cuda")
+        iv = P.to_dev(np.arange(M * 12, dtype=np.uint32).astype(np.uint8).reshape(M, 12))
+        aad = P.to_dev(np.full((M, 20), 7, np.uint8))
+        ws_g = torch.empty(max(1, sph.gcm_workspace(M, q.shape[1] + s_b.shape[1])), dtype=torch.uint8,
+                           device="cuda")
+        outs += [cq, cs, tag, ok, q2, s2]
 
     def step():
         sph.cloud_partial(dw.h[:, de:], dw.w_cloud, dw.subset, cfg.clip_c, workspace=ws_c,
                           out=(q, s, None), bits=bits, block=block)
-        sph.fuse_verify(q, s, dw.h[:, :de], dw.w_end, dw.subset, cfg.sessions, cfg.rows_per_session,
+        qe, se = q, s
+        if sealed:
+            sph.gcm_seal_segments(key, (q, s_b), iv, aad, out=(cq, cs), tag=tag, workspace=ws_g)
+            sph.gcm_open_segments(key, (cq, cs), iv, tag, aad, out=(q2, s2_b), ok=ok, workspace=ws_g)
+            qe, se = q2, s2
+        sph.fuse_verify(qe, se, dw.h[:, :de], dw.w_end, dw.subset, cfg.sessions, cfg.rows_per_session,
                         drafts, workspace=ws_f, out=(tok, acc, f), want_fused=True, bits=bits, block=block)
 
     say(f"[gpu] graph {name}: eager")
     step()
     torch.cuda.synchronize()
-    ref = [P.host(t).copy() for t in (q, s, tok, acc, f)]
+    ref = [P.host(t).copy() for t in outs]
+    if sealed:                                  # outs: q s tok acc f cq cs tag ok q2 s2
+        assert ref[8].tolist() == [1] * M
+        np.testing.assert_array_equal(ref[9], ref[0])
+        np.testing.assert_array_equal(ref[10].view(np.uint8), ref[1].view(np.uint8))
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -73,12 +100,12 @@ def test_step_in_a_graph_replays_exactly(name, bits, block):
         step()
     torch.cuda.synchronize()
     for rep in range(3):
-        for t in (q, s, tok, acc, f):            # program work between replays
+        for t in outs:                           # program work between replays
             t.zero_()
         torch.cuda.synchronize()
         say(f"[gpu] graph {name}: replay {rep}")
         g.replay()
         torch.cuda.synchronize()
-        for r, t in zip(ref, (q, s, tok, acc, f)):
+        for r, t in zip(ref, outs):
             np.testing.assert_array_equal(P.host(t).view(np.uint8), r.view(np.uint8))
     g.reset()
