@@ -323,3 +323,37 @@ def test_segments_seal_a_payload_as_one_message():
     np.testing.assert_array_equal(P.host(t2), P.host(t1))
     np.testing.assert_array_equal(P.host(a2), P.host(a1))
     np.testing.assert_array_equal(P.host(f2).view(np.uint32), P.host(f1).view(np.uint32))
+
+
+def test_limits_most_rows_and_longest_message():
+    # 65535 one-byte messages (the largest grid), six checked against the
+    # oracle and all opened; then one message of the largest length (16383
+    # data blocks + the length block, no AAD) and one byte more, refused
+    rng = np.random.default_rng(41)
+    key = rng.bytes(16)
+    rows = 65535
+    pt = rng.integers(0, 256, (rows, 1), dtype=np.uint8)
+    iv = rng.integers(0, 256, (rows, 12), dtype=np.uint8)
+    say(f"[gpu] gcm rows={rows} L=1")
+    k = sph.GcmKey(key)
+    ct, tag = sph.gcm_seal(k, _dev(pt), _dev(iv))
+    torch.cuda.synchronize()
+    ct_h, tag_h = P.host(ct), P.host(tag)
+    for m in (0, 1, 255, 256, 40000, rows - 1):
+        c, t = ogcm.gcm_encrypt(key, iv[m].tobytes(), pt[m].tobytes())
+        assert ct_h[m].tobytes() == c and tag_h[m].tobytes() == t
+    back, ok = sph.gcm_open(k, ct, _dev(iv), tag)
+    torch.cuda.synchronize()
+    assert int(P.host(ok).sum()) == rows
+    np.testing.assert_array_equal(P.host(back), pt)
+
+    L = 16 * 16383
+    pt1 = rng.integers(0, 256, (1, L), dtype=np.uint8)
+    iv1 = rng.integers(0, 256, (1, 12), dtype=np.uint8)
+    say(f"[gpu] gcm rows=1 L={L}")
+    ct1, tag1 = sph.gcm_seal(k, _dev(pt1), _dev(iv1))
+    torch.cuda.synchronize()
+    c, t = ogcm.gcm_encrypt(key, iv1[0].tobytes(), pt1[0].tobytes())
+    assert P.host(ct1)[0].tobytes() == c and P.host(tag1)[0].tobytes() == t
+    with pytest.raises(sph.SphError, match="exceeds 16384 blocks"):
+        sph.gcm_seal(k, _dev(np.zeros((1, L + 1), np.uint8)), _dev(iv1))
