@@ -46,7 +46,7 @@ extern "C" {
 #define SPH_OK             0
 #define SPH_E_INVALID_ARG (-1) /* bad pointer, size, stride, enum or scalar */
 #define SPH_E_SUBSET      (-2) /* subset ids not strictly ascending / out of range / empty */
-#define SPH_E_UNSUPPORTED (-3) /* valid request this build cannot run */
+#define SPH_E_UNSUPPORTED (-3) /* valid request the library has no kernel for */
 #define SPH_E_DEVICE      (-4) /* a HIP runtime call failed; message has the HIP error */
 #define SPH_E_WORKSPACE   (-5) /* workspace missing or smaller than required */
 
