@@ -39,6 +39,23 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ z,
   const int j1 = min(n, j0 + kQuantChunk);
   const bool per_row = qshift < 0;
 
+  // the chunk's z values of this thread (4 consecutive columns per 1024), all
+  // loaded before any is used, and before the row's partial maxima, so the
+  // two loads' latencies overlap
+  constexpr int VT = kQuantChunk / 1024;
+  float4 v[VT];
+#pragma unroll
+  for (int t = 0; t < VT; ++t) {
+    const int j = j0 + tid * 4 + 1024 * t;
+    if (vec) {
+      v[t] = j < j1 ? *reinterpret_cast<const float4*>(z + zrow + j) : make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {
+      v[t].x = j < j1 ? z[zrow + j] : 0.f;
+      v[t].y = j + 1 < j1 ? z[zrow + j + 1] : 0.f;
+      v[t].z = j + 2 < j1 ? z[zrow + j + 2] : 0.f;
+      v[t].w = j + 3 < j1 ? z[zrow + j + 3] : 0.f;
+    }
+  }
   float srow = 0.0f;
   if (per_row) {
     // all of a thread's partial maxima are loaded at once (no load waits on
@@ -64,22 +81,6 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ z,
     s_bmax[tid] = 0u;
   }
 
-  // the chunk's z values of this thread (4 consecutive columns per 1024), all
-  // loaded before any is used
-  constexpr int VT = kQuantChunk / 1024;
-  float4 v[VT];
-#pragma unroll
-  for (int t = 0; t < VT; ++t) {
-    const int j = j0 + tid * 4 + 1024 * t;
-    if (vec) {
-      v[t] = j < j1 ? *reinterpret_cast<const float4*>(z + zrow + j) : make_float4(0.f, 0.f, 0.f, 0.f);
-    } else {
-      v[t].x = j < j1 ? z[zrow + j] : 0.f;
-      v[t].y = j + 1 < j1 ? z[zrow + j + 1] : 0.f;
-      v[t].z = j + 2 < j1 ? z[zrow + j + 2] : 0.f;
-      v[t].w = j + 3 < j1 ? z[zrow + j + 3] : 0.f;
-    }
-  }
   auto absclip = [&](float x) { return fabsf(fminf(fmaxf(x, -clip), clip)); };
   if (!per_row) {
     // a wave's 256 columns of one iteration lie in one block
