@@ -228,6 +228,10 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
       const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       const int row = m0 + lrow;
       V best = V(0);
+      // fuse: the lane's largest fused value of the row and its column (the
+      // first, so the lowest, of equal values); one key per row afterwards
+      float bv = 0.0f;
+      int bc = -1;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int lcol = wn * TN + j * 32 + (lane & 31);
@@ -249,11 +253,14 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
             }
             const float f = __builtin_fmaf((float)code, s_qs[lrow], dot * s_qs[BM + lrow]);
             if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
-            const unsigned long long key = argmax_key_m(f, col);
-            best = key > best ? key : best;
+            if (bc < 0 || f > bv) {
+              bv = f;
+              bc = col;
+            }
           }
         }
       }
+      if constexpr (!kCloud) best = bc >= 0 ? argmax_key_m(bv, bc) : 0ull;
       red[i * 16 + r] = best;
     }
   }
