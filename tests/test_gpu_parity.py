@@ -164,6 +164,42 @@ def test_clip_zero_and_masked_supertoken_rows():
     assert vid not in tok
 
 
+# Tie rows on the MFMA endpoint path (128-, 320- and 256-row tiles): h row
+# e_c makes the cloud partial 0 (so q = 0, s = 0) and the fused logit of
+# position j equal to W_end[S_j, c] exactly; column c holds -1 except +1 at
+# the positions of pattern c.  The patterns put the maxima 32 positions apart
+# (one lane, two column slots of a tile), in two lanes of one tile, in two
+# tiles (one of them the ragged last), and three apart.  All-zero rows tie
+# at every position.  Eq. 15 with the lowest-id reading of ties.
+TIE_PATTERNS = [(5, 37), (300, 290), (2999, 700), (40, 8, 2000)]
+
+
+@pytest.mark.parametrize("rows,tie_rows,zero_row", [
+    (48, (0, 7, 20, 47), 30),
+    (300, (0, 130, 257, 299), 150),
+    (512, (0, 255, 256, 511), 100),
+], ids=["M48", "M300", "M512"])
+def test_mfma_endpoint_ties_go_to_the_lowest_id(rows, tie_rows, zero_row):
+    cfg = Config("ties_mfma", 40 + rows, d=256, d_end=64, vocab=6000, n_sub=3000,
+                 subset_kind="choice", sessions=rows // 4, rows_per_session=4)
+    wl = make_workload(cfg)
+    one, minus_one = np.uint16(0x3F80), np.uint16(0xBF80)   # bf16 +1, -1
+    h = wl.h_bits.copy()
+    we = wl.w_end_bits.copy()
+    for c, (r, pat) in enumerate(zip(tie_rows, TIE_PATTERNS)):
+        h[r] = 0
+        h[r, c] = one
+        we[wl.subset, c] = minus_one
+        we[wl.subset[list(pat)], c] = one
+    h[zero_row] = 0
+    stats, (q, s, z, tok, acc, f) = run_greedy_case(wl, h_bits=h, w_end_bits=we,
+                                                    tag=f"endpoint ties M={rows}")
+    for r, pat in zip(tie_rows, TIE_PATTERNS):
+        assert s[r] == 0 and not q[r].any()
+        assert tok[r] == wl.subset[min(pat)], (r, pat, tok[r])
+    assert tok[zero_row] == wl.subset[0]
+
+
 # ---------------------------------------------------------------------------
 # fp8 cloud weights
 # ---------------------------------------------------------------------------
