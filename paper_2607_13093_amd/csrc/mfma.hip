@@ -221,48 +221,62 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
   V red[P];
 #pragma unroll
   for (int t = FM * 16; t < P; ++t) red[t] = V(0);
+  // The fuse epilogue of a tile that lies inside the output and holds 8-bit
+  // codes (the common case) runs a copy of the loop without the bounds and
+  // code-width checks.  Only the 256-row tiles of 8 waves have one: on
+  // 320-row tiles (80 row keys per lane) a second copy spilled, and the
+  // 4-wave kernels spill more with it.
+  auto fill = [&](auto fast) {
+    constexpr bool kFast = decltype(fast)::value;
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
+    for (int i = 0; i < FM; ++i) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int row = m0 + lrow;
-      V best = V(0);
-      // fuse: the lane's largest fused value of the row and its column (the
-      // first, so the lowest, of equal values); one key per row afterwards
-      float bv = 0.0f;
-      int bc = -1;
+      for (int r = 0; r < 16; ++r) {
+        const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int row = m0 + lrow;
+        V best = V(0);
+        // fuse: the lane's largest fused value of the row and its column (the
+        // first, so the lowest, of equal values); one key per row afterwards
+        float bv = 0.0f;
+        int bc = -1;
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int lcol = wn * TN + j * 32 + (lane & 31);
-        const int col = n0 + lcol;
-        if (row < M && col < n) {
-          const float dot = acc[i][j][r];
-          if constexpr (kCloud) {
-            const float zv = cloud_value<WT>(dot, a, s_ids[lcol]);
-            if (EPI == kEpiCloud || a.z) __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
-            best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
-          } else {
-            int code;
-            if (a.qbits == 8) {
-              code = s_q[lrow * BN + lcol];
+        for (int j = 0; j < FN; ++j) {
+          const int lcol = wn * TN + j * 32 + (lane & 31);
+          const int col = n0 + lcol;
+          if (kFast || (row < M && col < n)) {
+            const float dot = acc[i][j][r];
+            if constexpr (kCloud) {
+              const float zv = cloud_value<WT>(dot, a, s_ids[lcol]);
+              if (EPI == kEpiCloud || a.z) __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
+              best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
             } else {
-              const int byte = (uint8_t)s_q[lrow * (BN / 2) + (lcol >> 1)];
-              const int nib = (lcol & 1) ? (byte >> 4) : (byte & 15);
-              code = nib >= 8 ? nib - 16 : nib;
-            }
-            const float f = __builtin_fmaf((float)code, s_qs[lrow], dot * s_qs[BM + lrow]);
-            if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
-            if (bc < 0 || f > bv) {
-              bv = f;
-              bc = col;
+              int code;
+              if (kFast || a.qbits == 8) {
+                code = s_q[lrow * BN + lcol];
+              } else {
+                const int byte = (uint8_t)s_q[lrow * (BN / 2) + (lcol >> 1)];
+                const int nib = (lcol & 1) ? (byte >> 4) : (byte & 15);
+                code = nib >= 8 ? nib - 16 : nib;
+              }
+              const float f = __builtin_fmaf((float)code, s_qs[lrow], dot * s_qs[BM + lrow]);
+              if (a.f) __builtin_nontemporal_store(f, a.f + (int64_t)row * n + col);
+              if (bc < 0 || f > bv) {
+                bv = f;
+                bc = col;
+              }
             }
           }
         }
+        if constexpr (!kCloud) best = bc >= 0 ? argmax_key_m(bv, bc) : 0ull;
+        red[i * 16 + r] = best;
       }
-      if constexpr (!kCloud) best = bc >= 0 ? argmax_key_m(bv, bc) : 0ull;
-      red[i * 16 + r] = best;
     }
+  };
+  if constexpr (kCloud || BM != 256 || WM * WN != 8) {
+    fill(std::false_type{});
+  } else {
+    if (m0 + BM <= M && n0 + BN <= n && a.qbits == 8) fill(std::true_type{});
+    else fill(std::false_type{});
   }
   half_wave_max_transpose<P>(red, lane);
   constexpr int PER = P / 32;
