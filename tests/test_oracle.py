@@ -351,6 +351,21 @@ def test_format_invariants(bits, block):
     assert oracle.payload_bytes(n, bits, block) == -(-n * bits // 8) + 4 * s.shape[1]
 
 
+def test_payload_bytes_pinned_to_eq21():
+    # eq. 21 (Section 7.6): codes cost |V_l| * b / 8 bytes; the paper's figure
+    # for a full 150,000-entry int8 logit row is about 146.5 KB.  The other
+    # cases are counted by hand (tests/golden/payload_eq21.json); the odd
+    # lengths and partial blocks fail a floor in place of a ceiling.
+    with open(os.path.join(GOLDEN, "payload_eq21.json")) as f:
+        g = json.load(f)
+    fig = g["paper_figure"]
+    codes = oracle.payload_bytes(fig["n"], fig["bits"], 0) - 4
+    assert codes == fig["code_bytes"]
+    assert round(codes / 1024, 1) == fig["kib_rounded_to_0_1"]
+    for c in g["hand_counted"]:
+        assert oracle.payload_bytes(c["n"], c["bits"], c["block"]) == c["bytes"], c
+
+
 def test_format_4bit_worked_example():
     # two blocks of 4 positions, codes in [-7, 7]
     z = np.array([[0.7, -1.4, 0.35, 0.0, 2.0, 3.5, -0.25, 7.0, 1.0]], dtype=np.float32)
