@@ -33,6 +33,7 @@ from .split_head import (  # noqa: F401
     philox4x32_10,
     philox_uniform,
     sample_select,
+    sample_candidates,
     accept_lengths,
     cloud_call,
     endpoint_call,

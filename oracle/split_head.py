@@ -525,6 +525,56 @@ def sample_select(f, subset, temperature, top_p, seed, rows_per_session, row_ind
     return tokens, {"nucleus": ksize, "cut_margin": cut_margin, "cdf_margin": cdf_margin}
 
 
+def sample_candidates(f, subset, temperature, top_p, seed, rows_per_session, margin,
+                      row_index=None):
+    """Every token the sampler of ``sample_select`` can return for a row when
+    each cumulative mass it compares may be off by up to ``margin``
+    (probability units): the nucleus cut may fall anywhere from the first
+    prefix reaching top_p - margin to the first reaching top_p + margin, and
+    for each such nucleus the draw may land on any member whose CDF interval
+    comes within ``margin`` of the target (eq. 15 with the top-p cut and the
+    ascending-id inverse CDF of ``sample_select``).
+
+    Returns a list of sorted int32 arrays of vocabulary ids, one per row; with
+    margin 0 each holds exactly ``sample_select``'s token (a target that sits
+    on an interval edge adds the member the edge belongs to).  Pinned by that
+    identity and by a row with two equal weights at a CDF boundary, where both
+    ids are candidates (tests/test_oracle.py).
+    """
+    f = np.asarray(f, dtype=np.float32)
+    subset = np.asarray(subset, dtype=np.int64)
+    M, n = f.shape
+    tau = float(np.float32(temperature))
+    tp = float(np.float32(top_p))
+    out = []
+    for m in range(M):
+        x = f[m].astype(np.float64)
+        e = np.exp((x - x.max()) / tau)
+        p = e / e.sum()
+        order = np.lexsort((subset, -p))
+        cum = np.cumsum(p[order])
+        if tp >= 1.0:
+            k_lo = k_hi = n
+        else:
+            k_lo = min(int(np.searchsorted(cum, tp - margin, side="left")) + 1, n)
+            k_hi = min(int(np.searchsorted(cum, tp + margin, side="left")) + 1, n)
+        g = m if row_index is None else int(row_index[m])
+        u = philox_uniform(seed, g % rows_per_session, g // rows_per_session)
+        cand = set()
+        for K in range(max(k_lo, 1), k_hi + 1):
+            members = np.sort(order[:K])
+            run = np.cumsum(p[members])
+            target = u * run[-1]
+            before = np.concatenate(([0.0], run[:-1]))
+            # member i is drawn when before[i] <= target < run[i]
+            hit = (before <= target + margin) & (run >= target - margin)
+            if target + margin >= run[-1]:
+                hit[-1] = True          # the fallback pick when rounding leaves none
+            cand.update(subset[members[hit]].tolist())
+        out.append(np.array(sorted(cand), dtype=np.int32))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # verification of the drafts (Section 5.5, Algorithm 1)
 # ---------------------------------------------------------------------------

@@ -190,18 +190,39 @@ def exempt_rows(f_ref, bound):
     return (slack >= 0).any(axis=1)
 
 
-def check_tokens_and_accept(tok_gpu, acc_gpu, ref_tok, ref_acc, exempt, subset, S, R):
+def check_tokens_and_accept(tok_gpu, acc_gpu, ref_tok, ref_acc, exempt, subset, S, R,
+                            f_ref, bound, drafts):
+    """Tokens: in S always; equal to the reference outside exempt rows; on an
+    exempt row that differs, the GPU's pick j must still be a near-maximum of
+    the reference logits, f_ref[j*] - f_ref[j] <= bound[j*] + bound[j] (what
+    the GPU's elementwise error bound allows, and nothing more).
+    Accept lengths: the GPU's must equal the verification rule applied to the
+    GPU's own tokens in every session, and the oracle's where no exempt row
+    among r <= a decides it."""
+    subset = np.asarray(subset)
     assert np.all(np.isin(tok_gpu, subset)), "token outside the subset"
     bad = (tok_gpu != ref_tok) & ~exempt
     assert not bad.any(), f"{bad.sum()} non-exempt token mismatches (rows {np.flatnonzero(bad)[:8]})"
-    k = R - 1
+    M = tok_gpu.shape[0]
+    r = np.arange(M)
+    f = f_ref.astype(np.float64)
+    jstar = np.argmax(f_ref, axis=1)
+    pos = np.searchsorted(subset, tok_gpu)
+    gap = f[r, jstar] - f[r, pos]
+    near = gap <= bound[r, jstar] + bound[r, pos]
+    diff = tok_gpu != ref_tok
+    assert near[diff].all(), (f"exempt rows {np.flatnonzero(diff & ~near)[:8]}: the GPU's token is not "
+                              f"within the error bound of the row maximum")
+    own = oracle.accept_lengths(tok_gpu, drafts, S, R)
+    np.testing.assert_array_equal(acc_gpu, own, err_msg="accept lengths differ from the rule "
+                                                        "applied to the GPU's own tokens")
     ex = exempt.reshape(S, R)
     for s in range(S):
         a = int(ref_acc[s])
         if ex[s, :a + 1].any():
             continue
         assert acc_gpu[s] == a, f"accept length of session {s}: gpu {acc_gpu[s]} oracle {a}"
-    return {"token_mismatch": int((tok_gpu != ref_tok).sum()), "token_exempt_rows": int(exempt.sum())}
+    return {"token_mismatch": int(diff.sum()), "token_exempt_rows": int(exempt.sum())}
 
 
 def block_cols(n, block):
@@ -230,7 +251,7 @@ def stage_d_greedy(q_gpu, s_gpu, f_gpu, tok_gpu, acc_gpu, wl, drafts, rows=None,
     ref_acc = oracle.accept_lengths(ref_tok, drafts, S, cfg.rows_per_session)
     ex = exempt_rows(f_ref, bound)
     return check_tokens_and_accept(tok_gpu, acc_gpu, ref_tok, ref_acc, ex, wl.subset, S,
-                                   cfg.rows_per_session)
+                                   cfg.rows_per_session, f_ref, bound, drafts)
 
 
 def stage_e_greedy(q_gpu, s_gpu, tok_gpu, acc_gpu, orc_cloud, wl, drafts, rows=None, block=0):
@@ -252,4 +273,18 @@ def stage_e_greedy(q_gpu, s_gpu, tok_gpu, acc_gpu, orc_cloud, wl, drafts, rows=N
              + ULP * np.abs(f_ref.astype(np.float64)))
     ex = exempt_rows(f_ref, bound)
     return check_tokens_and_accept(tok_gpu, acc_gpu, ref_tok, ref_acc, ex, wl.subset, S,
-                                   cfg.rows_per_session)
+                                   cfg.rows_per_session, f_ref, bound, drafts)
+
+
+def check_boundary_rows(tok_gpu, tok_ref, f, subset, cfg, rows, margin):
+    """A row exempt in stage D (the same fused logits on both sides) may only
+    differ by a decision at a boundary: the GPU's token must be one the
+    oracle's sampler reaches when the cut or the draw moves by `margin`."""
+    diff = np.flatnonzero(tok_gpu != tok_ref)
+    if diff.size == 0:
+        return
+    cand = oracle.sample_candidates(f[diff], subset, cfg.temperature, cfg.top_p, cfg.philox_seed,
+                                    cfg.rows_per_session, margin, row_index=np.asarray(rows)[diff])
+    for m, c in zip(diff, cand):
+        assert tok_gpu[m] in c, (f"row {rows[m]}: sampled {tok_gpu[m]}, oracle {tok_ref[m]}, "
+                                 f"boundary candidates {c[:8]}")

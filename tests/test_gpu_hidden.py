@@ -116,13 +116,14 @@ def run_hq_case(wl, tag, bits=8, block=0, sessions=None):
         acc_ref = oracle.accept_lengths(tok_ref, drafts, len(sess), R)
         ex = P.exempt_rows(f_ref, bound)
         st = P.check_tokens_and_accept(th[rows], ah[sess], tok_ref, acc_ref, ex, wl.subset,
-                                       len(sess), R)
+                                       len(sess), R, f_ref, bound, drafts)
     else:
         tok_ref, info = oracle.sample_select(fh, wl.subset, cfg.temperature, cfg.top_p,
                                              cfg.philox_seed, R, row_index=rows)
         ex = (info["cut_margin"] <= 1e-9) | (info["cdf_margin"] <= 1e-9)
         bad = (th[rows] != tok_ref) & ~ex
         assert not bad.any(), f"{bad.sum()} sampled tokens differ"
+        P.check_boundary_rows(th[rows], tok_ref, fh, wl.subset, cfg, rows, 1e-9)
         np.testing.assert_array_equal(ah, oracle.accept_lengths(th, drafts_all, S_all, R))
         st = {"exempt": int(ex.sum())}
     say(f"[gpu] {tag}: ok df_max={df.max(initial=0.0):.3e} {st}")

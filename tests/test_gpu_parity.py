@@ -96,10 +96,27 @@ def test_batched_full_pipeline():
     run_greedy_case(make_workload(CONFIGS["batched"]))
 
 
+# One whole session in each 256-row tile of the 2048-row launch (session s
+# holds rows 8s .. 8s+7, so sessions 0, 32, ..., 224 open tiles 0 .. 7),
+# plus the last session.
+DENSE_SESSIONS = list(range(0, 256, 32)) + [255]
+
+
 @pytest.mark.parametrize("name", ["dense_full", "dense_sub"])
 def test_dense_sampled_sessions(name):
-    # the full 2048-row launch; the oracle checks 4 whole sessions (32 rows)
-    run_greedy_case(make_workload(CONFIGS[name]), sessions=[0, 77, 160, 255])
+    # the full 2048-row launch, as the benchmark runs it; the oracle checks
+    # 9 whole sessions (72 rows) spread over every row tile
+    run_greedy_case(make_workload(CONFIGS[name]), sessions=DENSE_SESSIONS)
+
+
+@pytest.mark.parametrize("d_end", [48, 96])
+def test_paper_shape_full_vocabulary(d_end):
+    # the paper's evaluation shape (Section 7.3): hidden 4096, a vocabulary of
+    # 150000 ids with every id kept (the mixed-language mode), d_end 48 or 96
+    # (Table 6), one session verifying k = 4 drafts
+    cfg = Config("paper_shape", 60 + d_end, d=4096, d_end=d_end, vocab=150000, n_sub=150000,
+                 subset_kind="full", sessions=1, rows_per_session=5)
+    run_greedy_case(make_workload(cfg), tag=f"paper shape d_end={d_end}")
 
 
 # ---------------------------------------------------------------------------

@@ -155,6 +155,7 @@ def test_payload_format_sampling():
     exempt = (info["cut_margin"] <= 1e-9) | (info["cdf_margin"] <= 1e-9)
     bad = (th != tok_ref) & ~exempt
     assert not bad.any(), f"{bad.sum()} sampled tokens differ"
+    P.check_boundary_rows(th, tok_ref, fh, wl.subset, cfg, rows, 1e-9)
     np.testing.assert_array_equal(ah, oracle.accept_lengths(th, drafts, cfg.sessions,
                                                             cfg.rows_per_session))
     say(f"[gpu] payload sampling: ok, exempt {int(exempt.sum())}")

@@ -78,6 +78,7 @@ def run_sample_case(wl, sessions=None, tag="", h_bits=None):
     ex_d = _exempt(info_d)
     bad = (th[rows] != tok_d) & ~ex_d
     assert not bad.any(), f"stage D: {bad.sum()} sampled tokens differ (rows {rows[bad][:8]})"
+    P.check_boundary_rows(th[rows], tok_d, fh[rows], wl.subset, cfg, rows, EPS)
     # accept lengths from the GPU's tokens (exact integer rule)
     acc_ref = oracle.accept_lengths(th, drafts, cfg.sessions, R)
     np.testing.assert_array_equal(ah, acc_ref)
@@ -88,6 +89,7 @@ def run_sample_case(wl, sessions=None, tag="", h_bits=None):
     ex_e = _exempt(info_orc, extra)
     bad_e = (th[rows] != tok_orc) & ~ex_e
     assert not bad_e.any(), f"stage E: {bad_e.sum()} tokens differ"
+    check_in_perturbed_nucleus(th[rows], tok_orc, f_orc, wl.subset, cfg, extra)
     stats["D"] = {"rows": len(rows), "exempt": int(ex_d.sum()),
                   "mismatch": int((th[rows] != tok_d).sum()),
                   "nucleus_mean": float(np.mean(info_d["nucleus"]))}
@@ -95,6 +97,31 @@ def run_sample_case(wl, sessions=None, tag="", h_bits=None):
                   "df_max": float(df.max(initial=0.0))}
     say(f"[gpu] {tag or cfg.name}: ok {stats}")
     return stats, th, fh
+
+
+def check_in_perturbed_nucleus(tok_gpu, tok_ref, f_ref, subset, cfg, margin):
+    """Stage E: where the two pipelines' fused logits differ by up to d, every
+    weight moves by at most a factor exp(d / tau) = exp(margin / 4) and so
+    does the normaliser, so each probability by at most r = exp(margin / 2).
+    A token the GPU may sample lies in its nucleus: the GPU mass of the tokens
+    it ranks above is below top_p.  Every token whose oracle probability
+    exceeds the GPU token's by the factor r^2 is ranked above it on the GPU,
+    with a GPU mass no smaller than its oracle mass over r, so that mass over
+    r must be below top_p."""
+    diff = np.flatnonzero(tok_gpu != tok_ref)
+    if diff.size == 0 or cfg.top_p >= 1.0:
+        return
+    tau = float(np.float32(cfg.temperature))
+    r = np.exp(margin / 2.0)
+    subset = np.asarray(subset)
+    for m in diff:
+        x = f_ref[m].astype(np.float64)
+        p = np.exp((x - x.max()) / tau)
+        p /= p.sum()
+        pt = p[np.searchsorted(subset, tok_gpu[m])]
+        above = p[p > pt * r * r].sum() / r
+        assert above < float(np.float32(cfg.top_p)), (
+            f"stage E row {m}: token {tok_gpu[m]} lies outside the perturbed nucleus")
 
 
 def _sample_rows(f, subset, cfg, rows):

@@ -539,6 +539,68 @@ def test_sampling_walks_in_ascending_id_order():
         assert tok[row] == S[int(np.sum(edges <= u))]
 
 
+def test_sample_candidates_margin_zero_is_the_sample():
+    rng = np.random.default_rng(11)
+    f = rng.standard_normal((30, 200)).astype(np.float32)
+    S = np.sort(rng.choice(4000, 200, replace=False))
+    tok, _ = oracle.sample_select(f, S, 0.7, 0.9, 5, 3)
+    cand = oracle.sample_candidates(f, S, 0.7, 0.9, 5, 3, 0.0)
+    for m in range(30):
+        assert list(cand[m]) == [tok[m]]
+
+
+def test_sample_candidates_cdf_edge():
+    # p = (0.1, 0.2, 0.3, 0.4) on ids (10, 20, 30, 40), no cut: interval edges
+    # at 0.1, 0.3, 0.6.  A margin past the target's distance to the nearest
+    # edge (but short of the next edge) adds the id on the other side of it,
+    # one below that distance does not.
+    p = np.array([0.1, 0.2, 0.3, 0.4])
+    f = np.log(p).astype(np.float32)
+    S = np.array([10, 20, 30, 40])
+    pe = np.exp(f.astype(np.float64))
+    pe /= pe.sum()
+    edges = np.cumsum(pe)[:-1]
+    for row in range(24):
+        u = oracle.philox_uniform(77, row % 4, row // 4)
+        i = int(np.sum(edges <= u))
+        dist = np.abs(edges - u)
+        k = int(np.argmin(dist))
+        other = S[k + 1] if u < edges[k] else S[k]
+        d, d2 = np.sort(dist)[:2]
+        if not d2 > d:
+            continue
+        # margins below the nearest edge, and between the nearest and the next
+        one = oracle.sample_candidates(_rows(f, 1), S, 1.0, 1.0, 77, 4, d * 0.5, row_index=[row])[0]
+        two = oracle.sample_candidates(_rows(f, 1), S, 1.0, 1.0, 77, 4, (d + d2) / 2,
+                                       row_index=[row])[0]
+        assert list(one) == [S[i]]
+        assert sorted(two) == sorted({int(S[i]), int(other)})
+
+
+def test_sample_candidates_nucleus_cut():
+    # p = (0.05, 0.5, 0.15, 0.3) on ids (1, 2, 3, 4), top_p 0.78: the exact
+    # nucleus is {2, 4} (0.5 + 0.3 >= 0.78); a margin of 0.025 lets the cut
+    # take {2, 3, 4} too (0.95 >= 0.805).  Counted by hand for u in
+    # [0.62, 0.64]: nucleus {2, 4} (run 0.5, 0.8) puts the target 0.8u in
+    # [0.496, 0.512], within 0.025 of the edge 0.5 -> ids 2 and 4; nucleus
+    # {2, 3, 4} (run 0.5, 0.65, 0.95) puts 0.95u in [0.589, 0.608], whose
+    # window [0.564, 0.633] lies inside id 3's interval [0.5, 0.65) -> id 3.
+    p = np.array([0.05, 0.5, 0.15, 0.3])
+    f = np.log(p).astype(np.float32)
+    S = np.array([1, 2, 3, 4])
+    hits = 0
+    for row in range(4000):
+        u = oracle.philox_uniform(9, row % 4, row // 4)
+        if not (0.62 <= u <= 0.64):
+            continue
+        c = oracle.sample_candidates(_rows(f, 1), S, 1.0, 0.78, 9, 4, 0.025, row_index=[row])[0]
+        assert list(c) == [2, 3, 4]
+        c0 = oracle.sample_candidates(_rows(f, 1), S, 1.0, 0.78, 9, 4, 0.0, row_index=[row])[0]
+        assert list(c0) == [2 if 0.8 * u < 0.5 else 4]
+        hits += 1
+    assert hits >= 20
+
+
 def test_philox_uniform_takes_the_top_24_bits_of_word_0():
     # seed 0, row 0, session 0 is counter 0 / key 0: word 0 of the first known answer
     assert oracle.philox_uniform(0, 0, 0) == (0x6627E8D5 >> 8) * 2.0 ** -24
