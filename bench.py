@@ -2,12 +2,17 @@
 
 One step = one pass of the whole hot path over one batch: sph_cloud_partial
 (gathered partial logits, clip, per-row int8) then sph_fuse_verify (endpoint
-partial, dequantise + fuse + mask, greedy select, accepted draft prefix).
+partial, dequantise + fuse + mask, greedy select or temperature + top-p
+sample, accepted draft prefix).
 
-Default workload: single-session decode, d=4096, d_end=256, V=128256, a
-49152-id language subset (one block of 32768 ids plus 16384 scattered ids),
-1 session x 5 rows (k=4 drafts), bf16 h/W, clip 30, int8 payload with one
-scale per row (--bits / --block choose another payload format).
+Headline workload (default): the largest configuration, dense large-M with
+the full vocabulary: d=8192, d_end=512, V=128256, every id kept (no mask),
+256 sessions x 8 rows (k=7 drafts) = 2048 rows, bf16 h/W, clip 30, int8
+payload with one scale per row (--bits / --block choose another payload
+format).  The cloud projection is MFMA bound there.  The other workloads
+(dense subset, batched verify, sampling with fp8 weights, single-session
+decode, tiny) run after it in the same job and are reported under
+"configs" (--workload picks another headline, --others none skips them).
 
 Prints ONE JSON line.  `value` is rows*vocab/s = M*|S| / (seconds per step)
 with every input resident in HBM before the timed region; three copies of
@@ -31,7 +36,13 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16; fp8 weights are widened to bf16 before the MFMA
 N_COPIES = 3
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "cloud_gemv_decode_traffic.txt")
+PROFILES = os.path.join(ROOT, "profiles")
+# workloads reported after the headline one, in this order
+OTHER_WORKLOADS = ("dense_sub", "batched", "sample_fp8", "decode", "tiny")
+# the kernel source files each traced kernel is built from (for the counter
+# summaries' source digests)
+KERNEL_SOURCES = {"cloud_gemv": ("gemv.hip", "sph_internal.h"),
+                  "cloud_mfma": ("mfma.hip", "sph_internal.h")}
 
 
 def parse():
@@ -39,7 +50,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", default="decode")
+    p.add_argument("--workload", default="dense_full")
+    p.add_argument("--others", choices=("all", "none"), default="all",
+                   help="also time every other workload (fewer steps) and report it under "
+                        "'configs'")
     p.add_argument("--bits", type=int, default=8, choices=(4, 8),
                    help="payload code width b (eq. 18)")
     p.add_argument("--block", type=int, default=0,
@@ -130,22 +144,23 @@ def attainable_peaks(dev):
             "gemm_bf16_tflops": gemm_tflops}
 
 
-def source_digest():
+def source_digest(kernel):
     h = hashlib.sha256()
-    for name in ("gemv.hip", "sph_internal.h"):
+    for name in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, "paper_2607_13093_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(digest):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+def read_traffic(kernel, workload, digest):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (profiles/<kernel>_<workload>_traffic.txt), if
+    it was taken on the current kernel source; else None."""
     try:
         kv = {}
-        with open(TRAFFIC_PROFILE) as f:
+        with open(os.path.join(PROFILES, f"{kernel}_{workload}_traffic.txt")) as f:
             for line in f:
-                if ":" in line:
+                if ":" in line and not line.startswith("#"):
                     k, v = line.split(":", 1)
                     kv[k.strip()] = v.strip()
         if kv.get("kernel_source_sha256_16") != digest:
@@ -153,6 +168,12 @@ def read_traffic(digest):
         return float(kv["hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
+
+
+def dtype_of(cfg):
+    """Arithmetic type of the path: bf16 products with fp32 accumulation;
+    fp8 weights are widened exactly to bf16 before the products."""
+    return "bf16" if cfg.wtype == "bf16" else "e4m3 weights widened to bf16"
 
 
 def cpu_baseline(wl, seconds):
@@ -284,33 +305,25 @@ def sweep(args):
         sub.close()
 
 
-def main():
-    args = parse()
-    if args.sweep:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
-        sweep(args)
-        return
-    if args.copy_calibration:
-        copy_calibration(args.copy_calibration)
-        return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no "
-              "multi-GPU path", file=sys.stderr)
-        sys.exit(2)
+def progress(msg):
+    """A progress line on stderr (stdout carries only the JSON result)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
+
+def run_workload(wl, args, steps, warmup):
+    """Upload one workload, time `steps` steps (after `warmup`), then the same
+    steps again with the library's kernel trace on.  Returns the results and
+    frees the device tensors."""
     import numpy as np
     import torch
 
     import paper_2607_13093_amd as sph
-    from synth import CONFIGS, make_drafts, make_workload
+    from synth import make_drafts
 
-    cfg = CONFIGS[args.workload]
-    wl = make_workload(cfg)
+    cfg = wl.cfg
     n = len(wl.subset)
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    progress(f"{cfg.name}: upload, {warmup} warm-up and {steps} timed steps")
 
     def up(a, dt=None):
         t = torch.from_numpy(np.ascontiguousarray(a))
@@ -389,7 +402,7 @@ def main():
     if cfg.k:
         drafts.copy_(torch.from_numpy(make_drafts(cfg, tok.cpu().numpy(), wl.subset)))
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
 
@@ -400,19 +413,19 @@ def main():
         t_stop = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         t_start.record(stream)
-        for i in range(args.steps):
+        for i in range(steps):
             step(i)
         t_stop.record(stream)
         torch.cuda.synchronize()
-        return t_start.elapsed_time(t_stop) / args.steps
+        return t_start.elapsed_time(t_stop) / steps
 
     # Timed region: K steps, no instrumentation.
     ms_step = timed_loop()
     if args.seal and int(okm.min()) != 1:
         raise SystemExit("sealed payload rows failed authentication")
     # Kernel durations: the same K steps again with the library's trace on
-    # (HIP events recorded on the launch stream around every kernel).
-    cap = 16 * args.steps + 16
+    # (events attached to the kernel dispatches on the launch stream).
+    cap = 16 * steps + 16
     sph.trace_start(cap)
     ms_step_traced = timed_loop()
     recs = sph.trace_collect(cap)
@@ -420,73 +433,157 @@ def main():
     by = {}
     for name, ms in recs:
         by.setdefault(name, []).append(ms)
-    if "cloud_mfma" in by:
-        kern = "cloud_mfma"
-        k_ms = float(np.mean(by[kern]))
-        flops = 2.0 * M * n * cfg.d_cloud
+    kern = "cloud_mfma" if "cloud_mfma" in by else "cloud_gemv"
+    k_ms = float(np.mean(by[kern]))
+    nbytes = algorithmic_bytes(cfg, n)
+    flops = 2.0 * M * n * cfg.d_cloud
+    digest = source_digest(kern)
+    traffic = read_traffic(kern, cfg.name, digest)
+    if kern == "cloud_mfma":
         achieved = flops / (k_ms * 1e-3) / 1e12
         roof = {"kernel": kern, "bound": "mfma", "achieved": achieved,
                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
                 "algorithmic_flops_per_launch": flops,
-                "algorithmic_bytes_per_launch": algorithmic_bytes(cfg, n), "avg_launch_ms": k_ms}
-    else:
-        kern = "cloud_gemv"
-        k_ms = float(np.mean(by[kern]))
-        nbytes = algorithmic_bytes(cfg, n)
-        achieved = nbytes / (k_ms * 1e-3) / 1e9
-        digest = source_digest()
-        roof = {"kernel": kern, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                "traffic": read_traffic(digest) if args.workload == "decode" else None,
                 "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": k_ms,
                 "kernel_source_sha256_16": digest}
-
-    att = attainable_peaks(dev)
-    att_peak = att["read_gbs"] if roof["bound"] == "hbm" else att["mfma_bf16_tflops"]
-    roof["attainable_peak"] = att_peak
-    roof["frac_attainable"] = roof["achieved"] / att_peak
-
-    out = {
-        "metric": "split-head rows*vocab/s",
-        "value": M * n / (ms_step * 1e-3),
-        "unit": "rows*vocab/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {
-            "workload": f"{cfg.name}: d={cfg.d} d_end={cfg.d_end} V={cfg.vocab} |S|={n} "
-                        f"sessions={cfg.sessions} rows={cfg.rows_per_session} {cfg.wtype} "
-                        f"{cfg.mode} clip={cfg.clip_c}",
-            "rows": M,
-            "subset": n,
-            "payload": f"b={bits} " + ("one scale per row" if block == 0 else
-                                       f"one scale per {block} positions"),
-            "payload_bytes_per_row": code_bytes + 4 * nb,
-            "hidden_state": "int8 codes + fp32 scale per row" if args.hidden_int8 else "bf16",
-            "sealed": "AES-128-GCM, one message per row (codes, then scales)" if args.seal else "no",
-        },
-        "roofline": roof,
-        "attainable": att,
+    else:
+        achieved = nbytes / (k_ms * 1e-3) / 1e9
+        roof = {"kernel": kern, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": k_ms,
+                "kernel_source_sha256_16": digest}
+    # the roofline of the cloud call's dominant kernel: the slower of its byte
+    # and flop times at the nominal peaks (both matter at the ridge)
+    t_roof_ms = max(nbytes / (HBM_PEAK_GBS * 1e9), flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e3
+    res = {
+        "cfg": cfg, "n": n, "ms_step": ms_step, "ms_step_traced": ms_step_traced, "roof": roof,
+        "roofline_ms": t_roof_ms, "roofline_frac": t_roof_ms / k_ms,
         "kernels_ms": {k: float(np.mean(v)) for k, v in by.items()},
-        # kernel time of each call per step (the cloud call's and the endpoint
-        # call's kernels; launch gaps excluded) and of the pair
         "calls_ms": {
             "cloud": float(sum(np.mean(v) for k, v in by.items() if k.startswith("cloud_"))),
             "endpoint": float(sum(np.mean(v) for k, v in by.items() if k.startswith("fuse_"))),
             "pair": float(sum(np.mean(v) for k, v in by.items()
                               if k.startswith("cloud_") or k.startswith("fuse_"))),
         },
-        "ms_per_step_traced": ms_step_traced,
+        "payload_bytes_per_row": code_bytes + 4 * nb,
+    }
+    del h, wc, we, wsc, q, s, tok, acc, ws_c, ws_f, hq, hs, drafts
+    sub.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def workload_text(cfg, n):
+    return (f"{cfg.name}: d={cfg.d} d_end={cfg.d_end} V={cfg.vocab} |S|={n} "
+            f"sessions={cfg.sessions} rows={cfg.rows_per_session} {cfg.wtype} "
+            f"{cfg.mode} clip={cfg.clip_c}")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path, and this job uses a single MI355X", file=sys.stderr)
+        sys.exit(2)
+    if args.sweep:
+        sweep(args)
+        return
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+
+    import torch
+
+    from synth import CONFIGS, make_workload, with_subset
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.workload]
+    progress(f"{cfg.name}: drawing the synthetic inputs")
+    wl = make_workload(cfg)
+    r = run_workload(wl, args, args.steps, args.warmup)
+    progress("attainable peaks")
+    n = r["n"]
+    roof = r["roof"]
+    att = attainable_peaks(dev)
+    att_peak = att["read_gbs"] if roof["bound"] == "hbm" else att["mfma_bf16_tflops"]
+    roof["attainable_peak"] = att_peak
+    roof["frac_attainable"] = roof["achieved"] / att_peak
+    bits, block = args.bits, args.block
+
+    out = {
+        "metric": "split-head rows*vocab/s",
+        "value": cfg.M * n / (r["ms_step"] * 1e-3),
+        "unit": "rows*vocab/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": r["ms_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype_of(cfg),
+        "data": "synthetic",
+        "config": {
+            "workload": workload_text(cfg, n),
+            "rows": cfg.M,
+            "subset": n,
+            "payload": f"b={bits} " + ("one scale per row" if block == 0 else
+                                       f"one scale per {block} positions"),
+            "payload_bytes_per_row": r["payload_bytes_per_row"],
+            "hidden_state": "int8 codes + fp32 scale per row" if args.hidden_int8 else "bf16",
+            "sealed": "AES-128-GCM, one message per row (codes, then scales)" if args.seal else "no",
+        },
+        "roofline": roof,
+        "attainable": att,
+        "kernels_ms": r["kernels_ms"],
+        # kernel time of each call per step (the cloud call's and the endpoint
+        # call's kernels; launch gaps excluded) and of the pair
+        "calls_ms": r["calls_ms"],
+        "ms_per_step_traced": r["ms_step_traced"],
     }
     if args.cpu_seconds > 0:
+        progress("CPU baseline (the oracle)")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+
+    if args.others == "all":
+        # every other workload, fewer steps; the dense subset reuses the dense
+        # workload's hidden states and weights (same seed streams)
+        configs = {}
+        base = wl
+        for name in OTHER_WORKLOADS:
+            if name == args.workload:
+                continue
+            c2 = CONFIGS[name]
+            progress(f"{name}: drawing the synthetic inputs")
+            try:
+                w2 = with_subset(base, c2)
+            except ValueError:
+                base = None
+                w2 = make_workload(c2)
+            r2 = run_workload(w2, args, min(args.steps, 50), min(args.warmup, 5))
+            k2 = r2["roof"]["kernel"]
+            configs[name] = {
+                "workload": workload_text(c2, r2["n"]),
+                "dtype": dtype_of(c2),
+                "ms_per_step": r2["ms_step"],
+                "value": c2.M * r2["n"] / (r2["ms_step"] * 1e-3),
+                "unit": "rows*vocab/s",
+                "dominant_kernel": k2,
+                "dominant_kernel_us": r2["roof"]["avg_launch_ms"] * 1e3,
+                "bound": r2["roof"]["bound"],
+                "achieved": r2["roof"]["achieved"],
+                "achieved_unit": r2["roof"]["unit"],
+                "frac": r2["roof"]["frac"],
+                "roofline_us": r2["roofline_ms"] * 1e3,
+                "roofline_frac": r2["roofline_frac"],
+                "traffic": r2["roof"]["traffic"],
+                "kernels_ms": r2["kernels_ms"],
+            }
+            del w2
+        out["configs"] = configs
     print(json.dumps(out), flush=True)
 
 

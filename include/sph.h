@@ -65,6 +65,18 @@ int sph_abi_version(void);
  * the next sph_* call on the thread. */
 const char* sph_last_error(void);
 
+/* Debug aid (no counterpart in the paper): with debug synchronisation on,
+ * every kernel launch region of every call is followed by a synchronisation
+ * of the call's stream and an error check, so a kernel that fails at run
+ * time makes the call that launched it return SPH_E_DEVICE, with the
+ * region's name in the message, instead of surfacing at some later
+ * synchronisation.  Streams being captured into a graph are not
+ * synchronised.  It is off unless the environment variable SPH_DEBUG_SYNC
+ * is set to a value other than "0" when the library is first used.
+ * enable: 1 on, 0 off, negative to only query.  Returns the previous state
+ * (0 or 1).  Process-wide; calls already running are unaffected. */
+int sph_debug_sync(int enable);
+
 /*
  * Vocabulary subset plan: the language-restricted subset V_l of Section 5.4
  * (the endpoint names it by a subset identifier; Section 6.2 precomputes the
@@ -327,7 +339,9 @@ int sph_gcm_open_segments(sph_gcm_key key, const sph_gcm_segment* segments, int 
  * per kernel it launches: start and stop HIP events are attached to the
  * kernel dispatches themselves (hipExtLaunchKernelGGL), so a duration is
  * the kernel's execution on the launch stream as it ran in the caller's
- * workload, with no launch gap included.  Tracing is process-wide.
+ * workload, with no launch gap included.  Tracing is process-wide: records
+ * from calls on every thread go to the one trace, in the order their
+ * launches took a slot (thread-safe).
  */
 #define SPH_TRACE_NAME_LEN 32
 typedef struct {

@@ -18,6 +18,7 @@ c_vp = ctypes.c_void_p
 SIGNATURES = {
     "sph_abi_version": (ctypes.c_int, []),
     "sph_last_error": (ctypes.c_char_p, []),
+    "sph_debug_sync": (ctypes.c_int, [ctypes.c_int]),
     "sph_subset_create": (ctypes.c_int, [c_vp, c_i64, c_i64, c_vp, ctypes.POINTER(c_vp)]),
     "sph_subset_create_full": (ctypes.c_int, [c_i64, c_vp, ctypes.POINTER(c_vp)]),
     "sph_subset_size": (ctypes.c_int, [c_vp, ctypes.POINTER(c_i64), ctypes.POINTER(c_i64)]),

@@ -433,6 +433,13 @@ def fuse_verify_hq(q: torch.Tensor, scale: torch.Tensor, hq: torch.Tensor, h_sca
     return tokens, accept, fused
 
 
+def debug_sync(enable: Optional[bool] = None) -> bool:
+    """Switch the library's debug synchronisation (a stream synchronisation
+    and error check after every kernel launch region) on or off; None only
+    queries.  Returns the previous state."""
+    return bool(_lib.load().sph_debug_sync(-1 if enable is None else int(bool(enable))))
+
+
 def trace_start(capacity: int) -> None:
     """Record HIP events around the next `capacity` kernel launches."""
     check(_lib.load().sph_trace_start(int(capacity)))

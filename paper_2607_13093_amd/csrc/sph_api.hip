@@ -8,6 +8,8 @@
 #include <mutex>
 #include <string>
 #include <algorithm>
+#include <atomic>
+#include <cstdlib>
 #include <vector>
 
 #include "sph.h"
@@ -45,8 +47,35 @@ int ok() {
   return SPH_OK;
 }
 
+// Set by a failing debug synchronisation (see traced) to name the kernel the
+// error surfaced after; consumed by the next hip_fail on this thread.
+thread_local std::string t_sync_note;
+
 int hip_fail(hipError_t e, const char* what) {
+  if (!t_sync_note.empty()) {
+    const std::string note = t_sync_note;
+    t_sync_note.clear();
+    return fail(SPH_E_DEVICE, "%s (%s): %s", what, note.c_str(), hipGetErrorString(e));
+  }
   return fail(SPH_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Debug mode: every launch region is followed by a synchronisation of its
+// stream and an error check, so a failing kernel is reported by the call
+// that launched it.  Off by default; SPH_DEBUG_SYNC=1 in the environment
+// turns it on at the first call, sph_debug_sync() at any time.
+std::atomic<int> g_debug_sync{-1};
+
+bool debug_sync_on() {
+  int v = g_debug_sync.load(std::memory_order_acquire);
+  if (v < 0) {
+    const char* env = std::getenv("SPH_DEBUG_SYNC");
+    const int want = (env && env[0] && env[0] != '0') ? 1 : 0;
+    int expected = -1;
+    g_debug_sync.compare_exchange_strong(expected, want, std::memory_order_acq_rel);
+    v = g_debug_sync.load(std::memory_order_acquire);
+  }
+  return v > 0;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -69,10 +98,13 @@ struct TraceSlot {
   hipEvent_t start, stop;
   bool used;
 };
+// The trace is process-wide: g_trace and g_trace_used are guarded by
+// g_trace_mu; g_tracing is read without the lock (acquire) on every launch
+// and written under it (release), so an untraced launch costs one load.
 std::mutex g_trace_mu;
 std::vector<TraceSlot> g_trace;
 size_t g_trace_used = 0;
-bool g_tracing = false;
+std::atomic<bool> g_tracing{false};
 
 void trace_free_locked() {
   for (auto& t : g_trace) {
@@ -81,19 +113,20 @@ void trace_free_locked() {
   }
   g_trace.clear();
   g_trace_used = 0;
-  g_tracing = false;
+  g_tracing.store(false, std::memory_order_release);
 }
 
 // Launch `body` (returning hipError_t); while tracing, its kernels record the
-// slot's events on their dispatches (see launch_kernel).
+// slot's events on their dispatches (see launch_kernel).  In debug mode the
+// stream is synchronised afterwards (unless it is being captured into a
+// graph) and an execution error is returned as the region's error.
 template <class F>
 hipError_t traced(const char* name, hipStream_t s, F&& body) {
-  (void)s;
   long slot = -1;
   sph::TraceEvents ev{nullptr, nullptr, false};
-  if (g_tracing) {
+  if (g_tracing.load(std::memory_order_acquire)) {
     std::lock_guard<std::mutex> lk(g_trace_mu);
-    if (g_tracing && g_trace_used < g_trace.size()) {
+    if (g_tracing.load(std::memory_order_relaxed) && g_trace_used < g_trace.size()) {
       slot = (long)g_trace_used++;
       g_trace[(size_t)slot].name = name;
       g_trace[(size_t)slot].used = false;
@@ -102,11 +135,22 @@ hipError_t traced(const char* name, hipStream_t s, F&& body) {
     }
   }
   if (slot >= 0) sph::t_trace_events = &ev;
-  const hipError_t e = body();
+  hipError_t e = body();
   sph::t_trace_events = nullptr;
   if (slot >= 0) {
     std::lock_guard<std::mutex> lk(g_trace_mu);
     if ((size_t)slot < g_trace.size()) g_trace[(size_t)slot].used = ev.launched;
+  }
+  if (e == hipSuccess && debug_sync_on()) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    hipError_t ce = hipStreamIsCapturing(s, &cs);
+    if (ce == hipSuccess && cs == hipStreamCaptureStatusNone) {
+      e = hipStreamSynchronize(s);
+      if (e == hipSuccess) e = hipGetLastError();
+      if (e != hipSuccess) t_sync_note = std::string("debug sync after ") + name;
+    } else if (ce != hipSuccess) {
+      e = ce;
+    }
   }
   return e;
 }
@@ -164,6 +208,12 @@ size_t widen_ws(int64_t M, int64_t d_end) {
 extern "C" {
 
 int sph_abi_version(void) { return SPH_ABI_VERSION; }
+
+int sph_debug_sync(int enable) {
+  const int prev = debug_sync_on() ? 1 : 0;
+  if (enable >= 0) g_debug_sync.store(enable ? 1 : 0, std::memory_order_release);
+  return prev;
+}
 
 const char* sph_last_error(void) { return g_err.c_str(); }
 
@@ -756,13 +806,13 @@ int sph_trace_start(int capacity) {
     }
     g_trace.push_back(t);
   }
-  g_tracing = true;
+  g_tracing.store(true, std::memory_order_release);
   return ok();
 }
 
 int sph_trace_stop(sph_trace_record* out, int max_records, int* n_out) {
   std::lock_guard<std::mutex> lk(g_trace_mu);
-  g_tracing = false;
+  g_tracing.store(false, std::memory_order_release);
   const size_t used = g_trace_used;
   int rc = SPH_OK;
   int k = 0;  // regions that launched a kernel

@@ -15,6 +15,7 @@ from .workloads import (  # noqa: F401
     bf16_bits_to_f32,
     fp8_encode_rows,
     make_workload,
+    with_subset,
     make_drafts,
     plant_masked_supertoken,
     scale_rows_bf16,

@@ -35,6 +35,7 @@ __all__ = [
     "Workload",
     "CONFIGS",
     "make_workload",
+    "with_subset",
     "make_drafts",
     "f32_to_bf16_bits",
     "bf16_bits_to_f32",
@@ -218,6 +219,25 @@ def make_workload(cfg: Config, h_rows: Optional[int] = None) -> Workload:
     return Workload(cfg=cfg, h_bits=h_bits, w_end_bits=w_end, w_cloud_bits=w_cloud,
                     w_cloud_codes=codes, w_cloud_scale=scale, bias=bias,
                     subset=subset, full_vocab=(cfg.subset_kind == "full"), rngs=r)
+
+
+def with_subset(wl: Workload, cfg: Config) -> Workload:
+    """The workload of ``cfg`` built from the hidden states and weights already
+    drawn for ``wl``: valid when both configurations draw them from the same
+    seed streams with the same shapes (the same seed index, d, d_end,
+    vocabulary, weight type, rows and bias) and differ only in the subset,
+    which comes from its own stream.  Equal to ``make_workload(cfg)``."""
+    a, b = wl.cfg, cfg
+    same = (a.seed_index, a.d, a.d_end, a.vocab, a.wtype, a.M, a.with_bias) == \
+           (b.seed_index, b.d, b.d_end, b.vocab, b.wtype, b.M, b.with_bias)
+    if not same or wl.h_bits.shape[0] != cfg.M:
+        raise ValueError("with_subset: the two configurations draw different inputs")
+    r = _streams(cfg.seed_index)
+    subset = _draw_subset(cfg, r["subset"])
+    return Workload(cfg=cfg, h_bits=wl.h_bits, w_end_bits=wl.w_end_bits,
+                    w_cloud_bits=wl.w_cloud_bits, w_cloud_codes=wl.w_cloud_codes,
+                    w_cloud_scale=wl.w_cloud_scale, bias=wl.bias, subset=subset,
+                    full_vocab=(cfg.subset_kind == "full"), rngs=r)
 
 
 def make_drafts(cfg: Config, ref_tokens: np.ndarray, subset: np.ndarray,

@@ -40,6 +40,17 @@ def test_abi_version(lib):
     assert lib.sph_last_error() == b""
 
 
+def test_debug_sync_switch(lib):
+    # a query leaves the state alone; each switch returns the previous state
+    start = lib.sph_debug_sync(-1)
+    assert start in (0, 1)
+    assert lib.sph_debug_sync(1) == start
+    assert lib.sph_debug_sync(-1) == 1
+    assert lib.sph_debug_sync(0) == 1
+    assert lib.sph_debug_sync(-1) == 0
+    lib.sph_debug_sync(start)
+
+
 def _create(lib, ids, vocab):
     arr = np.ascontiguousarray(np.asarray(ids, dtype=np.int32))
     out = ctypes.c_void_p(123)
