@@ -552,16 +552,14 @@ def main():
         # every other workload, fewer steps; the dense subset reuses the dense
         # workload's hidden states and weights (same seed streams)
         configs = {}
-        base = wl
         for name in OTHER_WORKLOADS:
             if name == args.workload:
                 continue
             c2 = CONFIGS[name]
             progress(f"{name}: drawing the synthetic inputs")
             try:
-                w2 = with_subset(base, c2)
+                w2 = with_subset(wl, c2)
             except ValueError:
-                base = None
                 w2 = make_workload(c2)
             r2 = run_workload(w2, args, min(args.steps, 50), min(args.warmup, 5))
             k2 = r2["roof"]["kernel"]
