@@ -215,6 +215,30 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
                           int64_t block, void* q_out, float* scale_out, float* z_out,
                           void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the cloud
+ * call of sph_cloud_partial_fmt without a workspace argument.  Its
+ * workspace is a static device array of SPH_NOALLOC_SCRATCH_BYTES bytes
+ * that every GPU the library runs on holds until the process ends; the
+ * call allocates nothing, frees nothing and calls no allocating routine.
+ * Inputs, outputs, results and errors are those of sph_cloud_partial_fmt,
+ * plus SPH_E_WORKSPACE (nothing enqueued) when
+ * sph_cloud_partial_workspace(M, subset) exceeds the scratch size, e.g.
+ * 5 rows x 49152 ids need about 1 MB, 20 rows x 190000 ids about 15 MB.
+ * The scratch keeps the last call's contents and no kernel depends on
+ * its initial contents.  Every call on one GPU shares that GPU's scratch:
+ * calls that overlap on one GPU (on different streams, or from several
+ * threads without ordering) race and give undefined results; calls on one
+ * stream are ordered and safe.
+ */
+#define SPH_NOALLOC_SCRATCH_BYTES (16u << 20)
+int sph_cloud_partial_noalloc(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                              const void* w_cloud, int64_t ldw, int wtype,
+                              const float* w_row_scale, const float* bias, sph_subset subset,
+                              float clip_c, int bits, int64_t block, void* q_out,
+                              float* scale_out, float* z_out, void* stream);
+
 /* sph_fuse_verify reading a payload in format (bits, block):
  *   f[m, j] = fmaf(code[m, j], scale[m, k(j)], z_end[m, j]),  k(j) = j / block
  * (k = 0 for block 0).  (8, 0) is sph_fuse_verify.  Same workspace. */

@@ -12,6 +12,7 @@ from .api import (  # noqa: F401
     Subset,
     cloud_partial,
     cloud_partial_workspace,
+    cloud_partial_noalloc,
     debug_sync,
     fuse_verify,
     fuse_verify_workspace,

@@ -49,6 +49,13 @@ SIGNATURES = {
         ctypes.c_int, c_i64,                # bits, block
         c_vp, c_vp, c_vp,                   # q_out, scale_out, z_out
         c_vp, ctypes.c_size_t, c_vp]),      # workspace, ws_bytes, stream
+    "sph_cloud_partial_noalloc": (ctypes.c_int, [
+        c_vp, c_i64, c_i64, c_i64,          # h_cloud, ldh, M, d_cloud
+        c_vp, c_i64, ctypes.c_int, c_vp,    # w_cloud, ldw, wtype, w_row_scale
+        c_vp, c_vp, ctypes.c_float,         # bias, subset, clip_c
+        ctypes.c_int, c_i64,                # bits, block
+        c_vp, c_vp, c_vp,                   # q_out, scale_out, z_out
+        c_vp]),                             # stream
     "sph_fuse_verify_fmt": (ctypes.c_int, [
         c_vp, c_vp, ctypes.c_int, c_i64,    # q, scale, bits, block
         c_vp, c_i64, c_i64,                 # h_end, ldh, d_end

@@ -329,6 +329,36 @@ def cloud_partial(h_cloud: torch.Tensor, w_cloud: torch.Tensor, subset: Subset, 
     return q, scale, z
 
 
+NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def cloud_partial_noalloc(h_cloud: torch.Tensor, w_cloud: torch.Tensor, subset: Subset,
+                          clip_c: float, out, w_row_scale: Optional[torch.Tensor] = None,
+                          bias: Optional[torch.Tensor] = None, bits: int = 8, block: int = 0):
+    """cloud_partial without a workspace: the library's static device scratch
+    (NOALLOC_SCRATCH_BYTES per GPU) stands in for it.  `out` = (q, scale, z or
+    None) must be given; nothing is allocated.  Calls that overlap on one GPU
+    race (they share the scratch)."""
+    lib = _lib.load()
+    _require_gpu("h_cloud", h_cloud)
+    _require_gpu("w_cloud", w_cloud)
+    h_cloud = _as_bits16(h_cloud)
+    if w_cloud.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        wtype = _lib.SPH_W_BF16
+    elif w_cloud.dtype in (torch.float8_e4m3fn, torch.uint8):
+        wtype = _lib.SPH_W_FP8_E4M3
+    else:
+        raise TypeError(f"unsupported weight dtype {w_cloud.dtype}")
+    M, d_cloud = h_cloud.shape
+    q, scale, z = out
+    check(lib.sph_cloud_partial_noalloc(
+        h_cloud.data_ptr(), h_cloud.stride(0) if M > 0 else d_cloud, M, d_cloud,
+        w_cloud.data_ptr(), w_cloud.stride(0), wtype, _ptr(w_row_scale),
+        _ptr(bias), subset.handle, float(clip_c), int(bits), int(block),
+        q.data_ptr(), scale.data_ptr(), _ptr(z), _stream_handle(h_cloud.device)))
+    return q, scale, z
+
+
 def fuse_verify(q: torch.Tensor, scale: torch.Tensor, h_end: Optional[torch.Tensor],
                 w_end: Optional[torch.Tensor], subset: Subset, n_sessions: int,
                 rows_per_session: int, drafts: Optional[torch.Tensor], mode: int = GREEDY,

@@ -203,6 +203,39 @@ size_t widen_ws(int64_t M, int64_t d_end) {
   return align256((size_t)M * (size_t)((d_end + 7) / 8 * 8) * 2);
 }
 
+// ---- allocation-free cloud call -------------------------------------------
+// A file-scope device array stands in for the caller's workspace.  Each GPU
+// holds its own copy at its own address; the host never passes `scratch`
+// itself to a kernel (its host-side name is not a device address) but the
+// address hipGetSymbolAddress returns, looked up once per device with that
+// device current and kept in g_scratch_addr.
+constexpr size_t kScratchBytes = size_t(SPH_NOALLOC_SCRATCH_BYTES);
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+// Device address of this device's scratch (the current device), or an error.
+int scratch_address(const char* fn, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SPH_E_UNSUPPORTED, "%s: device %d beyond the %d the library tracks", fn, dev,
+                kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!ptr) return fail(SPH_E_DEVICE, "%s: no device address for the scratch array", fn);
+    g_scratch_addr[dev] = ptr;
+  }
+  *out = g_scratch_addr[dev];
+  return SPH_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -456,6 +489,28 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
   });
   if (e != hipSuccess) return hip_fail(e, "quantiser launch");
   return ok();
+}
+
+int sph_cloud_partial_noalloc(const void* h_cloud, int64_t ldh, int64_t M, int64_t d_cloud,
+                              const void* w_cloud, int64_t ldw, int wtype,
+                              const float* w_row_scale, const float* bias, sph_subset subset,
+                              float clip_c, int bits, int64_t block, void* q_out,
+                              float* scale_out, float* z_out, void* stream) {
+  const char* fn = "sph_cloud_partial_noalloc";
+  if (!subset) return fail(SPH_E_INVALID_ARG, "%s: subset is NULL", fn);
+  if (M < 0) return fail(SPH_E_INVALID_ARG, "%s: M=%lld out of range", fn, (long long)M);
+  const size_t need = cloud_ws(M, subset->n);
+  if (need > kScratchBytes)
+    return fail(SPH_E_WORKSPACE,
+                "%s: %lld rows x %lld ids need %zu bytes of scratch; the static scratch holds "
+                "%zu bytes (use sph_cloud_partial_fmt with a workspace)",
+                fn, (long long)M, (long long)subset->n, need, kScratchBytes);
+  void* ws = nullptr;
+  const int rc = scratch_address(fn, &ws);
+  if (rc != SPH_OK) return rc;
+  return sph_cloud_partial_fmt(h_cloud, ldh, M, d_cloud, w_cloud, ldw, wtype, w_row_scale, bias,
+                               subset, clip_c, bits, block, q_out, scale_out, z_out, ws,
+                               kScratchBytes, stream);
 }
 
 int sph_fuse_verify(const int8_t* q, const float* scale, const void* h_end, int64_t ldh,
