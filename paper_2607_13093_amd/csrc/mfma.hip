@@ -27,7 +27,10 @@
 // Epilogues: the cloud epilogue scales fp8 columns, adds the bias, writes
 // fp32 partial logits and the tile's row maxima of |clamp(z)|; the fuse
 // epilogue dequantises the payload (eq. 13), writes fused logits on request
-// and the tile's per-row (value, position) argmax key.
+// and the tile's per-row (value, position) argmax key.  The endpoint
+// projection with K a multiple of the K step (k_fuse_dma) computes the
+// transposed tile, so that a lane holds consecutive subset positions of one
+// row: four payload codes per LDS read and an argmax that stays in the lane.
 #include <atomic>
 #include <type_traits>
 
@@ -89,6 +92,13 @@ __device__ __forceinline__ uint32_t lane_xor_u32(uint32_t v) {
 }
 template <class T>
 __device__ __forceinline__ T vmax(T a, T b) { return a > b ? a : b; }
+
+// The 64-bit value of lane l ^ 32.
+__device__ __forceinline__ unsigned long long xor_lane_u64_32(unsigned long long v) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, 32, 64);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), 32, 64);
+  return ((unsigned long long)hi << 32) | lo;
+}
 
 // Values are float or 64-bit keys, moved as 32-bit words.
 template <class T, int O>
@@ -221,13 +231,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
   V red[P];
 #pragma unroll
   for (int t = FM * 16; t < P; ++t) red[t] = V(0);
-  // The fuse epilogue of a tile that lies inside the output and holds 8-bit
-  // codes (the common case) runs a copy of the loop without the bounds and
-  // code-width checks.  Only the 256-row tiles of 8 waves have one: on
-  // 320-row tiles (80 row keys per lane) a second copy spilled, and the
-  // 4-wave kernels spill more with it.
-  auto fill = [&](auto fast) {
-    constexpr bool kFast = decltype(fast)::value;
+  auto fill = [&]() {
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -243,7 +247,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
         for (int j = 0; j < FN; ++j) {
           const int lcol = wn * TN + j * 32 + (lane & 31);
           const int col = n0 + lcol;
-          if (kFast || (row < M && col < n)) {
+          if (row < M && col < n) {
             const float dot = acc[i][j][r];
             if constexpr (kCloud) {
               const float zv = cloud_value<WT>(dot, a, s_ids[lcol]);
@@ -251,7 +255,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
               best = fmaxf(best, fabsf(fminf(fmaxf(zv, -a.clip), a.clip)));
             } else {
               int code;
-              if (kFast || a.qbits == 8) {
+              if (a.qbits == 8) {
                 code = s_q[lrow * BN + lcol];
               } else {
                 const int byte = (uint8_t)s_q[lrow * (BN / 2) + (lcol >> 1)];
@@ -272,12 +276,7 @@ __device__ __forceinline__ void tile_epilogue(f32x16_t (&acc)[FM][FN], const Mfm
       }
     }
   };
-  if constexpr (kCloud || BM != 256 || WM * WN != 8) {
-    fill(std::false_type{});
-  } else {
-    if (m0 + BM <= M && n0 + BN <= n && a.qbits == 8) fill(std::true_type{});
-    else fill(std::false_type{});
-  }
+  fill();
   half_wave_max_transpose<P>(red, lane);
   constexpr int PER = P / 32;
 #pragma unroll
@@ -816,6 +815,276 @@ void k_mfma_dma8(const MfmaArgs a) {
 #endif
 }
 
+// Endpoint projection with its fuse epilogue (eqs. 11, 13-14), K a multiple
+// of the K step.  The block computes the transposed tile C^T[n][m] =
+// W[S_n] . h[m]: the weight rows are the MFMA's A operand and the rows of h
+// its B operand, so accumulator r of lane l in fragment (i, j) is subset
+// position i*32 + 8*(r/4) + 4*(l/32) + r%4 of row j*32 + l%32 (in the wave's
+// tile): each lane holds four consecutive positions of one row per register
+// group.  Operands are staged exactly as in k_mfma_dma.  A BM x 256 tile
+// runs WNN x WMM waves (WNN along the positions, WMM along the rows).
+//
+// Payload: the tile's codes (BM rows of 256 * qbits / 8 bytes) are staged
+// in LDS as 16-byte chunks, chunk k of row r at position k ^ (r mod chunks
+// per row), so one 32-bit read gives a lane its four 8-bit codes (a 16-bit
+// read its four 4-bit codes) and the 32 rows a read touches spread over
+// the banks.  With 8-bit codes on 16-byte aligned rows the tile is copied
+// global-to-LDS during the last K step into the operand buffers that step
+// does not read (rows [0, BM/2) into the idle A buffer, the rest into the
+// idle B buffer), where it lands while the last MFMAs run; otherwise it is
+// loaded after the main loop.
+//
+// Selection: f = fma(code, s, dot * hs) in ascending position order within
+// the lane keeps the lane's first maximum; the two lanes holding a row (l,
+// l ^ 32) keep the larger orderable key (value, then lowest position), and
+// LDS atomics combine the WNN waves sharing the row.  Against the
+// row-major epilogue (one LDS byte read per code and a 32-lane butterfly of
+// 64-bit keys) this ran dense_full's endpoint projection in 358 us instead
+// of 505, dense_sub in 85 instead of 114 and batched in 29 instead of 47,
+// with identical keys.
+template <int BM, int WNN, int WMM>
+constexpr size_t fuse_dma_lds_bytes() {
+  return (size_t)2 * (BM + kMfmaBN) * kBK * 2 + (size_t)kMfmaBN * 4 + (size_t)2 * BM * 4 +
+         (size_t)BM * 8;
+}
+
+template <int BM, int WNN, int WMM>
+__global__ __launch_bounds__(64 * WNN * WMM)
+__attribute__((amdgpu_waves_per_eu(WNN * WMM / 4, WNN * WMM / 4)))
+void k_fuse_dma(const MfmaArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int BN = kMfmaBN, NT = 64 * WNN * WMM;
+  constexpr int FI = BN / WNN / 32, FJ = BM / WMM / 32;  // position / row fragments per wave
+  static_assert(FI * WNN * 32 == BN && FJ * WMM * 32 == BM, "wave grid");
+  constexpr int IW = 4;  // waves issuing the operand copies (one per SIMD)
+  constexpr int A_INS = BM / 8 / IW, B_INS = BN / 8 / IW;
+  static_assert(A_INS * 8 * IW == BM && B_INS * 8 * IW == BN, "copy instructions");
+  constexpr int STAGE_B = (BM + BN) * kBK * 2;  // bytes of one operand stage
+  constexpr bool kLastStep = BM * BN <= STAGE_B && BM <= BN;  // 8-bit tile fits in one stage
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);                 // [2][BM][64]
+  uint16_t* Bs = As + 2 * BM * kBK;                                  // [2][BN][64]
+  int32_t* s_ids = reinterpret_cast<int32_t*>(smem + 2 * STAGE_B);
+  float* s_sc = reinterpret_cast<float*>(s_ids + BN);               // [2][BM]: scale, dot factor
+  unsigned long long* s_rkey = reinterpret_cast<unsigned long long*>(s_sc + 2 * BM);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int iw = wave < IW ? wave : 0;
+  const int wn = wave % WNN, wm = wave / WNN;
+  int mt, nt;
+  tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int M = a.M, K = a.K, n = a.n;
+  const int last_id = a.ids[min(n, n0 + BN) - 1];
+  for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  // a tile lies in one block of positions (blocks are multiples of BN)
+  const int kb = a.qshift < 0 ? 0 : (n0 >> a.qshift);
+  for (int i = tid; i < BM; i += NT) {
+    s_rkey[i] = 0ull;
+    s_sc[i] = m0 + i < M ? a.qscale[(int64_t)(m0 + i) * a.qnb + kb] : 0.0f;
+    s_sc[BM + i] = (a.hscale && m0 + i < M) ? a.hscale[m0 + i] : 1.0f;
+  }
+  __syncthreads();
+  const int lr = lane >> 3;
+  const uint8_t* pa[A_INS];
+  const uint8_t* pb[B_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    const int r = (iw * A_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int r = (iw * B_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+  }
+  auto issue = [&](int k0, int stage) {
+    if (wave >= IW) return;
+    uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
+    uint8_t* bs = reinterpret_cast<uint8_t*>(Bs + stage * BN * kBK);
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
+                                       (lds_void_t*)(as + (iw * A_INS + i) * 1024), 16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds(pb[i] + (int64_t)k0 * 2,
+                                       (lds_void_t*)(bs + (iw * B_INS + i) * 1024), 16, 0, 0);
+  };
+  const int qb = a.qbits;
+  const int TB = BN * qb / 8;  // code bytes of a tile row
+  const int CPR = TB / 16;     // 16-byte chunks of a tile row
+  const int64_t c0 = (int64_t)n0 * qb / 8;
+  const int64_t rowbytes = ((int64_t)n * qb + 7) / 8;
+  const bool vec_q = (a.qstride & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
+  const bool dma_q = qb == 8 && vec_q;
+  // payload row r: staged in the last K step, rows [0, BM/2) in the idle
+  // stage's A buffer and [BM/2, BM) in its B buffer; staged after the
+  // loop, consecutive rows from the start of LDS
+  auto prow = [&](bool in_stage, int st, int r) -> uint8_t* {
+    if (!in_stage) return smem + r * TB;
+    return r < BM / 2 ? reinterpret_cast<uint8_t*>(As + st * BM * kBK) + r * TB
+                      : reinterpret_cast<uint8_t*>(Bs + st * BN * kBK) + (r - BM / 2) * TB;
+  };
+  // global-to-LDS copies of an 8-bit payload tile: a wave instruction fills
+  // 4 rows (1 KB, contiguous in either placement); rows past M read row
+  // M-1 and chunks past the row's end read the tile's first chunk (their
+  // positions are never selected)
+  auto stage_payload_dma = [&](bool in_stage, int st) {
+    for (int t = wave; t < BM / 4; t += WNN * WMM) {
+      const int r = t * 4 + (lane >> 4);
+      const int k = (lane & 15) ^ (r & 15);
+      const int64_t col = c0 + k * 16 < rowbytes ? c0 + k * 16 : c0;
+      __builtin_amdgcn_global_load_lds(a.q + (int64_t)min(m0 + r, M - 1) * a.qstride + col,
+                                       (lds_void_t*)prow(in_stage, st, t * 4), 16, 0, 0);
+    }
+  };
+
+  f32x16_t acc[FI][FJ];
+#pragma unroll
+  for (int i = 0; i < FI; ++i)
+#pragma unroll
+    for (int j = 0; j < FJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  if (K > 0) {
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  int stage = 0;
+  bool staged = false;
+  for (int k0 = 0; k0 < K; k0 += kBK) {
+    if (k0 + kBK < K) {
+      issue(k0 + kBK, stage ^ 1);
+    } else if (kLastStep && dma_q) {
+      // the last step reads one stage; the payload tile goes to the other
+      stage_payload_dma(true, stage ^ 1);
+      staged = true;
+    }
+    const uint16_t* as = As + stage * BM * kBK;
+    const uint16_t* bs = Bs + stage * BN * kBK;
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      bf16x8_t hf[FJ], wf[FI];
+      const int c = kk * 2 + (lane >> 5);
+#pragma unroll
+      for (int j = 0; j < FJ; ++j) {
+        const int row = wm * (BM / WMM) + j * 32 + (lane & 31);
+        hf[j] = *reinterpret_cast<const bf16x8_t*>(as + row * kBK + ((c ^ swz8(row)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < FI; ++i) {
+        const int row = wn * (BN / WNN) + i * 32 + (lane & 31);
+        wf[i] = *reinterpret_cast<const bf16x8_t*>(bs + row * kBK + ((c ^ swz8(row)) << 3));
+      }
+#pragma unroll
+      for (int i = 0; i < FI; ++i)
+#pragma unroll
+        for (int j = 0; j < FJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[i], hf[j], acc[i][j], 0, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's copies (operands or payload) have landed
+    __syncthreads();
+    stage ^= 1;
+  }
+  // after the last step's toggle, `stage` names the buffer that step did not read
+  const int pst = stage;
+  if (!staged) {
+    if (dma_q) {
+      stage_payload_dma(false, 0);
+      __builtin_amdgcn_s_waitcnt(0);
+    } else if (vec_q) {
+      for (int c = tid; c < BM * CPR; c += NT) {
+        const int r = c / CPR, k = c % CPR;
+        const int64_t col = c0 + k * 16;
+        const u32x4_t v = (m0 + r < M && col < rowbytes)
+                              ? *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)(m0 + r) * a.qstride + col)
+                              : u32x4_t{0u, 0u, 0u, 0u};
+        *reinterpret_cast<u32x4_t*>(prow(false, 0, r) + ((k ^ (r & (CPR - 1))) << 4)) = v;
+      }
+    } else {
+      for (int c = tid; c < BM * TB; c += NT) {
+        const int r = c / TB, byte = c % TB, k = byte >> 4;
+        const int64_t col = c0 + byte;
+        prow(false, 0, r)[((k ^ (r & (CPR - 1))) << 4) | (byte & 15)] =
+            (m0 + r < M && col < rowbytes) ? a.q[(int64_t)(m0 + r) * a.qstride + col] : (uint8_t)0;
+      }
+    }
+    __syncthreads();
+  }
+  // fused values in ascending position order: the lane's first maximum,
+  // the larger key of the row's two lanes, then LDS atomics over the waves
+  auto run = [&](auto edge) {
+    constexpr bool kEdge = decltype(edge)::value;  // bounds checks and the fused output
+#pragma unroll
+    for (int j = 0; j < FJ; ++j) {
+      const int ml = wm * (BM / WMM) + j * 32 + (lane & 31);
+      const float sc = s_sc[ml], hsc = s_sc[BM + ml];
+      float bv = -__builtin_inff();
+      int bn = -1;
+      const uint8_t* qrow = prow(staged, pst, ml);
+#pragma unroll
+      for (int i = 0; i < FI; ++i) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int nl = wn * (BN / WNN) + i * 32 + 8 * g + 4 * (lane >> 5);
+          uint32_t c4;  // the four codes as sign-extended bytes
+          if (qb == 8) {
+            c4 = *reinterpret_cast<const uint32_t*>(qrow + ((((nl >> 4) ^ (ml & 15)) << 4) | (nl & 15)));
+          } else {
+            const int byte = nl >> 1;
+            const uint32_t h =
+                *reinterpret_cast<const uint16_t*>(qrow + ((((byte >> 4) ^ (ml & 7)) << 4) | (byte & 15)));
+            c4 = (h & 0xFu) | ((h & 0xF0u) << 4) | ((h & 0xF00u) << 8) | ((h & 0xF000u) << 12);
+            c4 |= (c4 & 0x08080808u) * 0x1Eu;  // a nibble's sign bit fills bits 4..7 of its byte
+          }
+          float f4[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int code = (int)(int8_t)(c4 >> (8 * e));
+            f4[e] = __builtin_fmaf((float)code, sc, acc[i][j][4 * g + e] * hsc);
+            const bool in = !kEdge || n0 + nl + e < n;
+            if (in && f4[e] > bv) {
+              bv = f4[e];
+              bn = nl + e;
+            }
+          }
+          if constexpr (kEdge) {
+            // the fused row on request: the lane's four positions in one
+            // 16-byte store where they are inside and aligned (cached stores,
+            // so that the four instructions covering a row's 32 positions
+            // meet in L2)
+            const int m = m0 + ml;
+            if (a.f && m < M) {
+              float* dst = a.f + (int64_t)m * n + n0 + nl;
+              if (n0 + nl + 4 <= n && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+                *reinterpret_cast<float4*>(dst) = make_float4(f4[0], f4[1], f4[2], f4[3]);
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  if (n0 + nl + e < n) dst[e] = f4[e];
+              }
+            }
+          }
+        }
+      }
+      unsigned long long key = bn >= 0 ? argmax_key_m(bv, n0 + bn) : 0ull;
+      const unsigned long long other = xor_lane_u64_32(key);
+      key = key > other ? key : other;
+      if (lane < 32) atomicMax(&s_rkey[ml], key);
+    }
+  };
+  if (a.f || m0 + BM > M || n0 + BN > n) run(std::true_type{});
+  else run(std::false_type{});
+  __syncthreads();
+  for (int i = tid; i < BM; i += NT)
+    if (m0 + i < M) a.best_part[(int64_t)(m0 + i) * kMaxBlocks + nt] = s_rkey[i];
+#endif
+}
+
 template <int BM, int BN>
 constexpr size_t mfma_lds_bytes() {
   return (size_t)2 * (BM + BN) * kLDK * 2 + (size_t)BN * 4 + (size_t)(BM + 1) * 4 + 8 +
@@ -834,21 +1103,18 @@ constexpr size_t mfma_dma8_lds_bytes() {
          (size_t)BM * 8;
 }
 
-// Waves of a row tile.  256- and 320-row tiles use 8 waves, two per SIMD, so
-// one wave's MFMAs run while the other waits at a barrier or on LDS: 2 x 4
-// (wave tiles 128 x 64 / 160 x 64) for the cloud projection, whose long K
-// loop ran 6% faster so than with 4 x 2; 4 x 2 (wave tile 64 x 128) for the
-// endpoint projection, whose short K loop leaves its epilogue dominant: 32
-// rows per lane instead of 64 halve the argmax butterfly.  128-row tiles use
-// 2 x 2.  On the dense 2048-row shapes 8 waves ran the cloud projection 9%
-// and the endpoint projection 28% faster than 4 (wave tile 128 x 128).
-// 32-row tiles (9 to 32 rows, direct-to-LDS only) use 1 x 4 waves of 32 x 64.
+// Waves of a cloud row tile (the direct-to-LDS kernels).  256- and 320-row
+// tiles use 8 waves, two per SIMD, so one wave's MFMAs run while the other
+// waits at a barrier or on LDS: 2 x 4 (wave tiles 128 x 64 / 160 x 64),
+// whose long K loop ran 6% faster so than with 4 x 2; on the dense 2048-row
+// shape 8 waves ran 9% faster than 4 (wave tile 128 x 128).  128-row tiles
+// use 2 x 2, 32-row tiles (9 to 32 rows) 1 x 4 waves of 32 x 64.  (The
+// endpoint projection's transposed tiles choose their own grid.)
 template <int BM, int EPI>
 struct WaveGrid {
   static constexpr bool kEight = BM >= 256;
-  static constexpr bool kTall = kEight && !(BM == 256 && EPI == kEpiFuse);
-  static constexpr int WM = BM == 32 ? 1 : kEight ? (kTall ? 2 : 4) : 2;
-  static constexpr int WN = BM == 32 ? 4 : kEight ? (kTall ? 4 : 2) : 2;
+  static constexpr int WM = BM == 32 ? 1 : kEight ? 2 : 2;
+  static constexpr int WN = BM == 32 ? 4 : kEight ? 4 : 2;
 };
 
 // The dynamic-LDS limit of a kernel is raised once per device (a host call,
@@ -872,7 +1138,20 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
   if (a.n_tiles > kMaxBlocks) return hipErrorInvalidValue;
-  if (a.K % kBK == 0) {
+  if constexpr (EPI == kEpiFuse) {
+    if (a.K % kBK == 0) {
+      // transposed tiles: waves along the positions x waves along the rows
+      constexpr int WNN = BM == 256 ? 2 : BM == 320 ? 4 : BM == 128 ? 2 : 4;
+      constexpr int WMM = BM == 256 ? 4 : BM == 320 ? 2 : BM == 128 ? 2 : 1;
+      auto kf = k_fuse_dma<BM, WNN, WMM>;
+      constexpr size_t lds_f = fuse_dma_lds_bytes<BM, WNN, WMM>();
+      static std::atomic<uint64_t> lds_set_fuse{0};
+      hipError_t e = set_lds_limit_once(lds_set_fuse, reinterpret_cast<const void*>(kf), lds_f);
+      if (e != hipSuccess) return e;
+      launch_kernel(kf, dim3(a.m_tiles * a.n_tiles), dim3(64 * WNN * WMM), lds_f, s, a);
+      return hipGetLastError();
+    }
+  } else if (a.K % kBK == 0) {
     auto kd = WT == 0 ? k_mfma_dma<BM, BN, WM, WN, EPI> : k_mfma_dma8<BM, BN, WM, WN, EPI>;
     constexpr size_t lds_d = WT == 0 ? mfma_dma_lds_bytes<BM, BN>() : mfma_dma8_lds_bytes<BM, BN>();
     hipError_t e = set_lds_limit_once(lds_set_dma, reinterpret_cast<const void*>(kd), lds_d);
