@@ -66,11 +66,13 @@ def parse():
                         "endpoint projects from them (sph_hidden_quantize + sph_fuse_verify_hq)")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the oracle's CPU baseline run (0 to skip)")
-    p.add_argument("--sweep", choices=("d_end", "subset", "drafts", "all"), default=None,
+    p.add_argument("--sweep", choices=("d_end", "subset", "drafts", "all", "layout"), default=None,
                    help="paper-shape sweeps of the decode step instead of the benchmark line: "
                         "hidden 4096, vocabulary 150000, one session; d_end in "
                         "{48,96,128,256,512}, subset 30/40/100%% of V, drafts k in {1,2,4,5,6,8}; "
-                        "one JSON line per point")
+                        "'layout': the decode shape with its 49152 ids as one contiguous run, as "
+                        "the workload's run plus scattered ids, and all scattered; one JSON line "
+                        "per point")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run plain device copies of MIB MiB (to scale rocprofv3 "
                         "FETCH_SIZE / WRITE_SIZE counters), then exit")
@@ -481,12 +483,65 @@ def workload_text(cfg, n):
             f"{cfg.mode} clip={cfg.clip_c}")
 
 
+def sweep_layout(args):
+    """The decode step's cloud projection with the same number of subset ids
+    (49152 of 128256, d = 4096, d_end = 256, 5 rows) laid out as one
+    contiguous run, as the decode workload's 32768-id run plus 16384
+    scattered ids, and as 49152 scattered ids: whether a table of contiguous
+    runs could speed up the gathered weight stream."""
+    import numpy as np
+    import torch
+
+    import paper_2607_13093_amd as sph
+    from synth import CONFIGS, make_workload
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS["decode"]
+    wl = make_workload(cfg)
+    n, V, de = cfg.n_sub, cfg.vocab, cfg.d_end
+    rng = np.random.default_rng(2607)
+    layouts = {
+        "one_run": np.arange(20000, 20000 + n, dtype=np.int32),
+        "run_plus_scattered": wl.subset,
+        "scattered": np.sort(rng.choice(V, n, replace=False)).astype(np.int32),
+    }
+    h = torch.from_numpy(wl.h_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    wc = [torch.from_numpy(wl.w_cloud_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+          for _ in range(N_COPIES)]
+    M = cfg.M
+    q = torch.empty((M, n), dtype=torch.int8, device=dev)
+    sc = torch.empty((M,), dtype=torch.float32, device=dev)
+    for name, ids in layouts.items():
+        sub = sph.Subset(ids, vocab=V)
+        ws = torch.empty(sph.cloud_partial_workspace(M, sub), dtype=torch.uint8, device=dev)
+        for i in range(args.warmup):
+            sph.cloud_partial(h[:, de:], wc[i % N_COPIES], sub, cfg.clip_c, workspace=ws, out=(q, sc, None))
+        torch.cuda.synchronize()
+        cap = 4 * args.steps + 16
+        sph.trace_start(cap)
+        for i in range(args.steps):
+            sph.cloud_partial(h[:, de:], wc[i % N_COPIES], sub, cfg.clip_c, workspace=ws, out=(q, sc, None))
+        torch.cuda.synchronize()
+        us = [ms * 1e3 for k, ms in sph.trace_collect(cap) if k == "cloud_gemv"]
+        nbytes = algorithmic_bytes(cfg, n)
+        runs = int(1 + np.count_nonzero(np.diff(ids) != 1))
+        print(json.dumps({"sweep": "layout", "layout": name, "ids": n, "runs": runs,
+                          "cloud_gemv_us_mean": float(np.mean(us)),
+                          "cloud_gemv_us_median": float(np.median(us)),
+                          "hbm_frac": nbytes / (np.median(us) * 1e-6) / 1e9 / HBM_PEAK_GBS}), flush=True)
+        sub.close()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
               "multi-GPU path, and this job uses a single MI355X", file=sys.stderr)
         sys.exit(2)
+    if args.sweep == "layout":
+        sweep_layout(args)
+        return
     if args.sweep:
         sweep(args)
         return
