@@ -41,3 +41,20 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_bench_algorithmic_work_matches_the_hand_counts():
+    # bytes of one cloud launch: every gathered weight row once (d_cloud
+    # weights, 2 bytes bf16 / 1 byte e4m3), its 4-byte id, an fp32 row scale for
+    # e4m3 weights, and the M rows of h_cloud; flops 2 M |S| d_cloud.  Counted by
+    # hand for the decode, batched and sampling workloads.
+    sys.path.insert(0, ROOT)
+    import bench
+    from synth import CONFIGS
+    dec = CONFIGS["decode"]       # 49152 ids x (3840*2 + 4) + 5 x 3840 x 2
+    assert bench.algorithmic_bytes(dec, 49152) == 49152 * 7684 + 38400 == 377722368
+    bat = CONFIGS["batched"]      # 60000 x (3584*2 + 4) + 320 x 3584 x 2
+    assert bench.algorithmic_bytes(bat, 60000) == 430320000 + 2293760
+    smp = CONFIGS["sample_fp8"]   # 65536 x (4800 + 4 + 4) + 640 x 4800 x 2
+    assert bench.algorithmic_bytes(smp, 65536) == 65536 * 4808 + 6144000
+    assert bench.dtype_of(smp) != "bf16" and bench.dtype_of(dec) == "bf16"
