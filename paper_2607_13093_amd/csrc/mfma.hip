@@ -94,10 +94,15 @@ template <class T>
 __device__ __forceinline__ T vmax(T a, T b) { return a > b ? a : b; }
 
 // The 64-bit value of lane l ^ 32.
+// v of lane l ^ 32: a permlane32 swap trades lanes [32, 64) of its first
+// operand with lanes [0, 32) of its second, so with v in both a low lane
+// finds its partner's value in the second result, a high lane in the first
 __device__ __forceinline__ unsigned long long xor_lane_u64_32(unsigned long long v) {
-  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, 32, 64);
-  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), 32, 64);
-  return ((unsigned long long)hi << 32) | lo;
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const auto sl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+  const auto sh = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  const bool low = (threadIdx.x & 32) == 0;
+  return ((unsigned long long)(low ? sh[1] : sh[0]) << 32) | (low ? sl[1] : sl[0]);
 }
 
 // Values are float or 64-bit keys, moved as 32-bit words.
@@ -818,30 +823,33 @@ void k_mfma_dma8(const MfmaArgs a) {
 // Endpoint projection with its fuse epilogue (eqs. 11, 13-14), K a multiple
 // of the K step.  The block computes the transposed tile C^T[n][m] =
 // W[S_n] . h[m]: the weight rows are the MFMA's A operand and the rows of h
-// its B operand, so accumulator r of lane l in fragment (i, j) is subset
-// position i*32 + 8*(r/4) + 4*(l/32) + r%4 of row j*32 + l%32 (in the wave's
-// tile): each lane holds four consecutive positions of one row per register
-// group.  Operands are staged exactly as in k_mfma_dma.  A BM x 256 tile
-// runs WNN x WMM waves (WNN along the positions, WMM along the rows).
+// its B operand.  The weight rows of each 32-row group are staged in the
+// order that puts subset position 16*(l/32) + r of the group in accumulator
+// r of lane l: a lane holds 16 consecutive positions of row j*32 + l%32 (in
+// the wave's tile) per fragment.  Operands are otherwise staged exactly as
+// in k_mfma_dma.  A BM x 256 tile runs WNN x WMM waves (WNN along the
+// positions, WMM along the rows).
 //
 // Payload: the tile's codes (BM rows of 256 * qbits / 8 bytes) are staged
-// in LDS as 16-byte chunks, chunk k of row r at position k ^ (r mod chunks
-// per row), so one 32-bit read gives a lane its four 8-bit codes (a 16-bit
-// read its four 4-bit codes) and the 32 rows a read touches spread over
-// the banks.  With 8-bit codes on 16-byte aligned rows the tile is copied
-// global-to-LDS during the last K step into the operand buffers that step
-// does not read (rows [0, BM/2) into the idle A buffer, the rest into the
-// idle B buffer), where it lands while the last MFMAs run; otherwise it is
-// loaded after the main loop.
+// in LDS as 16-byte chunks, swizzled per row, so one 16-byte read gives a
+// lane its 16 8-bit codes (an 8-byte read its 16 4-bit codes) and the rows
+// a read touches spread over the banks.  With 8-bit codes on 16-byte
+// aligned rows the tile is copied global-to-LDS during the last K step into
+// the operand buffers that step does not read (rows [0, BM/2) into the idle
+// A buffer, the rest into the idle B buffer), where it lands while the last
+// MFMAs run; otherwise it is loaded after the main loop.
 //
-// Selection: f = fma(code, s, dot * hs) in ascending position order within
-// the lane keeps the lane's first maximum; the two lanes holding a row (l,
-// l ^ 32) keep the larger orderable key (value, then lowest position), and
-// LDS atomics combine the WNN waves sharing the row.  Against the
-// row-major epilogue (one LDS byte read per code and a 32-lane butterfly of
-// 64-bit keys) this ran dense_full's endpoint projection in 358 us instead
-// of 505, dense_sub in 85 instead of 114 and batched in 29 instead of 47,
-// with identical keys.
+// Selection: f = fma(code, s, dot * hs) (the product only with hidden-state
+// scales), the lane's largest f, then the lowest of the lane's positions
+// holding it; the two lanes holding a row (l, l ^ 32) keep the larger
+// orderable key (value, then lowest position), and LDS atomics combine the
+// WNN waves sharing the row.  Against the row-major epilogue (one LDS byte
+// read per code and a 32-lane butterfly of 64-bit keys) the first form of
+// this kernel (four positions per register group, a 32-bit code read and a
+// running compare per value) ran dense_full's endpoint projection in 358 us
+// instead of 505, dense_sub in 85 instead of 114 and batched in 29 instead
+// of 47; the 16-position layout then took dense_sub to 81 us and batched to
+// 27, with identical keys throughout.
 template <int BM, int WNN, int WMM>
 constexpr size_t fuse_dma_lds_bytes() {
   return (size_t)2 * (BM + kMfmaBN) * kBK * 2 + (size_t)kMfmaBN * 4 + (size_t)2 * BM * 4 +
@@ -897,7 +905,12 @@ void k_fuse_dma(const MfmaArgs a) {
   for (int i = 0; i < B_INS; ++i) {
     const int r = (iw * B_INS + i) * 8 + lr;
     const int lc = (lane & 7) ^ swz8(r);
-    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+    // weight row r of a 32-row group holds subset position pr: MFMA row
+    // 8g + 4h + e (g = register group, h = lane / 32, e = element) gets
+    // position 16h + 4g + e, so a lane's 16 accumulators cover 16
+    // consecutive positions
+    const int pr = (r & ~31) | (((r >> 2) & 1) << 4) | (((r >> 3) & 3) << 2) | (r & 3);
+    pb[i] = a.w + (int64_t)s_ids[pr] * a.ldw_bytes + lc * 16;
   }
   auto issue = [&](int k0, int stage) {
     if (wave >= IW) return;
@@ -919,6 +932,9 @@ void k_fuse_dma(const MfmaArgs a) {
   const int64_t rowbytes = ((int64_t)n * qb + 7) / 8;
   const bool vec_q = (a.qstride & 15) == 0 && (reinterpret_cast<uintptr_t>(a.q) & 15) == 0;
   const bool dma_q = qb == 8 && vec_q;
+  // chunk swizzle of payload row r: 16 chunks of 8-bit codes, 8 of 4-bit
+  // codes (by r / 2, so that the 8-byte reads of 32 rows spread over the banks)
+  auto qswz = [&](int r) { return qb == 8 ? (r & 15) : ((r >> 1) & 7); };
   // payload row r: staged in the last K step, rows [0, BM/2) in the idle
   // stage's A buffer and [BM/2, BM) in its B buffer; staged after the
   // loop, consecutive rows from the start of LDS
@@ -1003,82 +1019,125 @@ void k_fuse_dma(const MfmaArgs a) {
         const u32x4_t v = (m0 + r < M && col < rowbytes)
                               ? *reinterpret_cast<const u32x4_t*>(a.q + (int64_t)(m0 + r) * a.qstride + col)
                               : u32x4_t{0u, 0u, 0u, 0u};
-        *reinterpret_cast<u32x4_t*>(prow(false, 0, r) + ((k ^ (r & (CPR - 1))) << 4)) = v;
+        *reinterpret_cast<u32x4_t*>(prow(false, 0, r) + ((k ^ qswz(r)) << 4)) = v;
       }
     } else {
       for (int c = tid; c < BM * TB; c += NT) {
         const int r = c / TB, byte = c % TB, k = byte >> 4;
         const int64_t col = c0 + byte;
-        prow(false, 0, r)[((k ^ (r & (CPR - 1))) << 4) | (byte & 15)] =
+        prow(false, 0, r)[((k ^ qswz(r)) << 4) | (byte & 15)] =
             (m0 + r < M && col < rowbytes) ? a.q[(int64_t)(m0 + r) * a.qstride + col] : (uint8_t)0;
       }
     }
     __syncthreads();
   }
-  // fused values in ascending position order: the lane's first maximum,
-  // the larger key of the row's two lanes, then LDS atomics over the waves
-  auto run = [&](auto edge) {
+  // lane l of fragment (i, j) holds positions i*32 + 16*(l/32) + r of row
+  // j*32 + l%32 in its 16 accumulators r: one 16-byte (8-bit) or 8-byte
+  // (4-bit) LDS read gives the lane its codes; the lane's largest fused
+  // value, then the lowest of its positions holding it
+  const bool hq = a.hscale != nullptr;
+  const int hh = lane >> 5;
+  auto run = [&](auto edge, auto hidden) {
     constexpr bool kEdge = decltype(edge)::value;  // bounds checks and the fused output
+    constexpr bool kHq = decltype(hidden)::value;  // rows carry hidden-state scales
 #pragma unroll
     for (int j = 0; j < FJ; ++j) {
       const int ml = wm * (BM / WMM) + j * 32 + (lane & 31);
-      const float sc = s_sc[ml], hsc = s_sc[BM + ml];
-      float bv = -__builtin_inff();
-      int bn = -1;
+      const float sc = s_sc[ml];
       const uint8_t* qrow = prow(staged, pst, ml);
+      u32x4_t cq[FI];
 #pragma unroll
       for (int i = 0; i < FI; ++i) {
+        const int nl0 = wn * (BN / WNN) + i * 32 + 16 * hh;
+        if (qb == 8) {
+          cq[i] = *reinterpret_cast<const u32x4_t*>(qrow + (((nl0 >> 4) ^ (ml & 15)) << 4));
+        } else {
+          const int bo = nl0 >> 1;
+          const uint2 h2 = *reinterpret_cast<const uint2*>(qrow + ((((bo >> 4) ^ ((ml >> 1) & 7)) << 4) | (bo & 15)));
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int nl = wn * (BN / WNN) + i * 32 + 8 * g + 4 * (lane >> 5);
-          uint32_t c4;  // the four codes as sign-extended bytes
-          if (qb == 8) {
-            c4 = *reinterpret_cast<const uint32_t*>(qrow + ((((nl >> 4) ^ (ml & 15)) << 4) | (nl & 15)));
-          } else {
-            const int byte = nl >> 1;
-            const uint32_t h =
-                *reinterpret_cast<const uint16_t*>(qrow + ((((byte >> 4) ^ (ml & 7)) << 4) | (byte & 15)));
-            c4 = (h & 0xFu) | ((h & 0xF0u) << 4) | ((h & 0xF00u) << 8) | ((h & 0xF000u) << 12);
+          for (int g = 0; g < 4; ++g) {
+            const uint32_t h = ((g < 2 ? h2.x : h2.y) >> (16 * (g & 1))) & 0xFFFFu;
+            uint32_t c4 = (h & 0xFu) | ((h & 0xF0u) << 4) | ((h & 0xF00u) << 8) | ((h & 0xF000u) << 12);
             c4 |= (c4 & 0x08080808u) * 0x1Eu;  // a nibble's sign bit fills bits 4..7 of its byte
-          }
-          float f4[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int code = (int)(int8_t)(c4 >> (8 * e));
-            f4[e] = __builtin_fmaf((float)code, sc, acc[i][j][4 * g + e] * hsc);
-            const bool in = !kEdge || n0 + nl + e < n;
-            if (in && f4[e] > bv) {
-              bv = f4[e];
-              bn = nl + e;
-            }
-          }
-          if constexpr (kEdge) {
-            // the fused row on request: the lane's four positions in one
-            // 16-byte store where they are inside and aligned (cached stores,
-            // so that the four instructions covering a row's 32 positions
-            // meet in L2)
-            const int m = m0 + ml;
-            if (a.f && m < M) {
-              float* dst = a.f + (int64_t)m * n + n0 + nl;
-              if (n0 + nl + 4 <= n && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
-                *reinterpret_cast<float4*>(dst) = make_float4(f4[0], f4[1], f4[2], f4[3]);
-              } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  if (n0 + nl + e < n) dst[e] = f4[e];
-              }
-            }
+            cq[i][g] = c4;
           }
         }
       }
-      unsigned long long key = bn >= 0 ? argmax_key_m(bv, n0 + bn) : 0ull;
+      if constexpr (kHq) {
+        const float hsc = s_sc[BM + ml];
+#pragma unroll
+        for (int i = 0; i < FI; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[i][j][r] *= hsc;
+      }
+      float bv = -__builtin_inff();
+#pragma unroll
+      for (int i = 0; i < FI; ++i) {
+        const int nl0 = wn * (BN / WNN) + i * 32 + 16 * hh;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int code = (int)(int8_t)(cq[i][r >> 2] >> (8 * (r & 3)));
+          acc[i][j][r] = __builtin_fmaf((float)code, sc, acc[i][j][r]);
+        }
+        if constexpr (kEdge) {
+          if (a.f) {
+            // lanes l and l + 32 trade halves so that each holds positions
+            // 8q + 4*(l/32) + [0, 4) in registers 4*ro(q), ro = 0, 2, 1, 3:
+            // each store instruction then covers 32 contiguous bytes of a row
+            float x[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) x[r] = acc[i][j][r];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+#pragma unroll
+              for (int b = 0; b < 16; b += 8) {
+                const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[b + e]),
+                                                                 __float_as_uint(x[b + 4 + e]), false, false);
+                x[b + e] = __uint_as_float(sw[0]);
+                x[b + 4 + e] = __uint_as_float(sw[1]);
+              }
+            }
+            const int m = m0 + ml;
+            if (m < M) {
+              const int nlb = wn * (BN / WNN) + i * 32 + 4 * hh;
+              float* dst = a.f + (int64_t)m * n + n0 + nlb;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const int ro = ((q & 1) << 3) | ((q >> 1) << 2);
+                if (n0 + nlb + 8 * q + 4 <= n && (reinterpret_cast<uintptr_t>(dst + 8 * q) & 15) == 0) {
+                  *reinterpret_cast<float4*>(dst + 8 * q) = make_float4(x[ro], x[ro + 1], x[ro + 2], x[ro + 3]);
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e)
+                    if (n0 + nlb + 8 * q + e < n) dst[8 * q + e] = x[ro + e];
+                }
+              }
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (n0 + nl0 + r >= n) acc[i][j][r] = -__builtin_inff();
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) bv = fmaxf(bv, acc[i][j][r]);
+      }
+      int bn = 0;
+#pragma unroll
+      for (int t = FI * 16 - 1; t >= 0; --t) bn = acc[t >> 4][j][t & 15] == bv ? t : bn;
+      const int pos = wn * (BN / WNN) + (bn >> 4) * 32 + 16 * hh + (bn & 15);
+      unsigned long long key = bv > -__builtin_inff() ? argmax_key_m(bv, n0 + pos) : 0ull;
       const unsigned long long other = xor_lane_u64_32(key);
       key = key > other ? key : other;
       if (lane < 32) atomicMax(&s_rkey[ml], key);
     }
   };
-  if (a.f || m0 + BM > M || n0 + BN > n) run(std::true_type{});
-  else run(std::false_type{});
+  if (a.f || m0 + BM > M || n0 + BN > n) {
+    if (hq) run(std::true_type{}, std::true_type{});
+    else run(std::true_type{}, std::false_type{});
+  } else {
+    if (hq) run(std::false_type{}, std::true_type{});
+    else run(std::false_type{}, std::false_type{});
+  }
   __syncthreads();
   for (int i = tid; i < BM; i += NT)
     if (m0 + i < M) a.best_part[(int64_t)(m0 + i) * kMaxBlocks + nt] = s_rkey[i];
