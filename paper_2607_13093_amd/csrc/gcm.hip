@@ -71,6 +71,7 @@ template <class TE, class SB, class RK>
 __host__ __device__ __forceinline__ void aes_block(TE te, SB sb, RK rk, int nr, const uint32_t in[4],
                                                    uint32_t out[4]) {
   uint32_t s0 = in[0] ^ rk[0], s1 = in[1] ^ rk[1], s2 = in[2] ^ rk[2], s3 = in[3] ^ rk[3];
+#pragma unroll
   for (int r = 1; r < nr; ++r) {
     // column c of the next state: T0[row 0 of column c] ^ T1[row 1 of c+1]
     // ^ T2[row 2 of c+2] ^ T3[row 3 of c+3] ^ round key (ShiftRows folded in)
@@ -217,20 +218,48 @@ __device__ __forceinline__ T* seg_ptr(T* const (&base)[kGcmMaxSegs], const int64
   return b + row * l + off;
 }
 
+// The T0 table sits in LDS as kTeSlices copies, entry x of copy c at word
+// x * kTeSlices + c, and lane l reads copy l mod kTeSlices: lanes that share
+// a bank are then the lanes l, l + 16, l + 32, l + 48, where one table would
+// let any two of the 64 lanes collide.  The S-box is byte 1 of T0
+// (T0[x] = (2S(x), S(x), S(x), 3S(x))).
+constexpr int kTeSlices = 16;
+
 struct GcmShared {
-  uint32_t te[256];
-  uint8_t sb[256];
+  __attribute__((aligned(16))) uint32_t te[256 * kTeSlices];
   uint32_t rk[60];
   uint32_t red[4][4];
+};
+
+struct TeSlice {
+  const uint32_t* t;  // the lane's copy
+  __device__ __forceinline__ uint32_t operator[](uint32_t x) const { return t[x * kTeSlices]; }
+};
+struct SboxSlice {
+  const uint32_t* t;
+  __device__ __forceinline__ uint8_t operator[](uint32_t x) const {
+    return (uint8_t)(t[x * kTeSlices] >> 16);
+  }
 };
 
 __device__ __forceinline__ void stage_key(GcmShared& sh, const uint8_t* key_dev, int nr) {
   const int tid = threadIdx.x;
   const uint32_t* te = reinterpret_cast<const uint32_t*>(key_dev);
-  sh.te[tid] = te[tid];
-  sh.sb[tid] = key_dev[1024 + tid];
+  // one global load per entry, its copies written as 16-byte stores
+  for (int x = tid; x < 256; x += blockDim.x) {
+    const uint32_t v = te[x];
+#pragma unroll
+    for (int q = 0; q < kTeSlices / 4; ++q)
+      *reinterpret_cast<uint4*>(&sh.te[x * kTeSlices + 4 * q]) = make_uint4(v, v, v, v);
+  }
   if (tid < 4 * (nr + 1)) sh.rk[tid] = reinterpret_cast<const uint32_t*>(key_dev + kGcmRkOffset)[tid];
   __syncthreads();
+}
+
+__device__ __forceinline__ void aes_block_lds(const GcmShared& sh, int nr, const uint32_t in[4],
+                                              uint32_t out[4]) {
+  const uint32_t* t = sh.te + (threadIdx.x & (kTeSlices - 1));
+  aes_block(TeSlice{t}, SboxSlice{t}, sh.rk, nr, in, out);
 }
 
 // Y . G from the nibble tables in LDS: 32 independent lookups, no shifts.
@@ -253,13 +282,13 @@ __device__ __forceinline__ void mul_by_g(uint32_t y[4], const uint4* __restrict_
 
 // Counter-mode output of data block j of a row and its GHASH input (the
 // ciphertext, zero past the message).
-template <bool OPEN>
-__device__ __forceinline__ void gcm_data_block(const GcmShared& sh, int nr, const GcmSegs& segs,
+template <bool OPEN, int NR>
+__device__ __forceinline__ void gcm_data_block(const GcmShared& sh, const GcmSegs& segs,
                                                int64_t L, const uint32_t ivw[3], int64_t row, int j,
                                                uint32_t c[4]) {
   uint32_t ctr[4] = {ivw[0], ivw[1], ivw[2], (uint32_t)(2 + j)};  // inc32 from J0 + 1
   uint32_t ks[4];
-  aes_block(sh.te, sh.sb, sh.rk, nr, ctr, ks);
+  aes_block_lds(sh, NR, ctr, ks);
   const int64_t p0 = (int64_t)j * 16;
   const int valid = (int)min<int64_t>(16, L - p0);
   int64_t st;
@@ -273,7 +302,16 @@ __device__ __forceinline__ void gcm_data_block(const GcmShared& sh, int nr, cons
   const bool whole = p0 + valid <= e0;
   uint32_t x[4], y[4];
   if (whole) {
-    load_be_words(seg_ptr(segs.in, segs.ld_in, s0, row, p0 - st), valid, x);
+    const uint8_t* src = seg_ptr(segs.in, segs.ld_in, s0, row, p0 - st);
+    if (valid == 16 && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src);
+      x[0] = __builtin_bswap32(v.x);
+      x[1] = __builtin_bswap32(v.y);
+      x[2] = __builtin_bswap32(v.z);
+      x[3] = __builtin_bswap32(v.w);
+    } else {
+      load_be_words(src, valid, x);
+    }
   } else {
     uint8_t b[16];
 #pragma unroll
@@ -291,9 +329,14 @@ __device__ __forceinline__ void gcm_data_block(const GcmShared& sh, int nr, cons
   for (int k = 0; k < 4; ++k) y[k] = x[k] ^ ks[k];
   if (whole) {
     uint8_t* dst = seg_ptr(segs.out, segs.ld_out, s0, row, p0 - st);
+    if (valid == 16 && (reinterpret_cast<uintptr_t>(dst) & 15) == 0) {
+      *reinterpret_cast<uint4*>(dst) = make_uint4(__builtin_bswap32(y[0]), __builtin_bswap32(y[1]),
+                                                  __builtin_bswap32(y[2]), __builtin_bswap32(y[3]));
+    } else {
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+      for (int i = 0; i < 16; ++i)
+        if (i < valid) dst[i] = (uint8_t)(y[i >> 2] >> (24 - 8 * (i & 3)));
+    }
   } else {
 #pragma unroll
     for (int i = 0; i < 16; ++i)
@@ -328,8 +371,9 @@ __device__ __forceinline__ void gcm_data_block(const GcmShared& sh, int nr, cons
 // remaining terms: AAD block i (A_i . H^(m-i)), the length block times H,
 // and E_K(J0).  Each workgroup xor-reduces its terms into one 16-byte
 // partial of the row.
-template <bool OPEN>
-__global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ key_dev, int nr,
+// NR: 10 rounds (AES-128) or 14 (AES-256), fixed so that the rounds unroll
+template <bool OPEN, int NR>
+__global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ key_dev,
                                                     const GcmSegs segs, int64_t L, int n, int chain,
                                                     int xpart, const uint8_t* __restrict__ iv,
                                                     const uint8_t* __restrict__ aad, int64_t ld_aad,
@@ -342,7 +386,7 @@ __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ 
     tab[tid] = src[tid];
     tab[tid + 256] = src[tid + 256];
   }
-  stage_key(sh, key_dev, nr);  // ends with a barrier
+  stage_key(sh, key_dev, NR);  // ends with a barrier
   const int64_t row = blockIdx.y;
   const uint32_t* pw = reinterpret_cast<const uint32_t*>(key_dev + kGcmPowOffset);
   uint32_t ivw[4];
@@ -357,7 +401,7 @@ __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ 
       const int j = j0 + kGcmStride * i;
       if (j >= n) break;
       uint32_t c[4];
-      gcm_data_block<OPEN>(sh, nr, segs, L, ivw, row, j, c);
+      gcm_data_block<OPEN, NR>(sh, segs, L, ivw, row, j, c);
       if (i > 0) mul_by_g(y, tab);
 #pragma unroll
       for (int k = 0; k < 4; ++k) y[k] ^= c[k];
@@ -377,7 +421,7 @@ __global__ __launch_bounds__(256) void k_gcm_blocks(const uint8_t* __restrict__ 
     uint32_t c[4], r[4];
     if (u == na + 1) {
       const uint32_t j0b[4] = {ivw[0], ivw[1], ivw[2], 1u};
-      aes_block(sh.te, sh.sb, sh.rk, nr, j0b, r);
+      aes_block_lds(sh, NR, j0b, r);
     } else {
       int e;
       if (u < na) {
@@ -443,12 +487,11 @@ hipError_t launch_gcm(bool open, const uint8_t* key_dev, int nr, const GcmSegs& 
   const int chain = gcm_chain(rows, n);
   int xpart = 0;
   const int nparts = gcm_parts(n, (la + 15) / 16, chain, &xpart);
-  if (open)
-    launch_kernel(k_gcm_blocks<true>, dim3(nparts, rows), dim3(kGcmStride), 0, s, key_dev, nr, segs, L, n,
-                  chain, xpart, iv, aad, ld_aad, la, partial, nparts);
-  else
-    launch_kernel(k_gcm_blocks<false>, dim3(nparts, rows), dim3(kGcmStride), 0, s, key_dev, nr, segs, L, n,
-                  chain, xpart, iv, aad, ld_aad, la, partial, nparts);
+  if (nr != 10 && nr != 14) return hipErrorInvalidValue;
+  auto kern = open ? (nr == 10 ? k_gcm_blocks<true, 10> : k_gcm_blocks<true, 14>)
+                   : (nr == 10 ? k_gcm_blocks<false, 10> : k_gcm_blocks<false, 14>);
+  launch_kernel(kern, dim3(nparts, rows), dim3(kGcmStride), 0, s, key_dev, segs, L, n, chain, xpart, iv,
+                aad, ld_aad, la, partial, nparts);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int fb = (rows + 255) / 256;
