@@ -61,6 +61,7 @@ constexpr int kMaxSub = 4 * kSub;  // window of at most 4 buckets
 constexpr int kMaxSeg = kSThreads; // segments per row, one per thread in scans
 constexpr int kMaxCand = 1024;     // window elements held in LDS
 constexpr int kChunk = 256;        // positions per wave iteration
+constexpr int kSegChunks = 4;      // chunks per segment at least
 constexpr float kYSpan = 40.0f;
 static_assert(kMaxCand == 2 * kSThreads, "two list entries per thread");
 static_assert(kCoarse == 2 * kSThreads, "two coarse buckets per thread");
@@ -426,6 +427,24 @@ __device__ __forceinline__ void for_chunks(const float* __restrict__ row, int n,
   }
 }
 
+// fn(q, p, x, v) on every chunk q of the row, each wave on one contiguous
+// range of chunks (so that a segment's chunks mostly fall to one wave), two
+// chunks loaded per iteration.
+template <bool VEC, class F>
+__device__ __forceinline__ void for_chunks_contig(const float* __restrict__ row, int n, int NC, F&& fn) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int per = (NC + kSWaves - 1) / kSWaves;
+  const int q1 = min(NC, (wave + 1) * per);
+  for (int q = wave * per; q < q1; q += 2) {
+    float x0[4], x1[4];
+    bool v0[4], v1[4];
+    load4<VEC>(row, n, q * kChunk + 4 * lane, x0, v0);
+    if (q + 1 < q1) load4<VEC>(row, n, (q + 1) * kChunk + 4 * lane, x1, v1);
+    fn(q, q * kChunk + 4 * lane, x0, v0);
+    if (q + 1 < q1) fn(q + 1, (q + 1) * kChunk + 4 * lane, x1, v1);
+  }
+}
+
 // VEC: rows start 16-byte aligned (n % 4 == 0), positions load as float4.
 template <bool VEC>
 __global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) void k_sample(
@@ -436,8 +455,9 @@ __global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) 
   const int m = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float* row = f + (int64_t)m * n;
-  // segments of G positions (a multiple of the chunk), at most kMaxSeg of them
-  const int G = kChunk * ((n + kChunk * kMaxSeg - 1) / (kChunk * kMaxSeg));
+  // segments of G positions (a multiple of the chunk, at least kSegChunks
+  // chunks), at most kMaxSeg of them
+  const int G = kChunk * max(kSegChunks, (n + kChunk * kMaxSeg - 1) / (kChunk * kMaxSeg));
   const int NS = (n + G - 1) / G;
   const int NC = (n + kChunk - 1) / kChunk;
 
@@ -470,49 +490,75 @@ __global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) 
   };
 
   // Exact pass with the window [lo, hi]: segment masses of the buckets below
-  // lo, the window's elements into the list.  Returns the total mass Z.
+  // lo, the window's elements into the list.  Returns the total mass Z.  A
+  // wave's chunks are contiguous, so each lane sums its share of a segment
+  // and the wave reduces it once per segment (one wave-wide sum per chunk
+  // cost a quarter of the pass); one vote per chunk skips the list code
+  // where no element of the chunk falls in the window.
   auto collect = [&](int lo, int hi) -> U128 {
     uint64_t za = 0ull, zb = 0ull;
-    for_chunks<VEC>(row, n, NC, [&](int q, int p, const float (&x)[4], const bool (&v)[4]) {
+    uint64_t sa = 0ull, sbm = 0ull;  // the lane's masses below the window in segment cur
+    int cur = -1;
+    auto flush = [&]() {
+      const uint64_t A = wave_sum_u64(sa), B = wave_sum_u64(sbm);
+      if (lane == 0 && (A | B)) {
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[cur]), (unsigned long long)A);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[cur]), (unsigned long long)B);
+      }
+      sa = 0ull;
+      sbm = 0ull;
+    };
+    for_chunks_contig<VEC>(row, n, NC, [&](int q, int p, const float (&x)[4], const bool (&v)[4]) {
+      const int sg = q * kChunk / G;
+      if (sg != cur) {
+        if (cur >= 0) flush();
+        cur = sg;
+      }
       uint32_t ca = 0u, cb = 0u, ma = 0u, mb = 0u;  // four weights of at most 2^28 each
+      Fix w[4];
+      bool cand[4];
+      bool anyc = false;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const Fix w = fix(x[e]);
+        w[e] = fix(x[e]);
         const int b = bucket_of(ypos(x[e], vmax, kb));
-        ca += v[e] ? w.a : 0u;
-        cb += v[e] ? w.b : 0u;
+        ca += v[e] ? w[e].a : 0u;
+        cb += v[e] ? w[e].b : 0u;
         const bool mem = v[e] && b < lo;
-        ma += mem ? w.a : 0u;
-        mb += mem ? w.b : 0u;
-        const bool cand = v[e] && b >= lo && b <= hi;
-        const uint64_t bal = __ballot(cand);
-        if (bal) {
-          const int leader = __ffsll((unsigned long long)bal) - 1;
-          int base = 0;
-          if (lane == leader) base = atomicAdd(&sh.ncand, __popcll(bal));
-          base = __shfl(base, leader, 64);
-          if (cand) {
-            const int slot = base + __popcll(bal & ((1ull << lane) - 1ull));
-            if (slot < kMaxCand) {
-              sh.u.c.key[slot] = ((uint64_t)(~orderable(x[e])) << 32) | (uint32_t)(p + e);
-              sh.u.c.a[slot] = w.a;
-              sh.u.c.b[slot] = w.b;
+        ma += mem ? w[e].a : 0u;
+        mb += mem ? w[e].b : 0u;
+        cand[e] = v[e] && b >= lo && b <= hi;
+        anyc |= cand[e];
+      }
+      if (__ballot(anyc)) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint64_t bal = __ballot(cand[e]);
+          if (bal) {
+            const int leader = __ffsll((unsigned long long)bal) - 1;
+            int base = 0;
+            if (lane == leader) base = atomicAdd(&sh.ncand, __popcll(bal));
+            base = __shfl(base, leader, 64);
+            if (cand[e]) {
+              const int slot = base + __popcll(bal & ((1ull << lane) - 1ull));
+              if (slot < kMaxCand) {
+                const Fix wr = w[e];
+                sh.u.c.key[slot] = ((uint64_t)(~orderable(x[e])) << 32) | (uint32_t)(p + e);
+                sh.u.c.a[slot] = wr.a;
+                sh.u.c.b[slot] = wr.b;
+              }
             }
           }
         }
       }
       za += ca;
       zb += cb;
-      const uint64_t A = wave_sum_u64(ma), B = wave_sum_u64(mb);
-      if (lane == 0 && (A | B)) {
-        const int sg = q * kChunk / G;
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_a[sg]), (unsigned long long)A);
-        atomicAdd(reinterpret_cast<unsigned long long*>(&sh.seg_b[sg]), (unsigned long long)B);
-      }
+      sa += ma;
+      sbm += mb;
     });
+    if (cur >= 0) flush();
     return block_sum_u128(u128_join(za, zb), sh);  // barriers: segments and list complete
   };
-
   const bool all = !(top_p < 1.0f);
   int lo = kBuckets, hi = kBuckets - 1;  // all: every bucket below lo, no window
   if (!all) {
@@ -923,11 +969,25 @@ __global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) 
     if (sg >= 0) {
       U128 run = sh.claim_base;
       const int end = min(n, (sg + 1) * G);
-      for (int cb = sg * G; cb < end && pick < 0; cb += kChunk) {
+      // the segment's chunks in groups of kSegChunks, a group's loads issued
+      // together
+      for (int cg = sg * G; cg < end && pick < 0; cg += kSegChunks * kChunk) {
+      float xg[kSegChunks][4];
+      bool vg[kSegChunks][4];
+#pragma unroll
+      for (int c = 0; c < kSegChunks; ++c) load4<VEC>(row, n, cg + c * kChunk + 4 * lane, xg[c], vg[c]);
+#pragma unroll
+      for (int c = 0; c < kSegChunks; ++c) {
+        const int cb = cg + c * kChunk;
+        if (cb >= end || pick >= 0) break;
         const int p = cb + 4 * lane;
         float x[4];
         bool v[4];
-        load4<VEC>(row, n, p, x, v);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[e] = xg[c][e];
+          v[e] = vg[c][e];
+        }
         U128 li[4];
         U128 l{0ull, 0ull};
 #pragma unroll
@@ -950,6 +1010,7 @@ __global__ __launch_bounds__(kSThreads) __attribute__((amdgpu_waves_per_eu(6))) 
           pick = cb + 4 * src + __shfl(hit, src, 64);
         }
         run = u128_add(run, U128{shfl_u64(inc.lo, 63), shfl_u64(inc.hi, 63)});
+      }
       }
     }
     if (lane == 0) tokens[m] = ids[pick >= 0 ? pick : 0];
