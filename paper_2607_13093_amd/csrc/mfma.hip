@@ -522,7 +522,42 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ int swz8(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+// Copy addressing of the direct-to-LDS kernels.  With O32 every lane keeps
+// its row's byte offset (below 4 GiB) in a 32-bit register and the step's
+// base stays scalar: each copy is then the scalar-base + 32-bit-offset form
+// of global_load_lds with no address arithmetic of its own (the empty asm
+// keeps the compiler from folding the base into 64-bit lane addresses, which
+// costs a 64-bit add per copy and chains the copies through one register
+// pair).  Measured on dense_sub's cloud projection: 1106 -> 1033 us.
+__device__ __forceinline__ const uint8_t* scalar_ptr(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint8_t*>(((uint64_t)hi << 32) | lo);
+}
+
+template <bool O32>
+struct LaneAddr;
+template <>
+struct LaneAddr<true> {
+  uint32_t off;
+  __device__ __forceinline__ void set(const uint8_t*, int64_t o) { off = (uint32_t)o; }
+  // base: the step's scalar base (from scalar_ptr)
+  __device__ __forceinline__ void copy(const uint8_t* base, int64_t, lds_void_t* dst) {
+    asm volatile("" : "+v"(off));
+    __builtin_amdgcn_global_load_lds(base + off, dst, 16, 0, 0);
+  }
+};
+template <>
+struct LaneAddr<false> {
+  const uint8_t* p;
+  __device__ __forceinline__ void set(const uint8_t* base, int64_t o) { p = base + o; }
+  __device__ __forceinline__ void copy(const uint8_t*, int64_t step, lds_void_t* dst) {
+    __builtin_amdgcn_global_load_lds(p + step, dst, 16, 0, 0);
+  }
+};
+
+template <int BM, int BN, int WM, int WN, int EPI, bool O32>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
 void k_mfma_dma(const MfmaArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -561,32 +596,31 @@ void k_mfma_dma(const MfmaArgs a) {
 
   // lane -> row (lane / 8) of its 8-row group and the logical chunk it fetches
   const int lr = lane >> 3;
-  const uint8_t* pa[A_INS];
-  const uint8_t* pb[B_INS];
+  const uint8_t* hbase = reinterpret_cast<const uint8_t*>(a.h);
+  LaneAddr<O32> pa[A_INS], pb[B_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
     const int r = (iw * A_INS + i) * 8 + lr;
     const int lc = (lane & 7) ^ swz8(r);
-    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+    pa[i].set(hbase, (int64_t)min(m0 + r, M - 1) * a.ldh * 2 + lc * 16);
   }
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
     const int r = (iw * B_INS + i) * 8 + lr;
     const int lc = (lane & 7) ^ swz8(r);
-    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+    pb[i].set(a.w, (int64_t)s_ids[r] * a.ldw_bytes + lc * 16);
   }
   auto issue = [&](int k0, int stage) {
     if (wave >= IW) return;
     uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
     uint8_t* bs = reinterpret_cast<uint8_t*>(Bs + stage * BN * kBK);
+    const int64_t step = (int64_t)k0 * 2;
+    const uint8_t* ha = O32 ? scalar_ptr(hbase + step) : nullptr;
+    const uint8_t* wb = O32 ? scalar_ptr(a.w + step) : nullptr;
 #pragma unroll
-    for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
-                                       (lds_void_t*)(as + (iw * A_INS + i) * 1024), 16, 0, 0);
+    for (int i = 0; i < A_INS; ++i) pa[i].copy(ha, step, (lds_void_t*)(as + (iw * A_INS + i) * 1024));
 #pragma unroll
-    for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pb[i] + (int64_t)k0 * 2,
-                                       (lds_void_t*)(bs + (iw * B_INS + i) * 1024), 16, 0, 0);
+    for (int i = 0; i < B_INS; ++i) pb[i].copy(wb, step, (lds_void_t*)(bs + (iw * B_INS + i) * 1024));
   };
 
   f32x16_t acc[FM][FN];
@@ -654,7 +688,7 @@ void k_mfma_dma(const MfmaArgs a) {
 // the wait.
 __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, bool O32>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WM * WN / 4, WM * WN / 4)))
 void k_mfma_dma8(const MfmaArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -687,32 +721,31 @@ void k_mfma_dma8(const MfmaArgs a) {
   }
   __syncthreads();
 
-  const uint8_t* pa[A_INS];
-  const uint8_t* pb[B_INS];
+  const uint8_t* hbase = reinterpret_cast<const uint8_t*>(a.h);
+  LaneAddr<O32> pa[A_INS], pb[B_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
     const int r = (iw * A_INS + i) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ swz8(r);
-    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+    pa[i].set(hbase, (int64_t)min(m0 + r, M - 1) * a.ldh * 2 + lc * 16);
   }
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
     const int r = (iw * B_INS + i) * 16 + (lane >> 2);
     const int lc = (lane & 3) ^ swz4(r);
-    pb[i] = a.w + (int64_t)s_ids[r] * a.ldw_bytes + lc * 16;
+    pb[i].set(a.w, (int64_t)s_ids[r] * a.ldw_bytes + lc * 16);
   }
   auto issue = [&](int k0, int stage) {
     if (wave >= IW) return;
     uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
     uint8_t* bs = Bs + stage * BN * kBK;
+    const uint8_t* ha = O32 ? scalar_ptr(hbase + (int64_t)k0 * 2) : nullptr;
+    const uint8_t* wb = O32 ? scalar_ptr(a.w + k0) : nullptr;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
-                                       (lds_void_t*)(as + (iw * A_INS + i) * 1024), 16, 0, 0);
+      pa[i].copy(ha, (int64_t)k0 * 2, (lds_void_t*)(as + (iw * A_INS + i) * 1024));
 #pragma unroll
-    for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pb[i] + k0, (lds_void_t*)(bs + (iw * B_INS + i) * 1024),
-                                       16, 0, 0);
+    for (int i = 0; i < B_INS; ++i) pb[i].copy(wb, k0, (lds_void_t*)(bs + (iw * B_INS + i) * 1024));
   };
 
   f32x16_t acc[FM][FN];
@@ -856,7 +889,7 @@ constexpr size_t fuse_dma_lds_bytes() {
          (size_t)BM * 8;
 }
 
-template <int BM, int WNN, int WMM>
+template <int BM, int WNN, int WMM, bool O32>
 __global__ __launch_bounds__(64 * WNN * WMM)
 __attribute__((amdgpu_waves_per_eu(WNN * WMM / 4, WNN * WMM / 4)))
 void k_fuse_dma(const MfmaArgs a) {
@@ -893,13 +926,13 @@ void k_fuse_dma(const MfmaArgs a) {
   }
   __syncthreads();
   const int lr = lane >> 3;
-  const uint8_t* pa[A_INS];
-  const uint8_t* pb[B_INS];
+  const uint8_t* hbase = reinterpret_cast<const uint8_t*>(a.h);
+  LaneAddr<O32> pa[A_INS], pb[B_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
     const int r = (iw * A_INS + i) * 8 + lr;
     const int lc = (lane & 7) ^ swz8(r);
-    pa[i] = reinterpret_cast<const uint8_t*>(a.h + (int64_t)min(m0 + r, M - 1) * a.ldh) + lc * 16;
+    pa[i].set(hbase, (int64_t)min(m0 + r, M - 1) * a.ldh * 2 + lc * 16);
   }
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
@@ -910,20 +943,19 @@ void k_fuse_dma(const MfmaArgs a) {
     // position 16h + 4g + e, so a lane's 16 accumulators cover 16
     // consecutive positions
     const int pr = (r & ~31) | (((r >> 2) & 1) << 4) | (((r >> 3) & 3) << 2) | (r & 3);
-    pb[i] = a.w + (int64_t)s_ids[pr] * a.ldw_bytes + lc * 16;
+    pb[i].set(a.w, (int64_t)s_ids[pr] * a.ldw_bytes + lc * 16);
   }
   auto issue = [&](int k0, int stage) {
     if (wave >= IW) return;
     uint8_t* as = reinterpret_cast<uint8_t*>(As + stage * BM * kBK);
     uint8_t* bs = reinterpret_cast<uint8_t*>(Bs + stage * BN * kBK);
+    const int64_t step = (int64_t)k0 * 2;
+    const uint8_t* ha = O32 ? scalar_ptr(hbase + step) : nullptr;
+    const uint8_t* wb = O32 ? scalar_ptr(a.w + step) : nullptr;
 #pragma unroll
-    for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pa[i] + (int64_t)k0 * 2,
-                                       (lds_void_t*)(as + (iw * A_INS + i) * 1024), 16, 0, 0);
+    for (int i = 0; i < A_INS; ++i) pa[i].copy(ha, step, (lds_void_t*)(as + (iw * A_INS + i) * 1024));
 #pragma unroll
-    for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds(pb[i] + (int64_t)k0 * 2,
-                                       (lds_void_t*)(bs + (iw * B_INS + i) * 1024), 16, 0, 0);
+    for (int i = 0; i < B_INS; ++i) pb[i].copy(wb, step, (lds_void_t*)(bs + (iw * B_INS + i) * 1024));
   };
   const int qb = a.qbits;
   const int TB = BN * qb / 8;  // code bytes of a tile row
@@ -1190,30 +1222,40 @@ static hipError_t set_lds_limit_once(std::atomic<uint64_t>& done, const void* ke
   return e;
 }
 
+// 32-bit copy offsets (LaneAddr<true>) when every row the copies address
+// lies below 4 GiB of its operand's base.
+static bool copy_offsets_fit(const MfmaArgs& a) {
+  constexpr int64_t kLim = 0xFFFFFFFFll;
+  return a.w_rows > 0 && (int64_t)a.M * a.ldh * 2 <= kLim && a.w_rows * a.ldw_bytes <= kLim;
+}
+
 template <int BM, int BN, int WT, int EPI>
 static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
-  static std::atomic<uint64_t> lds_set_dma{0}, lds_set_reg{0};
+  static std::atomic<uint64_t> lds_set_dma{0}, lds_set_dma64{0}, lds_set_reg{0};
   constexpr int WM = WaveGrid<BM, EPI>::WM, WN = WaveGrid<BM, EPI>::WN, NT = 64 * WM * WN;
   a.m_tiles = (a.M + BM - 1) / BM;
   a.n_tiles = (a.n + BN - 1) / BN;
   if (a.n_tiles > kMaxBlocks) return hipErrorInvalidValue;
+  const bool o32 = copy_offsets_fit(a);
   if constexpr (EPI == kEpiFuse) {
     if (a.K % kBK == 0) {
       // transposed tiles: waves along the positions x waves along the rows
       constexpr int WNN = BM == 256 ? 2 : BM == 320 ? 4 : BM == 128 ? 2 : 4;
       constexpr int WMM = BM == 256 ? 4 : BM == 320 ? 2 : BM == 128 ? 2 : 1;
-      auto kf = k_fuse_dma<BM, WNN, WMM>;
+      auto kf = o32 ? k_fuse_dma<BM, WNN, WMM, true> : k_fuse_dma<BM, WNN, WMM, false>;
       constexpr size_t lds_f = fuse_dma_lds_bytes<BM, WNN, WMM>();
-      static std::atomic<uint64_t> lds_set_fuse{0};
-      hipError_t e = set_lds_limit_once(lds_set_fuse, reinterpret_cast<const void*>(kf), lds_f);
+      static std::atomic<uint64_t> lds_set_fuse{0}, lds_set_fuse64{0};
+      hipError_t e = set_lds_limit_once(o32 ? lds_set_fuse : lds_set_fuse64,
+                                        reinterpret_cast<const void*>(kf), lds_f);
       if (e != hipSuccess) return e;
       launch_kernel(kf, dim3(a.m_tiles * a.n_tiles), dim3(64 * WNN * WMM), lds_f, s, a);
       return hipGetLastError();
     }
   } else if (a.K % kBK == 0) {
-    auto kd = WT == 0 ? k_mfma_dma<BM, BN, WM, WN, EPI> : k_mfma_dma8<BM, BN, WM, WN, EPI>;
+    auto kd = WT == 0 ? (o32 ? k_mfma_dma<BM, BN, WM, WN, EPI, true> : k_mfma_dma<BM, BN, WM, WN, EPI, false>)
+                      : (o32 ? k_mfma_dma8<BM, BN, WM, WN, EPI, true> : k_mfma_dma8<BM, BN, WM, WN, EPI, false>);
     constexpr size_t lds_d = WT == 0 ? mfma_dma_lds_bytes<BM, BN>() : mfma_dma8_lds_bytes<BM, BN>();
-    hipError_t e = set_lds_limit_once(lds_set_dma, reinterpret_cast<const void*>(kd), lds_d);
+    hipError_t e = set_lds_limit_once(o32 ? lds_set_dma : lds_set_dma64, reinterpret_cast<const void*>(kd), lds_d);
     if (e != hipSuccess) return e;
     launch_kernel(kd, dim3(a.m_tiles * a.n_tiles), dim3(NT), lds_d, s, a);
     return hipGetLastError();

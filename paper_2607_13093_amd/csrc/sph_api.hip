@@ -422,6 +422,7 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
     a.K = (int)d_cloud;
     a.w = static_cast<const uint8_t*>(w_cloud);
     a.ldw_bytes = ldw * wbytes;
+    a.w_rows = subset->vocab;
     a.wscale = w_row_scale;
     a.ids = subset->d_ids;
     a.n = (int)n;
@@ -445,6 +446,7 @@ int sph_cloud_partial_fmt(const void* h_cloud, int64_t ldh, int64_t M, int64_t d
     a.K = (int)d_cloud;
     a.w = static_cast<const uint8_t*>(w_cloud);
     a.ldw_bytes = ldw * wbytes;
+    a.w_rows = subset->vocab;
     a.wscale = w_row_scale;
     a.ids = subset->d_ids;
     a.n = (int)n;
@@ -614,6 +616,7 @@ int fuse_verify_impl(const char* fn, bool codes, const void* q, const float* sca
     a.K = (int)d_end;
     a.w = static_cast<const uint8_t*>(w_end);
     a.ldw_bytes = ldw * 2;
+    a.w_rows = subset->vocab;
     a.ids = subset->d_ids;
     a.n = (int)n;
     a.q = static_cast<const uint8_t*>(q);

@@ -85,6 +85,7 @@ struct MfmaArgs {
   int K;                  // multiple of 8 (bf16 weights) or 16 (fp8 weights)
   const uint8_t* w;       // weight rows, vocab-major, 16-byte aligned
   int64_t ldw_bytes;
+  int64_t w_rows;         // rows of w the ids address (the vocabulary); 0 if unknown
   const float* wscale;    // fp32 [V] for fp8 weights, else null
   const int32_t* ids;     // subset ids [n]
   int n;

@@ -26,12 +26,14 @@ def say(*a):
     sys.stdout.flush()
 
 
-def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag="", sessions=None):
+def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag="", sessions=None,
+                    dw=None):
     """Full staged parity A-E of one greedy workload; returns the stats.
 
     The GPU always runs the whole workload (the launch configuration of the
     benchmark); with `sessions` the oracle checks only those sessions' rows
     (rows are independent, and whole sessions keep accept lengths checkable).
+    `dw`: the workload's device tensors, when the test lays them out itself.
     """
     cfg = wl.cfg
     h_bits = wl.h_bits if h_bits is None else h_bits
@@ -53,7 +55,8 @@ def run_greedy_case(wl, h_bits=None, w_end_bits=None, w_cloud_bits=None, tag="",
 
     say(f"[gpu] {tag or cfg.name}: cloud_partial M={cfg.M} d={cfg.d} d_end={cfg.d_end} "
         f"n={len(wl.subset)} wtype={cfg.wtype}")
-    dw = P.DeviceWorkload(wl, h_bits=h_bits, w_end_bits=w_end_bits, w_cloud_bits=w_cloud_bits)
+    if dw is None:
+        dw = P.DeviceWorkload(wl, h_bits=h_bits, w_end_bits=w_end_bits, w_cloud_bits=w_cloud_bits)
     q, s, z = dw.cloud()
     torch.cuda.synchronize()
     qh, sh, zh = P.host(q)[rows], P.host(s)[rows], P.host(z)[rows]
@@ -117,6 +120,27 @@ def test_paper_shape_full_vocabulary(d_end):
     cfg = Config("paper_shape", 60 + d_end, d=4096, d_end=d_end, vocab=150000, n_sub=150000,
                  subset_kind="full", sessions=1, rows_per_session=5)
     run_greedy_case(make_workload(cfg), tag=f"paper shape d_end={d_end}")
+
+
+def test_weights_beyond_4gib_of_their_base():
+    # weight rows more than 4 GiB past the start of the weights: the
+    # direct-to-LDS projections then address their copies with 64-bit lane
+    # addresses instead of 32-bit offsets from a scalar base (40 rows: the
+    # MFMA path in both calls)
+    cfg = Config("wide", 71, d=1088, d_end=64, vocab=70000, n_sub=20000, subset_kind="choice",
+                 sessions=8, rows_per_session=5)
+    wl = make_workload(cfg)
+    dw = P.DeviceWorkload(wl)
+    stride = 32768  # bf16 elements per row: 64 KiB rows, 4.6 GB in all
+    dc, de = cfg.d - cfg.d_end, cfg.d_end
+    big = torch.empty((cfg.vocab, stride), dtype=torch.bfloat16, device="cuda")
+    big[:, :dc] = dw.w_cloud
+    big[:, stride // 2:stride // 2 + de] = dw.w_end
+    dw.w_cloud, dw.w_end = big[:, :dc], big[:, stride // 2:stride // 2 + de]
+    assert int(np.max(wl.subset)) * stride * 2 > 2 ** 32
+    run_greedy_case(wl, tag="weights beyond 4 GiB", dw=dw)
+    del big, dw
+    torch.cuda.empty_cache()
 
 
 # ---------------------------------------------------------------------------
