@@ -770,6 +770,17 @@ void k_mfma_dma8(const MfmaArgs a) {
       // fit in registers next to the accumulators, so the next stage's loads
       // go out first and each sub-step reads its own fragments (the other
       // wave of the SIMD covers any wait on the loads).
+      // the step's fp8 codes (8 bytes per fragment and sub-step) are read
+      // before the next stage's copies go out: a read of LDS behind pending
+      // copies waits for them, and these are the reads that would
+      uint2 qb[kBK / 16][FN];
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int row = wn * TN + j * 32 + (lane & 31);
+          qb[kk][j] = *reinterpret_cast<const uint2*>(bs + row * kBK + ((kk ^ swz4(row)) << 4) + 8 * (lane >> 5));
+        }
       if (k0 + kBK < K) issue(k0 + kBK, stage ^ 1);
 #pragma unroll
       for (int kk = 0; kk < kBK / 16; ++kk) {
@@ -782,9 +793,7 @@ void k_mfma_dma8(const MfmaArgs a) {
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          const int row = wn * TN + j * 32 + (lane & 31);
-          const uint2 q = *reinterpret_cast<const uint2*>(bs + row * kBK + ((kk ^ swz4(row)) << 4) +
-                                                          8 * (lane >> 5));
+          const uint2 q = qb[kk][j];
           u32x4_t w;
           w.x = e4m3x2_to_bf16x2_m<false>(q.x);
           w.y = e4m3x2_to_bf16x2_m<true>(q.x);
