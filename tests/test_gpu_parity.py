@@ -122,24 +122,27 @@ def test_paper_shape_full_vocabulary(d_end):
     run_greedy_case(make_workload(cfg), tag=f"paper shape d_end={d_end}")
 
 
-def test_weights_beyond_4gib_of_their_base():
+@pytest.mark.parametrize("wtype", ["bf16", "fp8"])
+def test_weights_beyond_4gib_of_their_base(wtype):
     # weight rows more than 4 GiB past the start of the weights: the
     # direct-to-LDS projections then address their copies with 64-bit lane
     # addresses instead of 32-bit offsets from a scalar base (40 rows: the
-    # MFMA path in both calls)
+    # MFMA path in both calls; bf16 or E4M3 cloud weights)
     cfg = Config("wide", 71, d=1088, d_end=64, vocab=70000, n_sub=20000, subset_kind="choice",
-                 sessions=8, rows_per_session=5)
+                 sessions=8, rows_per_session=5, wtype=wtype)
     wl = make_workload(cfg)
     dw = P.DeviceWorkload(wl)
-    stride = 32768  # bf16 elements per row: 64 KiB rows, 4.6 GB in all
+    row_bytes = 65536  # 70000 rows of 64 KiB: 4.6 GB
     dc, de = cfg.d - cfg.d_end, cfg.d_end
-    big = torch.empty((cfg.vocab, stride), dtype=torch.bfloat16, device="cuda")
-    big[:, :dc] = dw.w_cloud
-    big[:, stride // 2:stride // 2 + de] = dw.w_end
-    dw.w_cloud, dw.w_end = big[:, :dc], big[:, stride // 2:stride // 2 + de]
-    assert int(np.max(wl.subset)) * stride * 2 > 2 ** 32
-    run_greedy_case(wl, tag="weights beyond 4 GiB", dw=dw)
-    del big, dw
+    wc = torch.empty((cfg.vocab, row_bytes // dw.w_cloud.element_size()), dtype=dw.w_cloud.dtype,
+                     device="cuda")
+    wc[:, :dc] = dw.w_cloud
+    we = torch.empty((cfg.vocab, row_bytes // 2), dtype=torch.bfloat16, device="cuda")
+    we[:, :de] = dw.w_end
+    dw.w_cloud, dw.w_end = wc[:, :dc], we[:, :de]
+    assert int(np.max(wl.subset)) * row_bytes > 2 ** 32
+    run_greedy_case(wl, tag=f"{wtype} weights beyond 4 GiB", dw=dw)
+    del wc, we, dw
     torch.cuda.empty_cache()
 
 
