@@ -730,6 +730,258 @@ void k_mfma_dma(const MfmaArgs a) {
 #endif
 }
 
+// One wave per SIMD for the dense bf16 cloud projection (256 x 256 tiles, an
+// even number of 64-wide K steps).  Four waves, each a 128 x 128 wave tile of
+// 4 x 4 fragments whose 256 accumulators stay in the AGPRs: per 16-wide
+// sub-step a wave reads 8 fragments for 16 MFMAs, where the two-wave kernel
+// reads 6 for 8, so the LDS traffic per flop drops by a third.  With no second
+// wave on the SIMD the schedule is explicit: the MFMAs and the LDS fragment
+// reads are inline asm (their order is kept as written), each sub-step's 16
+// MFMAs run on one of two fragment register sets while the next sub-step's 8
+// reads go out after its first 8 MFMAs, and the step barrier comes after the
+// 12th MFMA of the third sub-step, so the rest of the step's MFMAs cover the
+// barrier and the next stage's first reads.  The copies for two steps ahead
+// are issued in the last sub-step (past the end they copy the last step again:
+// in-bounds reads into a stage nobody reads), which keeps the K loop
+// straight-line code: with a branch in it the compiler spilled registers that
+// reads still in flight were to fill.  Because the compiler sees neither the
+// asm reads nor the MFMAs, every wait is explicit (lgkmcnt before a sub-step's
+// MFMAs, vmcnt before the barrier) and each sub-step's fragments are kept
+// allocated to its end.
+__device__ __forceinline__ void w1_mfma(f32x16_t& c, const bf16x8_t& a, const bf16x8_t& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+template <int OFF>
+__device__ __forceinline__ void w1_read(bf16x8_t& d, uint32_t addr) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
+}
+__device__ __forceinline__ void w1_wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void w1_wait_mem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+typedef __attribute__((address_space(3))) const char* lds_cptr_t;
+
+constexpr int kW1Barrier = 12;  // the step barrier follows this many MFMAs of the third sub-step
+
+template <int EPI>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_mfma_w1(const MfmaArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  static_assert(EPI == kEpiCloud, "cloud epilogue only");
+  constexpr int BM = 256, BN = 256, NT = 256, WN = 2, TM = 128, TN = 128, FM = 4, FN = 4;
+  constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;  // 8 + 8 copies per wave per step
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint16_t* As = reinterpret_cast<uint16_t*>(smem);  // [2][256][64]
+  uint16_t* Bs = As + 2 * BM * kBK;                   // [2][256][64]
+  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + 2 * BN * kBK);
+  uint32_t* s_rmax = reinterpret_cast<uint32_t*>(s_ids + BN);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WN, wn = wave % WN;
+  int mt, nt;
+  tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
+  const int m0 = mt * BM, n0 = nt * BN;
+  const int M = a.M, K = a.K, n = a.n;
+  const int S = K / kBK;  // even and at least 2 (the launcher's condition)
+  const int last_id = a.ids[min(n, n0 + BN) - 1];
+  for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+  for (int i = tid; i < BM; i += NT) s_rmax[i] = 0u;
+  __syncthreads();
+
+  const int lr = lane >> 3;
+  const uint8_t* hbase = reinterpret_cast<const uint8_t*>(a.h);
+  LaneAddr<true> pa[A_INS], pb[B_INS];
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) {
+    const int r = (wave * A_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pa[i].set(hbase, (int64_t)min(m0 + r, M - 1) * a.ldh * 2 + lc * 16);
+  }
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) {
+    const int r = (wave * B_INS + i) * 8 + lr;
+    const int lc = (lane & 7) ^ swz8(r);
+    pb[i].set(a.w, (int64_t)s_ids[r] * a.ldw_bytes + lc * 16);
+  }
+  // copy i (0..15) of this wave's share of step s into stage st
+  auto copy1 = [&](int i, int s, int st) {
+    const int64_t step = (int64_t)s * kBK * 2;
+    if (i < A_INS) {
+      uint8_t* as = reinterpret_cast<uint8_t*>(As) + st * BM * kBK * 2;
+      pa[i].copy(scalar_ptr(hbase + step), step, (lds_void_t*)(as + (wave * A_INS + i) * 1024));
+    } else {
+      uint8_t* bs = reinterpret_cast<uint8_t*>(Bs) + st * BN * kBK * 2;
+      pb[i - A_INS].copy(scalar_ptr(a.w + step), step, (lds_void_t*)(bs + (wave * B_INS + i - A_INS) * 1024));
+    }
+  };
+  // fragment reads: row (lane & 31) of a fragment, 16-byte chunk 2 kk + lane / 32
+  // (swizzled); the fragments of a wave are 32 rows (4 KB) apart and the
+  // stages 32 KB apart, both immediate offsets of the read
+  uint32_t adA[4], adB[4];
+  {
+    const int sw = swz8(lane & 31);  // rows 32 apart share the swizzle
+    const uint32_t baseA = (uint32_t)(uintptr_t)(lds_cptr_t)As + (uint32_t)((wm * TM + (lane & 31)) * 128);
+    const uint32_t baseB = (uint32_t)(uintptr_t)(lds_cptr_t)Bs + (uint32_t)((wn * TN + (lane & 31)) * 128);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint32_t c = (uint32_t)(((kk * 2 + (lane >> 5)) ^ sw) << 4);
+      adA[kk] = baseA + c;
+      adB[kk] = baseB + c;
+    }
+  }
+  f32x16_t acc[FM][FN];
+  {
+    f32x16_t z0;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z0[r] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) asm volatile("; zero accumulators" : "=a"(acc[i][j]) : "0"(z0));
+  }
+  bf16x8_t f0a[FM], f0b[FN], f1a[FM], f1b[FN];
+  // read q (0..7) of sub-step KK's fragments of stage ST into set B
+  auto rd1 = [&](auto kkc, auto stc, auto bc, int q) {
+    constexpr int KK = decltype(kkc)::value, ST = decltype(stc)::value, B = decltype(bc)::value;
+    constexpr int SO = ST * 32768;
+#define SPH_W1_READ(FA, FB)                            \
+    switch (q) {                                       \
+      case 0: w1_read<SO + 0>(FA[0], adA[KK]); break;      \
+      case 1: w1_read<SO + 0>(FB[0], adB[KK]); break;      \
+      case 2: w1_read<SO + 4096>(FA[1], adA[KK]); break;   \
+      case 3: w1_read<SO + 4096>(FB[1], adB[KK]); break;   \
+      case 4: w1_read<SO + 8192>(FA[2], adA[KK]); break;   \
+      case 5: w1_read<SO + 8192>(FB[2], adB[KK]); break;   \
+      case 6: w1_read<SO + 12288>(FA[3], adA[KK]); break;  \
+      default: w1_read<SO + 12288>(FB[3], adB[KK]); break; \
+    }
+    if constexpr (B == 0) { SPH_W1_READ(f0a, f0b) } else { SPH_W1_READ(f1a, f1b) }
+#undef SPH_W1_READ
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  // the 16 MFMAs of set B, hook(t) after MFMA t
+  auto phase = [&](auto bc, auto hook) {
+    constexpr int B = decltype(bc)::value;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int i = t >> 2, j = t & 3;
+      if constexpr (B == 0) w1_mfma(acc[i][j], f0a[i], f0b[j]);
+      else w1_mfma(acc[i][j], f1a[i], f1b[j]);
+      hook(t);
+    }
+    if constexpr (B == 0)
+      asm volatile("" :: "v"(f0a[0]), "v"(f0a[1]), "v"(f0a[2]), "v"(f0a[3]), "v"(f0b[0]), "v"(f0b[1]), "v"(f0b[2]), "v"(f0b[3]));
+    else
+      asm volatile("" :: "v"(f1a[0]), "v"(f1a[1]), "v"(f1a[2]), "v"(f1a[3]), "v"(f1b[0]), "v"(f1b[1]), "v"(f1b[2]), "v"(f1b[3]));
+  };
+  auto step = [&](auto stc, int s) {
+    constexpr int ST = decltype(stc)::value;
+    using STc = std::integral_constant<int, ST>;
+    using SNc = std::integral_constant<int, ST ^ 1>;
+    const int s2 = min(s + 2, S - 1);
+    w1_wait_lds();
+    phase(I0{}, [&](int t) { if (t < 8) rd1(I1{}, STc{}, I1{}, t); });
+    w1_wait_lds();
+    phase(I1{}, [&](int t) { if (t < 8) rd1(I2{}, STc{}, I0{}, t); });
+    w1_wait_lds();
+    phase(I0{}, [&](int t) {
+      if (t < 8) rd1(I3{}, STc{}, I1{}, t);
+      if (t == kW1Barrier - 1) {
+        // this wave's reads of the stage and copies for the next step are done
+        w1_wait_lds();
+        w1_wait_mem();
+        __builtin_amdgcn_s_barrier();
+      }
+    });
+    w1_wait_lds();
+    phase(I1{}, [&](int t) {
+      if (t < 8) rd1(I0{}, SNc{}, I0{}, t);
+      copy1(t, s2, ST);
+    });
+  };
+#pragma unroll
+  for (int i = 0; i < A_INS + B_INS; ++i) copy1(i, 0, 0);
+#pragma unroll
+  for (int i = 0; i < A_INS + B_INS; ++i) copy1(i, 1, 1);
+  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // step 0 has landed
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < 8; ++q) rd1(I0{}, I0{}, I0{}, q);
+  for (int s = 0; s < S; s += 2) {
+    step(I0{}, s);
+    step(I1{}, s + 1);
+  }
+  // the last copies (into stages nobody reads) and reads land before the
+  // LDS is given up; the last MFMAs' results are written before the AGPRs
+  // are read
+  w1_wait_mem();
+  w1_wait_lds();
+  asm volatile("s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
+
+  // Epilogue: each fragment leaves the AGPRs on its own (the generic tile
+  // epilogue, which reads all 256 accumulators, spilled); z and the tile's
+  // row maxima of |clamp(z)| as there.
+  constexpr int P = FM * 16;
+  float red[P];
+#pragma unroll
+  for (int t = 0; t < P; ++t) red[t] = 0.0f;
+  const float clip = a.clip;
+  if (m0 + BM <= M && n0 + BN <= n && n <= (1 << 27) && !a.bias) {
+    uint32_t loff = ((uint32_t)(lane >> 5) * 4u * (uint32_t)n + (uint32_t)(lane & 31)) * 4u;
+    asm volatile("" : "+v"(loff));
+    const int row0 = __builtin_amdgcn_readfirstlane(m0 + wm * TM);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        f32x16_t v;
+        asm volatile("; fragment out of the AGPRs" : "=v"(v) : "0"(acc[i][j]));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = row0 + i * 32 + 8 * (r >> 2) + (r & 3);
+          const uint8_t* rb = scalar_ptr(a.z + (int64_t)row * n + n0 + wn * TN);
+          __builtin_nontemporal_store(v[r], (__attribute__((address_space(1))) float*)(rb + loff + j * 128));
+          red[i * 16 + r] = fmaxf(red[i * 16 + r], fminf(fabsf(v[r]), clip));
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        f32x16_t v;
+        asm volatile("; fragment out of the AGPRs" : "=v"(v) : "0"(acc[i][j]));
+        const int lcol = wn * TN + j * 32 + (lane & 31);
+        const int col = n0 + lcol;
+        const float cb = a.bias ? a.bias[s_ids[lcol]] : 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < M && col < n) {
+            const float zv = a.bias ? v[r] + cb : v[r];
+            __builtin_nontemporal_store(zv, a.z + (int64_t)row * n + col);
+            red[i * 16 + r] = fmaxf(red[i * 16 + r], fabsf(fminf(fmaxf(zv, -clip), clip)));
+          }
+        }
+      }
+    }
+  }
+  half_wave_max_transpose<P>(red, lane);
+  constexpr int PER = P / 32;
+#pragma unroll
+  for (int t = 0; t < PER; ++t) {
+    const int idx = (lane & 31) * PER + t;
+    const int i = idx / 16, r = idx % 16;
+    const int lrow = wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    atomicMax(&s_rmax[lrow], __float_as_uint(red[t]));
+  }
+  __syncthreads();
+  for (int i = tid; i < BM; i += NT)
+    if (m0 + i < M) a.amax_part[(int64_t)(m0 + i) * kMaxBlocks + nt] = __uint_as_float(s_rmax[i]);
+#endif
+}
+
 // Direct-to-LDS variant for fp8 E4M3 weights (K a multiple of 64).  The A
 // tile is staged as above; the B tile keeps its bytes: a weight row holds 64
 // codes per K step (64 bytes, four 16-byte chunks), and a wave instruction
@@ -1322,6 +1574,17 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
       return hipGetLastError();
     }
   } else if (a.K % kBK == 0) {
+    if constexpr (BM == 256 && WT == 0 && EPI == kEpiCloud) {
+      if (o32 && (a.K / kBK) % 2 == 0) {
+        // one wave per SIMD (an even number of K steps)
+        static std::atomic<uint64_t> lds_set_w1{0};
+        constexpr size_t lds_w = mfma_dma_lds_bytes<BM, BN>();
+        hipError_t e = set_lds_limit_once(lds_set_w1, reinterpret_cast<const void*>(k_mfma_w1<EPI>), lds_w);
+        if (e != hipSuccess) return e;
+        launch_kernel(k_mfma_w1<EPI>, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_w, s, a);
+        return hipGetLastError();
+      }
+    }
     auto kd = WT == 0 ? (o32 ? k_mfma_dma<BM, BN, WM, WN, EPI, true> : k_mfma_dma<BM, BN, WM, WN, EPI, false>)
                       : (o32 ? k_mfma_dma8<BM, BN, WM, WN, EPI, true> : k_mfma_dma8<BM, BN, WM, WN, EPI, false>);
     constexpr size_t lds_d = WT == 0 ? mfma_dma_lds_bytes<BM, BN>() : mfma_dma8_lds_bytes<BM, BN>();
