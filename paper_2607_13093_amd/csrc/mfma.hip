@@ -741,8 +741,9 @@ void k_mfma_dma(const MfmaArgs a) {
 // reads go out after its first 8 MFMAs, and the step barrier comes after the
 // 12th MFMA of the third sub-step, so the rest of the step's MFMAs cover the
 // barrier and the next stage's first reads.  The copies for two steps ahead
-// are issued in the last sub-step (past the end they copy the last step again:
-// in-bounds reads into a stage nobody reads), which keeps the K loop
+// go out in halves, in the last sub-step and the next step's first (past the
+// end they copy the last step again: in-bounds reads into a stage nobody
+// reads; halving them ran dense_sub 2.5% faster), which keeps the K loop
 // straight-line code: with a branch in it the compiler spilled registers that
 // reads still in flight were to fill.  Because the compiler sees neither the
 // asm reads nor the MFMAs, every wait is explicit (lgkmcnt before a sub-step's
@@ -878,9 +879,14 @@ void k_mfma_w1(const MfmaArgs a) {
     constexpr int ST = decltype(stc)::value;
     using STc = std::integral_constant<int, ST>;
     using SNc = std::integral_constant<int, ST ^ 1>;
-    const int s2 = min(s + 2, S - 1);
+    const int s1 = min(s + 1, S - 1), s2 = min(s + 2, S - 1);
     w1_wait_lds();
-    phase(I0{}, [&](int t) { if (t < 8) rd1(I1{}, STc{}, I1{}, t); });
+    phase(I0{}, [&](int t) {
+      if (t < 8) rd1(I1{}, STc{}, I1{}, t);
+      // the second half of the copies for the next step (the first half went
+      // out in the previous step's last sub-step; the prologue copies step 1 whole)
+      if (s > 0 && t < 8) copy1(8 + t, s1, ST ^ 1);
+    });
     w1_wait_lds();
     phase(I1{}, [&](int t) { if (t < 8) rd1(I2{}, STc{}, I0{}, t); });
     w1_wait_lds();
@@ -895,8 +901,10 @@ void k_mfma_w1(const MfmaArgs a) {
     });
     w1_wait_lds();
     phase(I1{}, [&](int t) {
-      if (t < 8) rd1(I0{}, SNc{}, I0{}, t);
-      copy1(t, s2, ST);
+      if (t < 8) {
+        rd1(I0{}, SNc{}, I0{}, t);
+        copy1(t, s2, ST);
+      }
     });
   };
 #pragma unroll
