@@ -739,8 +739,9 @@ void k_mfma_dma(const MfmaArgs a) {
 // reads are inline asm (their order is kept as written), each sub-step's 16
 // MFMAs run on one of two fragment register sets while the next sub-step's 8
 // reads go out after its first 8 MFMAs, and the step barrier comes after the
-// 12th MFMA of the third sub-step, so the rest of the step's MFMAs cover the
-// barrier and the next stage's first reads.  The copies for two steps ahead
+// 14th MFMA of the third sub-step, so the rest of the step's MFMAs cover the
+// barrier and the next stage's first reads (after the 8th: 2% slower; 10th,
+// 12th, 16th: within 1.5%).  The copies for two steps ahead
 // go out in halves, in the last sub-step and the next step's first (past the
 // end they copy the last step again: in-bounds reads into a stage nobody
 // reads; halving them ran dense_sub 2.5% faster), which keeps the K loop
@@ -760,7 +761,7 @@ __device__ __forceinline__ void w1_wait_lds() { asm volatile("s_waitcnt lgkmcnt(
 __device__ __forceinline__ void w1_wait_mem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 typedef __attribute__((address_space(3))) const char* lds_cptr_t;
 
-constexpr int kW1Barrier = 12;  // the step barrier follows this many MFMAs of the third sub-step
+constexpr int kW1Barrier = 14;  // the step barrier follows this many MFMAs of the third sub-step
 
 template <int EPI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
