@@ -736,20 +736,20 @@ void k_mfma_dma(const MfmaArgs a) {
 // sub-step a wave reads 8 fragments for 16 MFMAs, where the two-wave kernel
 // reads 6 for 8, so the LDS traffic per flop drops by a third.  With no second
 // wave on the SIMD the schedule is explicit: the MFMAs and the LDS fragment
-// reads are inline asm (their order is kept as written), each sub-step's 16
-// MFMAs run on one of two fragment register sets while the next sub-step's 8
-// reads go out after its first 8 MFMAs, and the step barrier comes after the
-// 14th MFMA of the third sub-step, so the rest of the step's MFMAs cover the
-// barrier and the next stage's first reads (after the 8th: 2% slower; 10th,
-// 12th, 16th: within 1.5%).  The copies for two steps ahead
-// go out in halves, in the last sub-step and the next step's first (past the
-// end they copy the last step again: in-bounds reads into a stage nobody
-// reads; halving them ran dense_sub 2.5% faster), which keeps the K loop
-// straight-line code: with a branch in it the compiler spilled registers that
-// reads still in flight were to fill.  Because the compiler sees neither the
-// asm reads nor the MFMAs, every wait is explicit (lgkmcnt before a sub-step's
-// MFMAs, vmcnt before the barrier) and each sub-step's fragments are kept
-// allocated to its end.
+// reads are inline asm (their order is kept as written).  Four fragment
+// register sets, one per sub-step: while a sub-step's 16 MFMAs issue, the
+// reads for the sub-step two ahead go out after its first 8 MFMAs, into the
+// set the MFMAs of two sub-steps ago used.  One barrier per step, between the
+// second and third sub-steps: the third and fourth then read the next stage
+// and copy the step after next into this one (8 copies each).  Past the end
+// the copies repeat the last step (in-bounds reads into a stage nobody reads),
+// so the K loop is straight-line code: with a branch in it the compiler
+// spilled registers that reads still in flight were to fill.  The compiler
+// sees neither the asm reads nor the MFMAs, so every wait is explicit
+// (lgkmcnt before each sub-step's MFMAs, vmcnt and lgkmcnt before the
+// barrier), and each sub-step's fragments stay allocated to its end.
+// Measured (harness, dense_full / dense_sub): reads one sub-step ahead with
+// two sets 3397 / 1022 us, two ahead with four sets 3300 / 970 us.
 __device__ __forceinline__ void w1_mfma(f32x16_t& c, const bf16x8_t& a, const bf16x8_t& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
 }
@@ -758,10 +758,11 @@ __device__ __forceinline__ void w1_read(bf16x8_t& d, uint32_t addr) {
   asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(addr), "i"(OFF));
 }
 __device__ __forceinline__ void w1_wait_lds() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// the older of two groups of 8 reads (LDS reads complete in order)
+__device__ __forceinline__ void w1_wait_lds8() { asm volatile("s_waitcnt lgkmcnt(8)" ::: "memory"); }
 __device__ __forceinline__ void w1_wait_mem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 typedef __attribute__((address_space(3))) const char* lds_cptr_t;
 
-constexpr int kW1Barrier = 14;  // the step barrier follows this many MFMAs of the third sub-step
 
 template <int EPI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
@@ -838,7 +839,7 @@ void k_mfma_w1(const MfmaArgs a) {
 #pragma unroll
       for (int j = 0; j < FN; ++j) asm volatile("; zero accumulators" : "=a"(acc[i][j]) : "0"(z0));
   }
-  bf16x8_t f0a[FM], f0b[FN], f1a[FM], f1b[FN];
+  bf16x8_t f0a[FM], f0b[FN], f1a[FM], f1b[FN], f2a[FM], f2b[FN], f3a[FM], f3b[FN];
   // read q (0..7) of sub-step KK's fragments of stage ST into set B
   auto rd1 = [&](auto kkc, auto stc, auto bc, int q) {
     constexpr int KK = decltype(kkc)::value, ST = decltype(stc)::value, B = decltype(bc)::value;
@@ -854,57 +855,61 @@ void k_mfma_w1(const MfmaArgs a) {
       case 6: w1_read<SO + 12288>(FA[3], adA[KK]); break;  \
       default: w1_read<SO + 12288>(FB[3], adB[KK]); break; \
     }
-    if constexpr (B == 0) { SPH_W1_READ(f0a, f0b) } else { SPH_W1_READ(f1a, f1b) }
+    if constexpr (B == 0) { SPH_W1_READ(f0a, f0b) }
+    else if constexpr (B == 1) { SPH_W1_READ(f1a, f1b) }
+    else if constexpr (B == 2) { SPH_W1_READ(f2a, f2b) }
+    else { SPH_W1_READ(f3a, f3b) }
 #undef SPH_W1_READ
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
-  // the 16 MFMAs of set B, hook(t) after MFMA t
+  // the 16 MFMAs of set B, hook(t) after MFMA t; the set stays allocated to the end
   auto phase = [&](auto bc, auto hook) {
     constexpr int B = decltype(bc)::value;
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       const int i = t >> 2, j = t & 3;
       if constexpr (B == 0) w1_mfma(acc[i][j], f0a[i], f0b[j]);
-      else w1_mfma(acc[i][j], f1a[i], f1b[j]);
+      else if constexpr (B == 1) w1_mfma(acc[i][j], f1a[i], f1b[j]);
+      else if constexpr (B == 2) w1_mfma(acc[i][j], f2a[i], f2b[j]);
+      else w1_mfma(acc[i][j], f3a[i], f3b[j]);
       hook(t);
     }
     if constexpr (B == 0)
       asm volatile("" :: "v"(f0a[0]), "v"(f0a[1]), "v"(f0a[2]), "v"(f0a[3]), "v"(f0b[0]), "v"(f0b[1]), "v"(f0b[2]), "v"(f0b[3]));
-    else
+    else if constexpr (B == 1)
       asm volatile("" :: "v"(f1a[0]), "v"(f1a[1]), "v"(f1a[2]), "v"(f1a[3]), "v"(f1b[0]), "v"(f1b[1]), "v"(f1b[2]), "v"(f1b[3]));
+    else if constexpr (B == 2)
+      asm volatile("" :: "v"(f2a[0]), "v"(f2a[1]), "v"(f2a[2]), "v"(f2a[3]), "v"(f2b[0]), "v"(f2b[1]), "v"(f2b[2]), "v"(f2b[3]));
+    else
+      asm volatile("" :: "v"(f3a[0]), "v"(f3a[1]), "v"(f3a[2]), "v"(f3a[3]), "v"(f3b[0]), "v"(f3b[1]), "v"(f3b[2]), "v"(f3b[3]));
   };
   auto step = [&](auto stc, int s) {
     constexpr int ST = decltype(stc)::value;
     using STc = std::integral_constant<int, ST>;
     using SNc = std::integral_constant<int, ST ^ 1>;
-    const int s1 = min(s + 1, S - 1), s2 = min(s + 2, S - 1);
+    const int s2 = min(s + 2, S - 1);
+    w1_wait_lds8();
+    phase(I0{}, [&](int t) { if (t < 8) rd1(I2{}, STc{}, I2{}, t); });
+    w1_wait_lds8();
+    phase(I1{}, [&](int t) { if (t < 8) rd1(I3{}, STc{}, I3{}, t); });
+    // this wave's reads of the stage and copies for the next step are done
     w1_wait_lds();
-    phase(I0{}, [&](int t) {
-      if (t < 8) rd1(I1{}, STc{}, I1{}, t);
-      // the second half of the copies for the next step (the first half went
-      // out in the previous step's last sub-step; the prologue copies step 1 whole)
-      if (s > 0 && t < 8) copy1(8 + t, s1, ST ^ 1);
-    });
-    w1_wait_lds();
-    phase(I1{}, [&](int t) { if (t < 8) rd1(I2{}, STc{}, I0{}, t); });
-    w1_wait_lds();
-    phase(I0{}, [&](int t) {
-      if (t < 8) rd1(I3{}, STc{}, I1{}, t);
-      if (t == kW1Barrier - 1) {
-        // this wave's reads of the stage and copies for the next step are done
-        w1_wait_lds();
-        w1_wait_mem();
-        __builtin_amdgcn_s_barrier();
-      }
-    });
-    w1_wait_lds();
-    phase(I1{}, [&](int t) {
+    w1_wait_mem();
+    __builtin_amdgcn_s_barrier();
+    phase(I2{}, [&](int t) {
       if (t < 8) {
         rd1(I0{}, SNc{}, I0{}, t);
         copy1(t, s2, ST);
+      }
+    });
+    w1_wait_lds8();
+    phase(I3{}, [&](int t) {
+      if (t < 8) {
+        rd1(I1{}, SNc{}, I1{}, t);
+        copy1(8 + t, s2, ST);
       }
     });
   };
@@ -916,6 +921,8 @@ void k_mfma_w1(const MfmaArgs a) {
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < 8; ++q) rd1(I0{}, I0{}, I0{}, q);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) rd1(I1{}, I0{}, I1{}, q);
   for (int s = 0; s < S; s += 2) {
     step(I0{}, s);
     step(I1{}, s + 1);
