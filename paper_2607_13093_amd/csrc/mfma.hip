@@ -764,29 +764,41 @@ __device__ __forceinline__ void w1_wait_mem() { asm volatile("s_waitcnt vmcnt(0)
 typedef __attribute__((address_space(3))) const char* lds_cptr_t;
 
 
-template <int EPI>
+// NB weight stages: 2 (an even number of K steps; 128 KB of LDS), or 3 (a
+// multiple of 6 steps; all 160 KB of LDS: the weight copies go out three
+// steps ahead instead of two, and the ids and row maxima live outside the
+// stages: ids are read from global memory, the row maxima take the first
+// stage after the K loop).  Three stages: dense_full 3300 -> 3250 us,
+// dense_sub 996 -> 970 us (harness).
+template <int EPI, int NB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_mfma_w1(const MfmaArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
   static_assert(EPI == kEpiCloud, "cloud epilogue only");
+  static_assert(NB == 2 || NB == 3, "two or three weight stages");
   constexpr int BM = 256, BN = 256, NT = 256, WN = 2, TM = 128, TN = 128, FM = 4, FN = 4;
   constexpr int A_INS = BM / 8 / 4, B_INS = BN / 8 / 4;  // 8 + 8 copies per wave per step
+  constexpr int SB = BN * kBK * 2;                        // bytes of a stage (32 KB)
   extern __shared__ __align__(16) uint8_t smem[];
-  uint16_t* As = reinterpret_cast<uint16_t*>(smem);  // [2][256][64]
-  uint16_t* Bs = As + 2 * BM * kBK;                   // [2][256][64]
-  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + 2 * BN * kBK);
-  uint32_t* s_rmax = reinterpret_cast<uint32_t*>(s_ids + BN);
+  uint8_t* As = smem;                                     // [2][256][128 B]
+  uint8_t* Bs = smem + 2 * SB;                            // [NB][256][128 B]
+  // ids and row maxima: after the stages (NB = 2), or none / the first stage
+  // once the K loop is done (NB = 3)
+  int32_t* s_ids = reinterpret_cast<int32_t*>(Bs + NB * SB);
+  uint32_t* s_rmax = NB == 2 ? reinterpret_cast<uint32_t*>(s_ids + BN) : reinterpret_cast<uint32_t*>(smem);
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   int mt, nt;
   tile_of_block(blockIdx.x, a.m_tiles, a.n_tiles, mt, nt);
   const int m0 = mt * BM, n0 = nt * BN;
   const int M = a.M, K = a.K, n = a.n;
-  const int S = K / kBK;  // even and at least 2 (the launcher's condition)
+  const int S = K / kBK;  // a multiple of 2 (NB = 2) or 6 (NB = 3): the launcher's condition
   const int last_id = a.ids[min(n, n0 + BN) - 1];
-  for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
-  for (int i = tid; i < BM; i += NT) s_rmax[i] = 0u;
-  __syncthreads();
+  if constexpr (NB == 2) {
+    for (int i = tid; i < BN; i += NT) s_ids[i] = n0 + i < n ? a.ids[n0 + i] : last_id;
+    for (int i = tid; i < BM; i += NT) s_rmax[i] = 0u;
+    __syncthreads();
+  }
 
   const int lr = lane >> 3;
   const uint8_t* hbase = reinterpret_cast<const uint8_t*>(a.h);
@@ -801,23 +813,23 @@ void k_mfma_w1(const MfmaArgs a) {
   for (int i = 0; i < B_INS; ++i) {
     const int r = (wave * B_INS + i) * 8 + lr;
     const int lc = (lane & 7) ^ swz8(r);
-    pb[i].set(a.w, (int64_t)s_ids[r] * a.ldw_bytes + lc * 16);
+    const int id = NB == 2 ? s_ids[r] : (n0 + r < n ? a.ids[n0 + r] : last_id);
+    pb[i].set(a.w, (int64_t)id * a.ldw_bytes + lc * 16);
   }
-  // copy i (0..15) of this wave's share of step s into stage st
-  auto copy1 = [&](int i, int s, int st) {
+  // copy i (0..7) of this wave's share of step s into stage st
+  auto copyA = [&](int i, int s, int st) {
     const int64_t step = (int64_t)s * kBK * 2;
-    if (i < A_INS) {
-      uint8_t* as = reinterpret_cast<uint8_t*>(As) + st * BM * kBK * 2;
-      pa[i].copy(scalar_ptr(hbase + step), step, (lds_void_t*)(as + (wave * A_INS + i) * 1024));
-    } else {
-      uint8_t* bs = reinterpret_cast<uint8_t*>(Bs) + st * BN * kBK * 2;
-      pb[i - A_INS].copy(scalar_ptr(a.w + step), step, (lds_void_t*)(bs + (wave * B_INS + i - A_INS) * 1024));
-    }
+    pa[i].copy(scalar_ptr(hbase + step), step, (lds_void_t*)(As + st * SB + (wave * A_INS + i) * 1024));
+  };
+  auto copyB = [&](int i, int s, int st) {
+    const int64_t step = (int64_t)s * kBK * 2;
+    pb[i].copy(scalar_ptr(a.w + step), step, (lds_void_t*)(Bs + st * SB + (wave * B_INS + i) * 1024));
   };
   // fragment reads: row (lane & 31) of a fragment, 16-byte chunk 2 kk + lane / 32
   // (swizzled); the fragments of a wave are 32 rows (4 KB) apart and the
-  // stages 32 KB apart, both immediate offsets of the read
-  uint32_t adA[4], adB[4];
+  // stages 32 KB apart, both immediate offsets of the read (the third weight
+  // stage, past the 16-bit offset field, has base addresses of its own)
+  uint32_t adA[4], adB[4], adB2[4];
   {
     const int sw = swz8(lane & 31);  // rows 32 apart share the swizzle
     const uint32_t baseA = (uint32_t)(uintptr_t)(lds_cptr_t)As + (uint32_t)((wm * TM + (lane & 31)) * 128);
@@ -827,6 +839,7 @@ void k_mfma_w1(const MfmaArgs a) {
       const uint32_t c = (uint32_t)(((kk * 2 + (lane >> 5)) ^ sw) << 4);
       adA[kk] = baseA + c;
       adB[kk] = baseB + c;
+      adB2[kk] = baseB + 2u * SB + c;
     }
   }
   f32x16_t acc[FM][FN];
@@ -840,20 +853,22 @@ void k_mfma_w1(const MfmaArgs a) {
       for (int j = 0; j < FN; ++j) asm volatile("; zero accumulators" : "=a"(acc[i][j]) : "0"(z0));
   }
   bf16x8_t f0a[FM], f0b[FN], f1a[FM], f1b[FN], f2a[FM], f2b[FN], f3a[FM], f3b[FN];
-  // read q (0..7) of sub-step KK's fragments of stage ST into set B
-  auto rd1 = [&](auto kkc, auto stc, auto bc, int q) {
-    constexpr int KK = decltype(kkc)::value, ST = decltype(stc)::value, B = decltype(bc)::value;
-    constexpr int SO = ST * 32768;
-#define SPH_W1_READ(FA, FB)                            \
-    switch (q) {                                       \
-      case 0: w1_read<SO + 0>(FA[0], adA[KK]); break;      \
-      case 1: w1_read<SO + 0>(FB[0], adB[KK]); break;      \
-      case 2: w1_read<SO + 4096>(FA[1], adA[KK]); break;   \
-      case 3: w1_read<SO + 4096>(FB[1], adB[KK]); break;   \
-      case 4: w1_read<SO + 8192>(FA[2], adA[KK]); break;   \
-      case 5: w1_read<SO + 8192>(FB[2], adB[KK]); break;   \
-      case 6: w1_read<SO + 12288>(FA[3], adA[KK]); break;  \
-      default: w1_read<SO + 12288>(FB[3], adB[KK]); break; \
+  // read q (0..7) of sub-step KK's fragments (A stage SA, weight stage SW) into set B
+  auto rd1 = [&](auto kkc, auto sac, auto swc, auto bc, int q) {
+    constexpr int KK = decltype(kkc)::value, SA = decltype(sac)::value, SW = decltype(swc)::value;
+    constexpr int B = decltype(bc)::value;
+    constexpr int OA = SA * SB, OB = SW == 2 ? 0 : SW * SB;
+    const uint32_t ab = SW == 2 ? adB2[KK] : adB[KK];
+#define SPH_W1_READ(FA, FB)                             \
+    switch (q) {                                        \
+      case 0: w1_read<OA + 0>(FA[0], adA[KK]); break;     \
+      case 1: w1_read<OB + 0>(FB[0], ab); break;          \
+      case 2: w1_read<OA + 4096>(FA[1], adA[KK]); break;  \
+      case 3: w1_read<OB + 4096>(FB[1], ab); break;       \
+      case 4: w1_read<OA + 8192>(FA[2], adA[KK]); break;  \
+      case 5: w1_read<OB + 8192>(FB[2], ab); break;       \
+      case 6: w1_read<OA + 12288>(FA[3], adA[KK]); break; \
+      default: w1_read<OB + 12288>(FB[3], ab); break;     \
     }
     if constexpr (B == 0) { SPH_W1_READ(f0a, f0b) }
     else if constexpr (B == 1) { SPH_W1_READ(f1a, f1b) }
@@ -886,46 +901,76 @@ void k_mfma_w1(const MfmaArgs a) {
     else
       asm volatile("" :: "v"(f3a[0]), "v"(f3a[1]), "v"(f3a[2]), "v"(f3a[3]), "v"(f3b[0]), "v"(f3b[1]), "v"(f3b[2]), "v"(f3b[3]));
   };
-  auto step = [&](auto stc, int s) {
-    constexpr int ST = decltype(stc)::value;
-    using STc = std::integral_constant<int, ST>;
-    using SNc = std::integral_constant<int, ST ^ 1>;
-    const int s2 = min(s + 2, S - 1);
+  // step s, with h stage SA = s % 2 and weight stage SW = s % NB: the weights
+  // for step s + NB and h for step s + 2 are copied into this step's stages
+  // after the barrier (past the end: the last step again)
+  auto step = [&](auto sac, auto swc, int s) {
+    constexpr int SA = decltype(sac)::value, SW = decltype(swc)::value;
+    using SAc = std::integral_constant<int, SA>;
+    using SWc = std::integral_constant<int, SW>;
+    using SAn = std::integral_constant<int, SA ^ 1>;
+    using SWn = std::integral_constant<int, (SW + 1) % NB>;
+    const int sa = min(s + 2, S - 1), sw = min(s + NB, S - 1);
     w1_wait_lds8();
-    phase(I0{}, [&](int t) { if (t < 8) rd1(I2{}, STc{}, I2{}, t); });
+    phase(I0{}, [&](int t) { if (t < 8) rd1(I2{}, SAc{}, SWc{}, I2{}, t); });
     w1_wait_lds8();
-    phase(I1{}, [&](int t) { if (t < 8) rd1(I3{}, STc{}, I3{}, t); });
-    // this wave's reads of the stage and copies for the next step are done
+    phase(I1{}, [&](int t) { if (t < 8) rd1(I3{}, SAc{}, SWc{}, I3{}, t); });
+    // this wave's reads of the stages are done, and its copies for the next
+    // step have landed (with three weight stages the newest 8, the weights of
+    // step s + 2, may still be in flight)
     w1_wait_lds();
-    w1_wait_mem();
+    if constexpr (NB == 2) w1_wait_mem();
+    else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     phase(I2{}, [&](int t) {
       if (t < 8) {
-        rd1(I0{}, SNc{}, I0{}, t);
-        copy1(t, s2, ST);
+        rd1(I0{}, SAn{}, SWn{}, I0{}, t);
+        copyA(t, sa, SA);
       }
     });
     w1_wait_lds8();
     phase(I3{}, [&](int t) {
       if (t < 8) {
-        rd1(I1{}, SNc{}, I1{}, t);
-        copy1(8 + t, s2, ST);
+        rd1(I1{}, SAn{}, SWn{}, I1{}, t);
+        copyB(t, sw, SW);
       }
     });
   };
+  // prologue: h steps 0 and 1, weight steps 0 .. NB - 1; steps 0 land first
 #pragma unroll
-  for (int i = 0; i < A_INS + B_INS; ++i) copy1(i, 0, 0);
+  for (int i = 0; i < A_INS; ++i) copyA(i, 0, 0);
 #pragma unroll
-  for (int i = 0; i < A_INS + B_INS; ++i) copy1(i, 1, 1);
-  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");  // step 0 has landed
+  for (int i = 0; i < B_INS; ++i) copyB(i, 0, 0);
+#pragma unroll
+  for (int i = 0; i < A_INS; ++i) copyA(i, 1, 1);
+#pragma unroll
+  for (int i = 0; i < B_INS; ++i) copyB(i, 1, 1);
+  if constexpr (NB == 3) {
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i) copyB(i, 2, 2);
+    asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+  }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < 8; ++q) rd1(I0{}, I0{}, I0{}, q);
+  for (int q = 0; q < 8; ++q) rd1(I0{}, I0{}, I0{}, I0{}, q);
 #pragma unroll
-  for (int q = 0; q < 8; ++q) rd1(I1{}, I0{}, I1{}, q);
-  for (int s = 0; s < S; s += 2) {
-    step(I0{}, s);
-    step(I1{}, s + 1);
+  for (int q = 0; q < 8; ++q) rd1(I1{}, I0{}, I0{}, I1{}, q);
+  if constexpr (NB == 2) {
+    for (int s = 0; s < S; s += 2) {
+      step(I0{}, I0{}, s);
+      step(I1{}, I1{}, s + 1);
+    }
+  } else {
+    for (int s = 0; s < S; s += 6) {
+      step(I0{}, I0{}, s);
+      step(I1{}, I1{}, s + 1);
+      step(I0{}, I2{}, s + 2);
+      step(I1{}, I0{}, s + 3);
+      step(I0{}, I1{}, s + 4);
+      step(I1{}, I2{}, s + 5);
+    }
   }
   // the last copies (into stages nobody reads) and reads land before the
   // LDS is given up; the last MFMAs' results are written before the AGPRs
@@ -933,6 +978,11 @@ void k_mfma_w1(const MfmaArgs a) {
   w1_wait_mem();
   w1_wait_lds();
   asm volatile("s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7\n s_nop 7" ::: "memory");
+  if constexpr (NB == 3) {
+    __syncthreads();  // every wave is done with the stages: the row maxima take the first
+    for (int i = tid; i < BM; i += NT) s_rmax[i] = 0u;
+    __syncthreads();
+  }
 
   // Epilogue: each fragment leaves the AGPRs on its own (the generic tile
   // epilogue, which reads all 256 accumulators, spilled); z and the tile's
@@ -970,7 +1020,8 @@ void k_mfma_w1(const MfmaArgs a) {
         asm volatile("; fragment out of the AGPRs" : "=v"(v) : "0"(acc[i][j]));
         const int lcol = wn * TN + j * 32 + (lane & 31);
         const int col = n0 + lcol;
-        const float cb = a.bias ? a.bias[s_ids[lcol]] : 0.0f;
+        float cb = 0.0f;
+        if (a.bias) cb = a.bias[NB == 2 ? s_ids[lcol] : (col < n ? a.ids[col] : last_id)];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = m0 + wm * TM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -1591,13 +1642,22 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
     }
   } else if (a.K % kBK == 0) {
     if constexpr (BM == 256 && WT == 0 && EPI == kEpiCloud) {
+      if (o32 && (a.K / kBK) % 6 == 0) {
+        // one wave per SIMD, three weight stages (all 160 KB of LDS)
+        static std::atomic<uint64_t> lds_set_w3{0};
+        constexpr size_t lds_w = (size_t)5 * BM * kBK * 2;
+        hipError_t e = set_lds_limit_once(lds_set_w3, reinterpret_cast<const void*>(k_mfma_w1<EPI, 3>), lds_w);
+        if (e != hipSuccess) return e;
+        launch_kernel(k_mfma_w1<EPI, 3>, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_w, s, a);
+        return hipGetLastError();
+      }
       if (o32 && (a.K / kBK) % 2 == 0) {
         // one wave per SIMD (an even number of K steps)
         static std::atomic<uint64_t> lds_set_w1{0};
         constexpr size_t lds_w = mfma_dma_lds_bytes<BM, BN>();
-        hipError_t e = set_lds_limit_once(lds_set_w1, reinterpret_cast<const void*>(k_mfma_w1<EPI>), lds_w);
+        hipError_t e = set_lds_limit_once(lds_set_w1, reinterpret_cast<const void*>(k_mfma_w1<EPI, 2>), lds_w);
         if (e != hipSuccess) return e;
-        launch_kernel(k_mfma_w1<EPI>, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_w, s, a);
+        launch_kernel(k_mfma_w1<EPI, 2>, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_w, s, a);
         return hipGetLastError();
       }
     }
