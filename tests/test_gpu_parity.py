@@ -292,14 +292,16 @@ def test_fp8_cloud_partial_32_row_tiles():
 
 @pytest.mark.parametrize("wtype,sessions,rows,d", [("bf16", 32, 8, 1088), ("fp8", 32, 8, 1088),
                                                     ("bf16", 64, 5, 1088), ("fp8", 64, 5, 1088),
-                                                    ("bf16", 32, 8, 832), ("bf16", 50, 10, 832)])
+                                                    ("bf16", 32, 8, 832), ("bf16", 50, 10, 832),
+                                                    ("bf16", 32, 8, 1024)])
 def test_bias_and_weight_scales_on_whole_tiles(wtype, sessions, rows, d):
     # 256 or 320 rows fill their row tile, so every n-tile but the last lies
     # wholly inside z: the cloud epilogue's straight-line form adds the bias
     # (and, for E4M3 weights, multiplies by the row scale) once per column.
     # bf16 on 256-row tiles runs one wave per SIMD: 16 K steps (d = 1088)
     # take two weight stages, 12 (d = 832) three, whose ragged tiles read
-    # the bias ids from global memory (500 rows: a ragged row tile too)
+    # the bias ids from global memory (500 rows: a ragged row tile too);
+    # 15 steps (d = 1024) take the two-wave kernel
     cfg = Config(f"whole_tiles_{wtype}_{sessions * rows}_{d}", 37, d=d, d_end=64, vocab=6000,
                  n_sub=3001, subset_kind="choice", sessions=sessions, rows_per_session=rows,
                  wtype=wtype, with_bias=True)
