@@ -765,11 +765,15 @@ typedef __attribute__((address_space(3))) const char* lds_cptr_t;
 
 
 // NB weight stages: 2 (an even number of K steps; 128 KB of LDS), or 3 (a
-// multiple of 6 steps; all 160 KB of LDS: the weight copies go out three
-// steps ahead instead of two, and the ids and row maxima live outside the
-// stages: ids are read from global memory, the row maxima take the first
-// stage after the K loop).  Three stages: dense_full 3300 -> 3250 us,
-// dense_sub 996 -> 970 us (harness).
+// multiple of 6 steps; all 160 KB of LDS, and the ids and row maxima live
+// outside the stages: ids are read from global memory, the row maxima take
+// the first stage after the K loop).  With three, a step's first two
+// sub-steps copy the weights of two steps ahead into the stage the previous
+// step read and its last two copy h, one copy per 4 MFMAs in every sub-step,
+// so the barrier waits for all but the newest 8 copies (those weights).
+// Harness, dense_full / dense_sub: two stages 3300 / 996 us; three, weights
+// copied in the last sub-step three steps ahead, 3250 / 970 us; three with
+// the copies spread over the step 3290 -> 3257 / 1004 -> 961 us (A/B runs).
 template <int EPI, int NB>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_mfma_w1(const MfmaArgs a) {
@@ -911,10 +915,20 @@ void k_mfma_w1(const MfmaArgs a) {
     using SAn = std::integral_constant<int, SA ^ 1>;
     using SWn = std::integral_constant<int, (SW + 1) % NB>;
     const int sa = min(s + 2, S - 1), sw = min(s + NB, S - 1);
+    // three weight stages: this step's first two sub-steps copy the weights
+    // of step s + 2 (4 copies each, one per 4 MFMAs) into the stage step
+    // s - 1 read
+    constexpr int SWp = (SW + 2) % 3;
     w1_wait_lds8();
-    phase(I0{}, [&](int t) { if (t < 8) rd1(I2{}, SAc{}, SWc{}, I2{}, t); });
+    phase(I0{}, [&](int t) {
+      if (t < 8) rd1(I2{}, SAc{}, SWc{}, I2{}, t);
+      if (NB == 3 && s > 0 && (t & 3) == 1) copyB(t >> 2, sa, SWp);
+    });
     w1_wait_lds8();
-    phase(I1{}, [&](int t) { if (t < 8) rd1(I3{}, SAc{}, SWc{}, I3{}, t); });
+    phase(I1{}, [&](int t) {
+      if (t < 8) rd1(I3{}, SAc{}, SWc{}, I3{}, t);
+      if (NB == 3 && s > 0 && (t & 3) == 1) copyB(4 + (t >> 2), sa, SWp);
+    });
     // this wave's reads of the stages are done, and its copies for the next
     // step have landed (with three weight stages the newest 8, the weights of
     // step s + 2, may still be in flight)
@@ -922,19 +936,32 @@ void k_mfma_w1(const MfmaArgs a) {
     if constexpr (NB == 2) w1_wait_mem();
     else asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
     __builtin_amdgcn_s_barrier();
-    phase(I2{}, [&](int t) {
-      if (t < 8) {
-        rd1(I0{}, SAn{}, SWn{}, I0{}, t);
-        copyA(t, sa, SA);
-      }
-    });
-    w1_wait_lds8();
-    phase(I3{}, [&](int t) {
-      if (t < 8) {
-        rd1(I1{}, SAn{}, SWn{}, I1{}, t);
-        copyB(t, sw, SW);
-      }
-    });
+    if constexpr (NB == 2) {
+      phase(I2{}, [&](int t) {
+        if (t < 8) {
+          rd1(I0{}, SAn{}, SWn{}, I0{}, t);
+          copyA(t, sa, SA);
+        }
+      });
+      w1_wait_lds8();
+      phase(I3{}, [&](int t) {
+        if (t < 8) {
+          rd1(I1{}, SAn{}, SWn{}, I1{}, t);
+          copyB(t, sw, SW);
+        }
+      });
+    } else {
+      // h of step s + 2 into this step's h stage, 4 copies per sub-step
+      phase(I2{}, [&](int t) {
+        if (t < 8) rd1(I0{}, SAn{}, SWn{}, I0{}, t);
+        if ((t & 3) == 1) copyA(t >> 2, sa, SA);
+      });
+      w1_wait_lds8();
+      phase(I3{}, [&](int t) {
+        if (t < 8) rd1(I1{}, SAn{}, SWn{}, I1{}, t);
+        if ((t & 3) == 1) copyA(4 + (t >> 2), sa, SA);
+      });
+    }
   };
   // prologue: h steps 0 and 1, weight steps 0 .. NB - 1; steps 0 land first
 #pragma unroll
