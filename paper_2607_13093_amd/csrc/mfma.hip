@@ -1669,7 +1669,9 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
     }
   } else if (a.K % kBK == 0) {
     if constexpr (BM == 256 && WT == 0 && EPI == kEpiCloud) {
-      if (o32 && (a.K / kBK) % 6 == 0) {
+      // (the one-wave kernels copy their first steps unconditionally: they
+      // need at least 6 or 2 steps; a zero-width slice takes the kernel below)
+      if (o32 && a.K >= 6 * kBK && (a.K / kBK) % 6 == 0) {
         // one wave per SIMD, three weight stages (all 160 KB of LDS)
         static std::atomic<uint64_t> lds_set_w3{0};
         constexpr size_t lds_w = (size_t)5 * BM * kBK * 2;
@@ -1678,7 +1680,7 @@ static hipError_t launch_tile(MfmaArgs a, hipStream_t s) {
         launch_kernel(k_mfma_w1<EPI, 3>, dim3(a.m_tiles * a.n_tiles), dim3(256), lds_w, s, a);
         return hipGetLastError();
       }
-      if (o32 && (a.K / kBK) % 2 == 0) {
+      if (o32 && a.K >= 2 * kBK && (a.K / kBK) % 2 == 0) {
         // one wave per SIMD (an even number of K steps)
         static std::atomic<uint64_t> lds_set_w1{0};
         constexpr size_t lds_w = mfma_dma_lds_bytes<BM, BN>();

@@ -166,6 +166,10 @@ RAGGED = [
     (17, 17, 1096, 72, 9000, 4097), # 289 rows: one 320-row m-tile (8 waves), ragged n
     (24, 25, 1096, 72, 9000, 4097), # 600 rows: two 320-row m-tiles, the second ragged
     (13, 10, 2056, 8, 9000, 8193),  # 130 rows: two m-tiles, last n-tile of one column
+    # 256-row tiles at the edges of the one-wave kernel's step counts
+    (32, 8, 128, 64, 3000, 1001),   # one K step (the two-wave kernel)
+    (32, 8, 192, 64, 3000, 1001),   # two K steps (one wave, two weight stages)
+    (32, 8, 448, 64, 3000, 1001),   # six K steps (one wave, three weight stages)
     # 32-row tiles (9..32 rows, K a multiple of 64 in both calls)
     (3, 3, 1088, 64, 5000, 2501),   # 9 rows
     (4, 8, 2304, 256, 9000, 4097),  # 32 rows, ragged n
