@@ -78,3 +78,34 @@ def test_random_sampling_configuration(c):
                  temperature=c["tau"], top_p=c["top_p"],
                  philox_seed=0x2607_1309_0000_0000 + c["i"])
     run_sample_case(make_workload(cfg), tag=f"random sample {c['i']}")
+
+
+def _draw_one_wave(i, rng):
+    """bf16 shapes that the one-wave cloud kernel takes: 256-row tiles (129 to
+    256 rows, or 321 to 512) and an even number of 64-wide K steps, a multiple
+    of 6 in half of the cases (three weight stages)."""
+    while True:
+        sessions = int(rng.integers(8, 65))
+        R = int(rng.integers(4, 9))
+        M = sessions * R
+        if 129 <= M <= 256 or 321 <= M <= 512:
+            break
+    steps = int(rng.choice([6, 12, 18, 24])) if i % 2 == 0 else int(rng.choice([2, 4, 8, 10, 14, 16]))
+    d_end = int(rng.choice([0, 64, 128]))
+    n = int(rng.integers(1, 6001))
+    V = n + int(rng.integers(0, 4000))
+    bits, block = _FORMATS[int(rng.integers(0, 2))]  # per-row scales: the cloud kernel writes z
+    return dict(i=i, sessions=sessions, R=R, d=d_end + 64 * steps, d_end=d_end, V=V, n=n,
+                wtype="bf16", bits=bits, block=block, hq=False)
+
+
+_RNG_W = np.random.default_rng(2609)
+ONE_WAVE_CASES = [_draw_one_wave(i, _RNG_W) for i in range(10)]
+
+
+@pytest.mark.parametrize("c", ONE_WAVE_CASES, ids=[_id(c) for c in ONE_WAVE_CASES])
+def test_one_wave_cloud_configuration(c):
+    cfg = Config("random_one_wave", 700 + c["i"], d=c["d"], d_end=c["d_end"], vocab=c["V"],
+                 n_sub=c["n"], subset_kind="choice", sessions=c["sessions"], rows_per_session=c["R"],
+                 wtype="bf16", with_bias=bool(c["i"] % 3 == 1))
+    run_format_case(make_workload(cfg), c["bits"], c["block"], f"one-wave {_id(c)}")
