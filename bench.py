@@ -98,14 +98,17 @@ def algorithmic_bytes(cfg, n):
     return n * per_id + cfg.M * cfg.d_cloud * 2
 
 
-def attainable_peaks(dev):
+def attainable_peaks(dev, same_shape=None):
     """Attainable peaks measured in this job (best of 5 each):
     - read_gbs: the library's streaming-read probe over 1 GiB (16-byte
       non-temporal loads, as the skinny projection reads weight rows);
     - mfma_bf16_tflops: the library's MFMA probe (32x32x16 bf16 loop on random
       operands that change every iteration);
     - copy_gbs: a 1 GiB device copy (bytes read + written), vendor kernel;
-    - gemm_bf16_tflops: an 8192^3 bf16 GEMM on N(0,1) data, vendor library."""
+    - gemm_bf16_tflops: an 8192^3 bf16 GEMM on N(0,1) data, vendor library;
+    - with same_shape = (M, K, N): gemm_bf16_same_shape_tflops, the vendor
+      library's bf16 h @ W^T (bf16 output) on the projection's own shape, for
+      scale (the projection writes fp32 partials and row maxima as well)."""
     import torch
 
     import paper_2607_13093_amd as sph
@@ -142,8 +145,19 @@ def attainable_peaks(dev):
     gemm_tflops = 2.0 * n ** 3 / (best_ms(lambda: torch.matmul(a, b)) * 1e-3) / 1e12
     del a, b
     torch.cuda.empty_cache()
-    return {"read_gbs": read_gbs, "mfma_bf16_tflops": mfma_tflops, "copy_gbs": copy_gbs,
-            "gemm_bf16_tflops": gemm_tflops}
+    out = {"read_gbs": read_gbs, "mfma_bf16_tflops": mfma_tflops, "copy_gbs": copy_gbs,
+           "gemm_bf16_tflops": gemm_tflops}
+    if same_shape is not None:
+        m, k, nn = same_shape
+        a = torch.randn((m, k), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        b = (torch.randn((nn, k), generator=g, device=dev, dtype=torch.float32) / k ** 0.5).to(torch.bfloat16)
+        ms = best_ms(lambda: torch.nn.functional.linear(a, b))
+        out["gemm_bf16_same_shape"] = f"{m} x {k} x {nn}"
+        out["gemm_bf16_same_shape_ms"] = ms
+        out["gemm_bf16_same_shape_tflops"] = 2.0 * m * k * nn / (ms * 1e-3) / 1e12
+        del a, b
+        torch.cuda.empty_cache()
+    return out
 
 
 def source_digest(kernel):
@@ -562,7 +576,7 @@ def main():
     progress("attainable peaks")
     n = r["n"]
     roof = r["roof"]
-    att = attainable_peaks(dev)
+    att = attainable_peaks(dev, (cfg.M, cfg.d - cfg.d_end, n) if roof["bound"] == "mfma" else None)
     att_peak = att["read_gbs"] if roof["bound"] == "hbm" else att["mfma_bf16_tflops"]
     roof["attainable_peak"] = att_peak
     roof["frac_attainable"] = roof["achieved"] / att_peak
