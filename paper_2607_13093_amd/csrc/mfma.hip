@@ -731,7 +731,7 @@ void k_mfma_dma(const MfmaArgs a) {
 }
 
 // One wave per SIMD for the dense bf16 cloud projection (256 x 256 tiles, an
-// even number of 64-wide K steps).  Four waves, each a 128 x 128 wave tile of
+// even number, at least 2, of 64-wide K steps).  Four waves, each a 128 x 128 wave tile of
 // 4 x 4 fragments whose 256 accumulators stay in the AGPRs: per 16-wide
 // sub-step a wave reads 8 fragments for 16 MFMAs, where the two-wave kernel
 // reads 6 for 8, so the LDS traffic per flop drops by a third.  With no second
@@ -741,7 +741,8 @@ void k_mfma_dma(const MfmaArgs a) {
 // reads for the sub-step two ahead go out after its first 8 MFMAs, into the
 // set the MFMAs of two sub-steps ago used.  One barrier per step, between the
 // second and third sub-steps: the third and fourth then read the next stage
-// and copy the step after next into this one (8 copies each).  Past the end
+// and (two weight stages) copy the step after next into this one, 8 copies
+// each; three weight stages spread the copies differently (below).  Past the end
 // the copies repeat the last step (in-bounds reads into a stage nobody reads),
 // so the K loop is straight-line code: with a branch in it the compiler
 // spilled registers that reads still in flight were to fill.  The compiler
