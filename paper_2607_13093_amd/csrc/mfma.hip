@@ -1299,7 +1299,12 @@ void k_mfma_dma8(const MfmaArgs a) {
 // running compare per value) ran dense_full's endpoint projection in 358 us
 // instead of 505, dense_sub in 85 instead of 114 and batched in 29 instead
 // of 47; the 16-position layout then took dense_sub to 81 us and batched to
-// 27, with identical keys throughout.
+// 27, with identical keys throughout.  One wave per SIMD instead (the cloud
+// kernel's explicit schedule with 128 x 128 wave tiles, the payload copied in
+// place of the copies past the end) kept the keys identical but ran slower:
+// with 8 K steps a tile's prologue and epilogue weigh more than the LDS
+// traffic the larger wave tiles save (dense_full 379-396 against 350-364 us,
+// dense_sub 87 against 76).
 template <int BM, int WNN, int WMM>
 constexpr size_t fuse_dma_lds_bytes() {
   return (size_t)2 * (BM + kMfmaBN) * kBK * 2 + (size_t)kMfmaBN * 4 + (size_t)2 * BM * 4 +
